@@ -1,0 +1,187 @@
+/*
+ * ecospec_moe.h -- C ABI of the MoE verification pass on MI355X (gfx950).
+ *
+ * The library computes, for one MoE layer, what a speculative-decoding
+ * verifier must do for T draft tokens (EcoSpec, arXiv 2607.12696):
+ *   router top-k          -> moe_route_topk
+ *   expert union, Eq. 1   -> moe_expert_union
+ *   grouped SwiGLU experts streaming every activated expert's weights from
+ *   HBM once, gate-weighted combine -> moe_verify_layer
+ * and, on the host, the cost-aware draft-tree selection of Section 4.2
+ * (Eq. 7-9, Algorithm 1) -> moe_select_tree.
+ *
+ * Conventions for every call:
+ *   - Device pointers point to HIP device memory owned by the caller.  The
+ *     library never allocates or frees memory and never synchronises; all
+ *     device work is enqueued on `stream` (a hipStream_t; NULL is the null
+ *     stream).  Calls are stateless and may run concurrently on different
+ *     streams with different buffers.
+ *   - Argument errors are detected on the host before anything is enqueued
+ *     and return MOE_ERR_INVALID_ARG (or MOE_ERR_UNSUPPORTED for shapes the
+ *     kernels do not handle, MOE_ERR_WORKSPACE for a short workspace).  A
+ *     failed launch returns MOE_ERR_HIP.  Contents of device arrays are
+ *     preconditions, not checked: e.g. topk_idx entries must lie in [0, E).
+ *     A violated precondition gives unspecified results but no access
+ *     outside the buffers described here.
+ *   - Integers are int32, row-major, no padding.  bf16 values are stored as
+ *     their 16-bit patterns.
+ */
+#ifndef ECOSPEC_MOE_H
+#define ECOSPEC_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_ERR_INVALID_ARG = 1,
+    MOE_ERR_UNSUPPORTED = 2,
+    MOE_ERR_WORKSPACE = 3,
+    MOE_ERR_HIP = 4
+} moe_status_t;
+
+/* Gate-weight rule applied to the k selected router logits l_0..l_{k-1}. */
+typedef enum {
+    MOE_SCORE_SOFTMAX = 0, /* w_j = exp(l_j - max) / sum_i exp(l_i - max)        */
+    MOE_SCORE_SIGMOID = 1  /* w_j = sigmoid(l_j) / sum_i sigmoid(l_i)            */
+} moe_score_t;
+
+/* Expert weight storage.  Every matrix is stored out x in with the input
+ * (reduction) dimension contiguous: W_gate, W_up are [d_ff][d], W_down is
+ * [d][d_ff]; experts are stacked along a leading [E] dimension. */
+typedef enum {
+    MOE_W_BF16 = 0,          /* bf16 [E][N][K]                                               */
+    MOE_W_FP8_E4M3_B128 = 1, /* OCP e4m3fn codes u8 [E][N][K], fp32 scales [E][N/128][K/128];
+                                weight = e4m3fn(q[n][c]) * s[n/128][c/128]                      */
+    MOE_W_MXFP4 = 2          /* OCP MXFP4: e2m1 codes packed two per byte u8 [E][N][K/2], the
+                                low nibble holding the even K index; e8m0 scale codes u8
+                                [E][N][K/32]; weight = e2m1 * 2^(code-127)                      */
+} moe_wfmt_t;
+
+/* Draft-selection scores (Section 4.2 and the ablation of Section 5.4). */
+typedef enum {
+    MOE_SEL_COST_RATIO = 0,  /* Eq. 9:  P / (DeltaCost + eps), buffer updated (Algorithm 1) */
+    MOE_SEL_CONFIDENCE = 1,  /* P alone: the confidence-driven baseline                     */
+    MOE_SEL_GLOBAL_COST = 2, /* Eq. 10: P / (|E_traj| + eps), buffer never consulted        */
+    MOE_SEL_COST_DIFF = 3    /* P - lambda * DeltaCost                                      */
+} moe_sel_mode_t;
+
+/* Weights of one MoE layer; all pointers are device pointers.  The scale
+ * pointers are NULL for MOE_W_BF16.  The sh_* fields describe one always-on
+ * shared expert (same layout, leading dimension 1) with gate weight 1 that
+ * every token uses; all sh_* weight pointers NULL means no shared expert.
+ * Requirements: d % 64 == 0, d_ff % 32 == 0, and for FP8 d % 128 == 0 and
+ * d_ff % 128 == 0.  Each matrix must be 16-byte aligned. */
+typedef struct {
+    int fmt; /* moe_wfmt_t */
+    int d, d_ff, E;
+    const void *w_gate, *w_up, *w_down;
+    const void *s_gate, *s_up, *s_down;
+    const void *sh_gate, *sh_up, *sh_down;
+    const void *sh_s_gate, *sh_s_up, *sh_s_down;
+} moe_weights_t;
+
+/* Routing of T tokens as produced by moe_route_topk + moe_expert_union
+ * (device pointers).  Slot s = t*k + j is the j-th expert of token t. */
+typedef struct {
+    int T, k, E;
+    const int32_t *topk_idx; /* [T][k] */
+    const float *topk_w;     /* [T][k] */
+    const int32_t *counts;   /* [E]    */
+    const int32_t *union_ids;/* [E]    */
+    const int32_t *n_unique; /* [1]    */
+    const int32_t *offsets;  /* [E+1]  */
+    const int32_t *perm;     /* [T*k]  */
+} moe_routing_t;
+
+/*
+ * Router top-k (Section 1: each token goes to a top-k subset of experts;
+ * Table 13 gives k per model).
+ *   logits   [T][E] fp32, device.
+ *   topk_idx [T][k] out: for each token, the experts in routing order --
+ *            larger logit first, equal logits (-0 == +0) by lower expert
+ *            index, NaN after every number -- slot j holding rank j.
+ *   topk_w   [T][k] out: gate weights by `score`, computed in fp32.
+ * Limits: T >= 1, 1 <= E <= 1024, 1 <= k <= min(E, 64).
+ */
+moe_status_t moe_route_topk(const float *logits, int T, int E, int k, int score, int32_t *topk_idx,
+                            float *topk_w, void *stream);
+
+/*
+ * Expert union and grouping (Section 3, Eq. 1: the verifier must fetch the
+ * union of the experts routed to by all verified tokens).
+ *   topk_idx  [T][k] in (entries in [0, E)).
+ *   counts    [E]    out: slots routed to each expert.
+ *   union_ids [E]    out: experts with counts > 0 in ascending order, then -1.
+ *   n_unique  [1]    out: U, the number of distinct experts.
+ *   offsets   [E+1]  out: offsets[u] = first grouped position of union member
+ *                    u; offsets[u] = T*k for u >= U.
+ *   perm      [T*k]  out: slot at each grouped position; slots are ordered by
+ *                    (expert, slot), i.e. a stable counting sort.
+ * Limits: T >= 1, 1 <= k <= 64, 1 <= E <= 1024, T*k <= 2^24.
+ */
+moe_status_t moe_expert_union(const int32_t *topk_idx, int T, int k, int E, int32_t *counts,
+                              int32_t *union_ids, int32_t *n_unique, int32_t *offsets, int32_t *perm,
+                              void *stream);
+
+/* Bytes of device workspace moe_verify_layer needs for T tokens and top-k. */
+moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, size_t *bytes);
+
+/*
+ * MoE verification layer (Section 3; Fig. 1(a): cost grows with the number
+ * of distinct experts).  For every token t:
+ *   y[t] = sum_j topk_w[t][j] * FFN_{topk_idx[t][j]}(x[t])  (+ FFN_shared(x[t]))
+ *   FFN_e(x) = W_down[e] (silu(W_gate[e] x) * (W_up[e] x))
+ * Each distinct routed expert (and the shared one) is streamed from HBM once
+ * per call, whatever the number of tokens routed to it.
+ *   x  [T][d] bf16 in, y [T][d] bf16 out (may not alias x), device.
+ *   r  routing from moe_route_topk + moe_expert_union for the same T, k, E.
+ *   workspace: device buffer of at least moe_verify_workspace_size bytes,
+ *   256-byte aligned; its contents on entry do not matter.
+ * Arithmetic: weights decoded exactly to bf16, bf16 matrix cores with fp32
+ * accumulation, FP8 block scales applied to fp32 partial sums, the SwiGLU
+ * intermediate rounded to bf16, y rounded to bf16.  Deterministic: the same
+ * inputs give bit-identical y.
+ */
+moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
+                              void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Cost-aware draft-tree selection on the host (Section 4.2, Eq. 7-9,
+ * Algorithm 1 in the appendix; Eq. 10 of Section 5.4 for the global mode).
+ *   n       number of tree nodes; parent[n] (-1 for the root, parent ids
+ *           smaller than the child's), P[n] cumulative path probability.
+ *   pred    [n][L][K] predicted expert ids per node and layer (Eq. 4), each
+ *           in [0, E).
+ *   B0      initial buffer as a bitset [L][ceil(E/64)] uint64 (bit e of word
+ *           e/64 set = expert e of that layer already covered), or NULL.
+ *   budget  number of nodes to select (gamma); fewer if n < budget.
+ *   eps     the epsilon of Eq. 9/10; lambda weights the cost in COST_DIFF.
+ *   selected       [budget] out: node ids in pick order.
+ *   marginal_cost  [budget] out or NULL: number of (layer, expert) pairs of
+ *                  the pick's path not covered by B0 and earlier picks.
+ *   n_selected     out or NULL: number of entries written.
+ * The score of every unselected node is computed each round; ties go to the
+ * shallower node, then to the lower id, so the result is prefix-closed.
+ * Host memory only; limits: n <= 65536, L*K <= 65536, E <= 4096.
+ */
+moe_status_t moe_select_tree(int n, const int32_t *parent, const double *P, int L, int K,
+                             const int32_t *pred, int E, const uint64_t *B0, int budget, double eps,
+                             double lambda, int mode, int32_t *selected, int32_t *marginal_cost,
+                             int32_t *n_selected);
+
+/* Static description of a status code. */
+const char *moe_status_string(moe_status_t status);
+
+/* Message of the last HIP error seen by this thread (empty if none). */
+const char *moe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ECOSPEC_MOE_H */

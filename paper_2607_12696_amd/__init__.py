@@ -1,0 +1,236 @@
+"""MoE verification pass of EcoSpec (arXiv 2607.12696) on MI355X / gfx950.
+
+Thin ctypes binding of ``libecospec_moe.so`` (declared in
+``include/ecospec_moe.h``).  The functions carry the C names and only
+marshal arguments: PyTorch supplies device memory and the current HIP
+stream, and every step of the pass runs in the library's HIP kernels.  If
+the library has not been built, importing the functions that need it raises
+``ImportError``; there is no fallback.
+
+    moe_route_topk(logits, k, score)            -> (topk_idx, topk_w)
+    moe_expert_union(topk_idx, E)               -> Routing
+    moe_verify_workspace_size(weights, T, k)    -> bytes
+    moe_verify_layer(x, weights, routing)       -> y
+    moe_select_tree(parent, P, pred, E, budget) -> (selected, marginal_cost)
+    moe_verify_step(x, logits, weights, k, score) = the three device calls in order
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import threading
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libecospec_moe.so")
+
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
+MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
+MOE_W_BF16, MOE_W_FP8_E4M3_B128, MOE_W_MXFP4 = 0, 1, 2
+MOE_SEL_COST_RATIO, MOE_SEL_CONFIDENCE, MOE_SEL_GLOBAL_COST, MOE_SEL_COST_DIFF = 0, 1, 2, 3
+
+EXPORTED = ("moe_route_topk", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
+            "moe_select_tree", "moe_status_string", "moe_last_error")
+
+
+class MoeError(RuntimeError):
+    def __init__(self, fn: str, status: int, detail: str = ""):
+        self.status = status
+        super().__init__(f"{fn}: status {status} ({_status_string(status)}){': ' + detail if detail else ''}")
+
+
+class moe_weights_t(C.Structure):
+    _fields_ = [("fmt", C.c_int), ("d", C.c_int), ("d_ff", C.c_int), ("E", C.c_int)] + [
+        (n, C.c_void_p) for n in ("w_gate", "w_up", "w_down", "s_gate", "s_up", "s_down", "sh_gate", "sh_up",
+                                  "sh_down", "sh_s_gate", "sh_s_up", "sh_s_down")]
+
+
+class moe_routing_t(C.Structure):
+    _fields_ = [("T", C.c_int), ("k", C.c_int), ("E", C.c_int)] + [
+        (n, C.c_void_p) for n in ("topk_idx", "topk_w", "counts", "union_ids", "n_unique", "offsets", "perm")]
+
+
+_lock = threading.Lock()
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """The loaded library; raises ImportError if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_12696_amd.build`")
+            L = C.CDLL(LIB_PATH)
+            p, i = C.c_void_p, C.c_int
+            L.moe_route_topk.argtypes = [p, i, i, i, i, p, p, p]
+            L.moe_expert_union.argtypes = [p, i, i, i, p, p, p, p, p, p]
+            L.moe_verify_workspace_size.argtypes = [C.POINTER(moe_weights_t), i, i, C.POINTER(C.c_size_t)]
+            L.moe_verify_layer.argtypes = [p, C.POINTER(moe_weights_t), C.POINTER(moe_routing_t), p, p, C.c_size_t, p]
+            L.moe_select_tree.argtypes = [i, p, p, i, i, p, i, p, i, C.c_double, C.c_double, i, p, p, p]
+            L.moe_status_string.argtypes = [i]
+            L.moe_status_string.restype = C.c_char_p
+            L.moe_last_error.restype = C.c_char_p
+            for f in ("moe_route_topk", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
+                      "moe_select_tree"):
+                getattr(L, f).restype = i
+            _lib = L
+    return _lib
+
+
+def _status_string(s: int) -> str:
+    try:
+        return lib().moe_status_string(s).decode()
+    except ImportError:
+        return "library not loaded"
+
+
+def _check(fn: str, status: int):
+    if status != MOE_OK:
+        detail = lib().moe_last_error().decode() if status == MOE_ERR_HIP else ""
+        raise MoeError(fn, status, detail)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(t) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _dev_ptr(t, what: str) -> int:
+    if t is None:
+        return 0
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return t.data_ptr()
+
+
+# --------------------------------------------------------------------------- routing
+
+def moe_route_topk(logits, k: int, score: int, topk_idx=None, topk_w=None):
+    """Router top-k of fp32 logits [T, E] on the device -> (int32 [T, k], fp32 [T, k])."""
+    torch = _torch()
+    T, E = logits.shape
+    if logits.dtype != torch.float32:
+        raise ValueError("logits must be float32")
+    if topk_idx is None:
+        topk_idx = torch.empty(T, k, dtype=torch.int32, device=logits.device)
+    if topk_w is None:
+        topk_w = torch.empty(T, k, dtype=torch.float32, device=logits.device)
+    _check("moe_route_topk", lib().moe_route_topk(_dev_ptr(logits, "logits"), T, E, k, score,
+                                                    _dev_ptr(topk_idx, "topk_idx"), _dev_ptr(topk_w, "topk_w"),
+                                                    _stream(logits)))
+    return topk_idx, topk_w
+
+
+@dataclass
+class Routing:
+    """Device routing of T tokens: the outputs of moe_route_topk and moe_expert_union."""
+    T: int
+    k: int
+    E: int
+    topk_idx: object
+    topk_w: object
+    counts: object
+    union_ids: object
+    n_unique: object
+    offsets: object
+    perm: object
+
+    def c_struct(self) -> moe_routing_t:
+        r = moe_routing_t()
+        r.T, r.k, r.E = self.T, self.k, self.E
+        for n in ("topk_idx", "topk_w", "counts", "union_ids", "n_unique", "offsets", "perm"):
+            setattr(r, n, _dev_ptr(getattr(self, n), n))
+        return r
+
+
+def moe_expert_union(topk_idx, E: int, topk_w=None, out: Routing | None = None) -> Routing:
+    """Expert union, counts, offsets and stable grouping of topk_idx [T, k] on the device."""
+    torch = _torch()
+    T, k = topk_idx.shape
+    dev = topk_idx.device
+    if out is None:
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = Routing(T, k, E, topk_idx, topk_w, torch.empty(E, **i32), torch.empty(E, **i32),
+                      torch.empty(1, **i32), torch.empty(E + 1, **i32), torch.empty(T * k, **i32))
+    _check("moe_expert_union", lib().moe_expert_union(
+        _dev_ptr(topk_idx, "topk_idx"), T, k, E, _dev_ptr(out.counts, "counts"), _dev_ptr(out.union_ids, "union_ids"),
+        _dev_ptr(out.n_unique, "n_unique"), _dev_ptr(out.offsets, "offsets"), _dev_ptr(out.perm, "perm"),
+        _stream(topk_idx)))
+    return out
+
+
+# --------------------------------------------------------------------------- verify layer
+
+def weights_struct(w: dict) -> moe_weights_t:
+    """moe_weights_t for a layer dict (keys fmt, d, d_ff, E, gate, up, down, optional s_* and sh_*)."""
+    s = moe_weights_t()
+    s.fmt, s.d, s.d_ff = int(w["fmt"]), int(w["d"]), int(w["d_ff"])
+    s.E = int(w.get("E", w["gate"].shape[0]))
+    for name in ("gate", "up", "down"):
+        setattr(s, "w_" + name, _dev_ptr(w[name], name))
+        setattr(s, "s_" + name, _dev_ptr(w.get("s_" + name), "s_" + name))
+        setattr(s, "sh_" + name, _dev_ptr(w.get("sh_" + name), "sh_" + name))
+        setattr(s, "sh_s_" + name, _dev_ptr(w.get("sh_s_" + name), "sh_s_" + name))
+    return s
+
+
+def moe_verify_workspace_size(weights: dict, T: int, k: int) -> int:
+    n = C.c_size_t()
+    ws = weights_struct(weights)
+    _check("moe_verify_workspace_size", lib().moe_verify_workspace_size(C.byref(ws), T, k, C.byref(n)))
+    return n.value
+
+
+def moe_verify_layer(x, weights: dict, routing: Routing, y=None, workspace=None):
+    """y [T, d] bf16 = the MoE layer over the routed tokens x [T, d] bf16."""
+    torch = _torch()
+    T, d = x.shape
+    if x.dtype != torch.bfloat16:
+        raise ValueError("x must be bfloat16")
+    if y is None:
+        y = torch.empty_like(x)
+    if workspace is None:
+        workspace = torch.empty(moe_verify_workspace_size(weights, T, routing.k), dtype=torch.uint8, device=x.device)
+    ws = weights_struct(weights)
+    rs = routing.c_struct()
+    _check("moe_verify_layer", lib().moe_verify_layer(
+        _dev_ptr(x, "x"), C.byref(ws), C.byref(rs), _dev_ptr(y, "y"), _dev_ptr(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(x)))
+    return y
+
+
+def moe_verify_step(x, logits, weights: dict, k: int, score: int, workspace=None, y=None):
+    """Route, union and verify one layer: the whole hot path on the device."""
+    idx, w = moe_route_topk(logits, k, score)
+    r = moe_expert_union(idx, logits.shape[1], topk_w=w)
+    return moe_verify_layer(x, weights, r, y=y, workspace=workspace), r
+
+
+# --------------------------------------------------------------------------- selector (host)
+
+def moe_select_tree(parent, P, pred, E: int, budget: int, eps: float = 0.1, lam: float = 0.0,
+                    mode: int = MOE_SEL_COST_RATIO, B0=None):
+    """Cost-aware draft selection (Algorithm 1) on the host -> (selected, marginal_cost) int32 arrays."""
+    par = np.ascontiguousarray(parent, np.int32)
+    Pa = np.ascontiguousarray(P, np.float64)
+    pr = np.ascontiguousarray(pred, np.int32)
+    n, L, K = pr.shape
+    sel = np.zeros(max(budget, 1), np.int32)
+    cost = np.zeros(max(budget, 1), np.int32)
+    nsel = np.zeros(1, np.int32)
+    b0 = None if B0 is None else np.ascontiguousarray(B0, np.uint64)
+    _check("moe_select_tree", lib().moe_select_tree(
+        n, par.ctypes.data, Pa.ctypes.data, L, K, pr.ctypes.data, E, None if b0 is None else b0.ctypes.data,
+        budget, eps, lam, mode, sel.ctypes.data, cost.ctypes.data, nsel.ctypes.data))
+    m = int(nsel[0])
+    return sel[:m].copy(), cost[:m].copy()

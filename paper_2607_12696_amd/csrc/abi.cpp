@@ -1,0 +1,146 @@
+// C ABI of the verification pass: argument validation, workspace carve-up and
+// launch sequencing.  No allocation, no synchronisation.
+#include "ecospec_moe.h"
+
+#include <hip/hip_runtime_api.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "launch.hpp"
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+moe_status_t from_hip(hipError_t e)
+{
+    if (e == hipSuccess) return MOE_OK;
+    snprintf(g_last_error, sizeof g_last_error, "%s", hipGetErrorString(e));
+    return MOE_ERR_HIP;
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+constexpr int kMaxE = 1024;
+constexpr int kMaxK = 64;
+constexpr long kMaxSlots = 1L << 24;
+
+moe_status_t check_weights(const moe_weights_t *w)
+{
+    if (!w) return MOE_ERR_INVALID_ARG;
+    if (w->fmt < MOE_W_BF16 || w->fmt > MOE_W_MXFP4) return MOE_ERR_INVALID_ARG;
+    if (w->d < 1 || w->d_ff < 1 || w->E < 1 || w->E > kMaxE) return MOE_ERR_INVALID_ARG;
+    if (!w->w_gate || !w->w_up || !w->w_down) return MOE_ERR_INVALID_ARG;
+    if (w->fmt != MOE_W_BF16 && (!w->s_gate || !w->s_up || !w->s_down)) return MOE_ERR_INVALID_ARG;
+    const int nsh = (w->sh_gate != nullptr) + (w->sh_up != nullptr) + (w->sh_down != nullptr);
+    if (nsh != 0 && nsh != 3) return MOE_ERR_INVALID_ARG;
+    if (nsh == 3 && w->fmt != MOE_W_BF16 && (!w->sh_s_gate || !w->sh_s_up || !w->sh_s_down))
+        return MOE_ERR_INVALID_ARG;
+    // Tile shapes of the kernels: 16-row gate/up bands, 32-row down bands,
+    // 32-wide K chunks; FP8 needs whole 128x128 scale blocks.
+    if (w->d % 64 || w->d_ff % 32) return MOE_ERR_UNSUPPORTED;
+    if (w->fmt == MOE_W_FP8_E4M3_B128 && (w->d % 128 || w->d_ff % 128)) return MOE_ERR_UNSUPPORTED;
+    const void *mats[] = {w->w_gate, w->w_up, w->w_down, w->sh_gate, w->sh_up, w->sh_down};
+    for (const void *p : mats)
+        if (p && !aligned(p, 16)) return MOE_ERR_INVALID_ARG;
+    if (w->fmt == MOE_W_FP8_E4M3_B128) {
+        const void *sc[] = {w->s_gate, w->s_up, w->s_down, w->sh_s_gate, w->sh_s_up, w->sh_s_down};
+        for (const void *p : sc)
+            if (p && !aligned(p, 4)) return MOE_ERR_INVALID_ARG;
+    }
+    return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *moe_status_string(moe_status_t s)
+{
+    switch (s) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_INVALID_ARG: return "invalid argument";
+    case MOE_ERR_UNSUPPORTED: return "unsupported shape or format";
+    case MOE_ERR_WORKSPACE: return "workspace too small";
+    case MOE_ERR_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+const char *moe_last_error(void) { return g_last_error; }
+
+moe_status_t moe_route_topk(const float *logits, int T, int E, int k, int score, int32_t *topk_idx, float *topk_w,
+                            void *stream)
+{
+    if (!logits || !topk_idx || !topk_w) return MOE_ERR_INVALID_ARG;
+    if (T < 1 || E < 1 || E > kMaxE || k < 1 || k > E || k > kMaxK) return MOE_ERR_INVALID_ARG;
+    if ((long)T * E > (1L << 31) - 1 || (long)T * k > kMaxSlots) return MOE_ERR_INVALID_ARG;
+    if (score != MOE_SCORE_SOFTMAX && score != MOE_SCORE_SIGMOID) return MOE_ERR_INVALID_ARG;
+    return from_hip(ecospec::launch_route_topk(logits, T, E, k, score, topk_idx, topk_w, (hipStream_t)stream));
+}
+
+moe_status_t moe_expert_union(const int32_t *topk_idx, int T, int k, int E, int32_t *counts, int32_t *union_ids,
+                              int32_t *n_unique, int32_t *offsets, int32_t *perm, void *stream)
+{
+    if (!topk_idx || !counts || !union_ids || !n_unique || !offsets || !perm) return MOE_ERR_INVALID_ARG;
+    if (T < 1 || k < 1 || k > kMaxK || E < 1 || E > kMaxE || (long)T * k > kMaxSlots) return MOE_ERR_INVALID_ARG;
+    return from_hip(ecospec::launch_expert_union(topk_idx, T, k, E, counts, union_ids, n_unique, offsets, perm,
+                                                 (hipStream_t)stream));
+}
+
+moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, size_t *bytes)
+{
+    if (!bytes) return MOE_ERR_INVALID_ARG;
+    const moe_status_t st = check_weights(w);
+    if (st != MOE_OK) return st;
+    if (T < 1 || k < 1 || k > kMaxK || k > w->E || (long)T * k > kMaxSlots) return MOE_ERR_INVALID_ARG;
+    *bytes = ecospec::verify_workspace(w->d, w->d_ff, T, k, w->sh_gate != nullptr).total;
+    return MOE_OK;
+}
+
+moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
+                              void *workspace, size_t workspace_bytes, void *stream)
+{
+    moe_status_t st = check_weights(w);
+    if (st != MOE_OK) return st;
+    if (!x || !y || !r || !workspace || x == y) return MOE_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(workspace, 256)) return MOE_ERR_INVALID_ARG;
+    if (r->T < 1 || r->k < 1 || r->k > kMaxK || r->k > w->E || r->E != w->E || (long)r->T * r->k > kMaxSlots)
+        return MOE_ERR_INVALID_ARG;
+    if (!r->topk_w || !r->union_ids || !r->n_unique || !r->offsets || !r->perm) return MOE_ERR_INVALID_ARG;
+    const bool shared = w->sh_gate != nullptr;
+    const ecospec::VerifyWorkspace ws = ecospec::verify_workspace(w->d, w->d_ff, r->T, r->k, shared);
+    if (workspace_bytes < ws.total) return MOE_ERR_WORKSPACE;
+
+    ecospec::VerifyArgs a{};
+    a.fmt = w->fmt;
+    a.d = w->d;
+    a.d_ff = w->d_ff;
+    a.E = w->E;
+    a.T = r->T;
+    a.k = r->k;
+    a.w_gate = static_cast<const uint8_t *>(w->w_gate);
+    a.w_up = static_cast<const uint8_t *>(w->w_up);
+    a.w_down = static_cast<const uint8_t *>(w->w_down);
+    a.s_gate = w->s_gate;
+    a.s_up = w->s_up;
+    a.s_down = w->s_down;
+    a.sh_gate = static_cast<const uint8_t *>(w->sh_gate);
+    a.sh_up = static_cast<const uint8_t *>(w->sh_up);
+    a.sh_down = static_cast<const uint8_t *>(w->sh_down);
+    a.sh_s_gate = w->sh_s_gate;
+    a.sh_s_up = w->sh_s_up;
+    a.sh_s_down = w->sh_s_down;
+    a.topk_w = r->topk_w;
+    a.union_ids = r->union_ids;
+    a.n_unique = r->n_unique;
+    a.offsets = r->offsets;
+    a.perm = r->perm;
+    a.x = static_cast<const uint16_t *>(x);
+    a.y = static_cast<uint16_t *>(y);
+    a.h = reinterpret_cast<uint16_t *>(static_cast<uint8_t *>(workspace) + ws.h_offset);
+    a.o = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + ws.o_offset);
+    return from_hip(ecospec::launch_verify(a, (hipStream_t)stream));
+}
+
+}  // extern "C"

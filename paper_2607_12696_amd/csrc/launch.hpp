@@ -1,0 +1,40 @@
+// Internal launchers of the gfx950 kernels; the C ABI in abi.cpp validates
+// arguments and then calls these.  All enqueue on `stream` and return the
+// hipError_t of the launch.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ecospec {
+
+hipError_t launch_route_topk(const float *logits, int T, int E, int k, int score, int32_t *idx, float *w,
+                             hipStream_t stream);
+
+hipError_t launch_expert_union(const int32_t *idx, int T, int k, int E, int32_t *counts, int32_t *union_ids,
+                               int32_t *n_unique, int32_t *offsets, int32_t *perm, hipStream_t stream);
+
+struct VerifyArgs {
+    int fmt, d, d_ff, E, T, k;
+    const uint8_t *w_gate, *w_up, *w_down;  // routed experts, stacked [E]
+    const void *s_gate, *s_up, *s_down;
+    const uint8_t *sh_gate, *sh_up, *sh_down;  // shared expert or null
+    const void *sh_s_gate, *sh_s_up, *sh_s_down;
+    const float *topk_w;
+    const int32_t *union_ids, *n_unique, *offsets, *perm;
+    const uint16_t *x;  // [T][d] bf16
+    uint16_t *y;        // [T][d] bf16
+    uint16_t *h;        // workspace: [T*k + T][d_ff] bf16, grouped positions
+    float *o;           // workspace: [T*k + T][d] fp32, slots
+};
+
+// Workspace layout shared by the size query and the launcher.
+struct VerifyWorkspace {
+    size_t h_offset, h_bytes, o_offset, o_bytes, total;
+};
+VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared);
+
+hipError_t launch_verify(const VerifyArgs &a, hipStream_t stream);
+
+}  // namespace ecospec

@@ -1,0 +1,144 @@
+"""C ABI checks that need no GPU: the library loads, exports every function the
+header declares, and rejects invalid arguments on the host before any launch."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import paper_2607_12696_amd as moe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ecospec_moe.h")
+
+# Any non-null value: validation fails before the pointer is ever used.
+FAKE = 0x10000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    L = moe.lib()
+    names = declared_functions()
+    assert set(names) == set(moe.EXPORTED)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    L = moe.lib()
+    for s in range(5):
+        assert L.moe_status_string(s)
+    assert L.moe_status_string(99) == b"unknown status"
+
+
+@pytest.mark.parametrize("T,E,k,score,null", [
+    (0, 16, 2, 0, False), (4, 0, 1, 0, False), (4, 16, 0, 0, False), (4, 16, 17, 0, False),
+    (4, 1025, 8, 0, False), (4, 128, 65, 0, False), (4, 16, 2, 2, False), (4, 16, 2, 0, True)])
+def test_route_topk_rejects(T, E, k, score, null):
+    L = moe.lib()
+    p = 0 if null else FAKE
+    assert L.moe_route_topk(p, T, E, k, score, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("T,k,E", [(0, 2, 16), (4, 0, 16), (4, 65, 128), (4, 2, 0), (4, 2, 1025), (1 << 20, 32, 64)])
+def test_expert_union_rejects(T, k, E):
+    L = moe.lib()
+    assert L.moe_expert_union(FAKE, T, k, E, FAKE, FAKE, FAKE, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG
+
+
+def test_expert_union_rejects_null_output():
+    L = moe.lib()
+    assert L.moe_expert_union(FAKE, 4, 2, 16, FAKE, 0, FAKE, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG
+
+
+def _weights(fmt=0, d=256, d_ff=128, E=16, shared=False, scales=True):
+    w = moe.moe_weights_t()
+    w.fmt, w.d, w.d_ff, w.E = fmt, d, d_ff, E
+    w.w_gate = w.w_up = w.w_down = FAKE
+    if fmt and scales:
+        w.s_gate = w.s_up = w.s_down = FAKE
+    if shared:
+        w.sh_gate = w.sh_up = w.sh_down = FAKE
+        if fmt:
+            w.sh_s_gate = w.sh_s_up = w.sh_s_down = FAKE
+    return w
+
+
+def _routing(T=8, k=2, E=16):
+    r = moe.moe_routing_t()
+    r.T, r.k, r.E = T, k, E
+    for n in ("topk_idx", "topk_w", "counts", "union_ids", "n_unique", "offsets", "perm"):
+        setattr(r, n, FAKE)
+    return r
+
+
+def _ws(w, T, k):
+    n = C.c_size_t()
+    st = moe.lib().moe_verify_workspace_size(C.byref(w), T, k, C.byref(n))
+    return st, n.value
+
+
+def test_workspace_size_formula():
+    st, n = _ws(_weights(0, 256, 128, 16), 8, 2)
+    assert st == moe.MOE_OK
+    rows = 8 * 2
+    h = rows * 128 * 2
+    o = rows * 256 * 4
+    assert n == ((h + 255) // 256) * 256 + ((o + 255) // 256) * 256
+    st, n2 = _ws(_weights(1, 7168, 2048, 256, shared=True), 64, 8)
+    assert st == moe.MOE_OK and n2 >= (64 * 8 + 64) * (2048 * 2 + 7168 * 4)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(fmt=3), moe.MOE_ERR_INVALID_ARG),
+    (dict(d=0), moe.MOE_ERR_INVALID_ARG),
+    (dict(E=1025), moe.MOE_ERR_INVALID_ARG),
+    (dict(d=96), moe.MOE_ERR_UNSUPPORTED),
+    (dict(d_ff=48), moe.MOE_ERR_UNSUPPORTED),
+    (dict(fmt=1, d=320, d_ff=128), moe.MOE_ERR_UNSUPPORTED),
+    (dict(fmt=1, scales=False), moe.MOE_ERR_INVALID_ARG),
+    (dict(fmt=2, scales=False), moe.MOE_ERR_INVALID_ARG),
+])
+def test_weights_validation(kw, status):
+    assert _ws(_weights(**kw), 8, 2)[0] == status
+
+
+def test_partial_shared_expert_rejected():
+    w = _weights()
+    w.sh_gate = FAKE
+    assert _ws(w, 8, 2)[0] == moe.MOE_ERR_INVALID_ARG
+
+
+def test_misaligned_weight_rejected():
+    w = _weights()
+    w.w_up = FAKE + 8
+    assert _ws(w, 8, 2)[0] == moe.MOE_ERR_INVALID_ARG
+
+
+def test_verify_layer_rejects_before_launch():
+    L = moe.lib()
+    w, r = _weights(), _routing()
+    st, need = _ws(w, 8, 2)
+    assert st == moe.MOE_OK
+    args = lambda x=FAKE, y=2 * FAKE, ws=4 * FAKE, nb=need: (x, C.byref(w), C.byref(r), y, ws, nb, None)
+    assert L.moe_verify_layer(*args(nb=need - 1)) == moe.MOE_ERR_WORKSPACE
+    assert L.moe_verify_layer(*args(x=0)) == moe.MOE_ERR_INVALID_ARG
+    assert L.moe_verify_layer(*args(y=FAKE)) == moe.MOE_ERR_INVALID_ARG      # y aliases x
+    assert L.moe_verify_layer(*args(ws=4 * FAKE + 16)) == moe.MOE_ERR_INVALID_ARG  # workspace not 256-aligned
+    r.E = 32
+    assert L.moe_verify_layer(*args()) == moe.MOE_ERR_INVALID_ARG
+    r.E, r.k = 16, 17
+    assert L.moe_verify_layer(*args()) == moe.MOE_ERR_INVALID_ARG
+    r.k, r.perm = 2, None
+    assert L.moe_verify_layer(*args()) == moe.MOE_ERR_INVALID_ARG
+
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    with pytest.raises(ValueError):
+        moe.moe_route_topk(torch.zeros(2, 16), 2, 0)

@@ -1,0 +1,235 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bars: routing indices, union, counts, offsets and perm bit-exact; gate weights
+within 2e-6; y within max|dy| <= 1e-2 * max|y_oracle| (bf16/FP8/MXFP4 weights,
+fp32 accumulation).  Inputs are seeded synthetic draws handed to both sides;
+the oracle never sees a value the GPU produced.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_12696_amd as moe
+import synth
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+DEV = torch.device("cuda:0")
+YTOL = 1e-2
+WTOL = 2e-6
+
+
+def note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(layer):
+    return {k: (v.to(DEV) if hasattr(v, "to") else v) for k, v in layer.items()}
+
+
+def y_err(y_gpu, y_ref):
+    d = np.abs(y_gpu.astype(np.float64) - y_ref)
+    return d.max() / max(np.abs(y_ref).max(), 1e-30)
+
+
+def routed_logits(kind, T, sh, seed, U=None):
+    if kind == "scattered":
+        return synth.logits_scattered(T, sh.E, seed=seed)
+    if kind == "ties":
+        return synth.logits_tie_grid(T, sh.E, seed=seed)
+    if kind == "clustered":
+        return synth.routes_to_logits(synth.routes_clustered(T, sh.E, sh.k, 0.8, seed=seed), sh.E, seed=seed)
+    return synth.routes_to_logits(synth.routes_exact_u(T, sh.E, sh.k, U, seed=seed), sh.E, seed=seed)
+
+
+# ----------------------------------------------------------------------------- route + union
+
+ROUTE_CASES = [(E, k, score) for (E, k, score) in [(16, 2, 0), (128, 8, 0), (256, 8, 1), (128, 4, 0), (1, 1, 0),
+                                                     (1024, 64, 1), (100, 7, 1), (16, 16, 0)]]
+
+
+@pytest.mark.parametrize("E,k,score", ROUTE_CASES)
+@pytest.mark.parametrize("kind", ["scattered", "ties"])
+@pytest.mark.parametrize("T", [1, 8, 61, 300])
+def test_route_and_union_bit_exact(E, k, score, kind, T):
+    note(f"route/union E={E} k={k} score={score} kind={kind} T={T}")
+    lg = synth.logits_scattered(T, E, seed=T) if kind == "scattered" else synth.logits_tie_grid(T, E, seed=T)
+    idx_g, w_g = moe.moe_route_topk(lg.to(DEV), k, score)
+    r = moe.moe_expert_union(idx_g, E, topk_w=w_g)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), k, score)
+    assert np.array_equal(idx_g.cpu().numpy(), idx_o)
+    assert np.abs(w_g.cpu().numpy().astype(np.float64) - w_o).max() <= WTOL
+    u = oracle.union(idx_o, E)
+    assert int(r.n_unique.item()) == u["n_unique"]
+    for name in ("counts", "union_ids", "offsets", "perm"):
+        assert np.array_equal(getattr(r, name).cpu().numpy(), u[name]), name
+
+
+def test_route_nan_and_signed_zero_order():
+    lg = torch.tensor([[float("nan"), -float("inf"), 1.0, float("nan"), -3.0, 0.0, -0.0, 2.0]], dtype=torch.float32)
+    lg[0, 6] = -0.0
+    idx_g, _ = moe.moe_route_topk(lg.to(DEV), 8, 0)
+    idx_o, _ = oracle.route(lg.numpy(), 8, 0)
+    assert np.array_equal(idx_g.cpu().numpy(), idx_o)
+    assert list(idx_o[0]) == [7, 2, 5, 6, 4, 1, 0, 3]
+
+
+@pytest.mark.parametrize("T,E,k,U", [(8, 256, 8, 8), (64, 256, 8, 256), (64, 256, 8, 32), (3, 16, 2, 5),
+                                     (4096, 1024, 8, 1000), (1, 1024, 64, 64)])
+def test_union_on_given_routes(T, E, k, U):
+    note(f"union T={T} E={E} k={k} U={U}")
+    idx = synth.routes_exact_u(T, E, k, U, seed=4).astype(np.int32)
+    r = moe.moe_expert_union(torch.from_numpy(idx).to(DEV), E)
+    u = oracle.union(idx, E)
+    assert int(r.n_unique.item()) == U == u["n_unique"]
+    for name in ("counts", "union_ids", "offsets", "perm"):
+        assert np.array_equal(getattr(r, name).cpu().numpy(), u[name]), name
+
+
+# ----------------------------------------------------------------------------- verify layer, small shapes
+
+SMALL = {
+    "toy": synth.SHAPES["toy"],
+    "bf16_tail": synth.Shape("bf16_tail", 192, 96, 12, 3, synth.FMT_BF16, 0, False),
+    "fp8": synth.Shape("fp8", 256, 256, 16, 4, synth.FMT_FP8, 1, True),
+    "fp8_wide": synth.Shape("fp8_wide", 384, 128, 8, 2, synth.FMT_FP8, 1, True),
+    "mxfp4": synth.Shape("mxfp4", 320, 160, 16, 4, synth.FMT_MXFP4, 0, False),
+    "one": synth.Shape("one", 64, 32, 1, 1, synth.FMT_BF16, 0, False),
+}
+
+_small_layers = {}
+
+
+def small_layer(name):
+    if name not in _small_layers:
+        _small_layers[name] = synth.layer_weights(SMALL[name], seed=21)
+    return _small_layers[name]
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("T", [1, 5, 8, 37, 64, 130])
+def test_verify_small_matches_oracle(name, T):
+    sh = SMALL[name]
+    note(f"verify small shape={name} T={T}")
+    layer = small_layer(name)
+    x = synth.activations(T, sh.d, seed=T)
+    lg = synth.logits_scattered(T, sh.E, seed=T + 1)
+    y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), to_dev(layer), sh.k, sh.score)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), sh.k, sh.score)
+    y_ref = oracle.verify_tokens(layer, x, idx_o, w_o, threads=8)
+    err = y_err(y.float().cpu().numpy(), y_ref)
+    note(f"  rel err {err:.3e}")
+    assert err <= YTOL
+
+
+@pytest.mark.parametrize("name", ["toy", "fp8", "mxfp4"])
+def test_verify_is_deterministic(name):
+    sh = SMALL[name]
+    T = 64
+    dl = to_dev(small_layer(name))
+    x = synth.activations(T, sh.d, seed=3).to(DEV)
+    lg = synth.logits_scattered(T, sh.E, seed=3).to(DEV)
+    y1, _ = moe.moe_verify_step(x, lg, dl, sh.k, sh.score)
+    y2, _ = moe.moe_verify_step(x, lg, dl, sh.k, sh.score)
+    assert torch.equal(y1, y2)
+
+
+def test_all_experts_routed_k_equals_E():
+    sh = synth.Shape("kE", 128, 64, 6, 6, synth.FMT_BF16, 0, False)
+    layer = synth.layer_weights(sh, seed=5)
+    T = 20
+    x = synth.activations(T, sh.d, seed=5)
+    lg = synth.logits_scattered(T, sh.E, seed=5)
+    y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), to_dev(layer), sh.k, 0)
+    assert int(r.n_unique.item()) == sh.E
+    idx_o, w_o = oracle.route(lg.numpy(), sh.k, 0)
+    assert y_err(y.float().cpu().numpy(), oracle.verify_tokens(layer, x, idx_o, w_o)) <= YTOL
+
+
+def test_workspace_contents_do_not_matter():
+    sh = SMALL["fp8"]
+    T = 9
+    dl = to_dev(small_layer("fp8"))
+    x = synth.activations(T, sh.d, seed=8).to(DEV)
+    lg = synth.logits_scattered(T, sh.E, seed=8).to(DEV)
+    nbytes = moe.moe_verify_workspace_size(dl, T, sh.k)
+    ws1 = torch.zeros(nbytes, dtype=torch.uint8, device=DEV)
+    ws2 = torch.full((nbytes,), 0xFF, dtype=torch.uint8, device=DEV)
+    y1, _ = moe.moe_verify_step(x, lg, dl, sh.k, sh.score, workspace=ws1)
+    y2, _ = moe.moe_verify_step(x, lg, dl, sh.k, sh.score, workspace=ws2)
+    assert torch.equal(y1, y2)
+
+
+# ----------------------------------------------------------------------------- full model shapes, sampled rows
+
+_full = {}
+
+
+def full_layer(name):
+    """Device weights of a full-size layer, generated on the GPU (cached per module)."""
+    if name not in _full:
+        _full.clear()
+        torch.cuda.empty_cache()
+        note(f"generating full {name} layer on the GPU")
+        _full[name] = synth.layer_weights(synth.SHAPES[name], seed=0, device=DEV)
+        torch.cuda.synchronize()
+    return _full[name]
+
+
+def host_experts(dl, experts):
+    """Copy only the listed experts (and the shared one) to the host for the oracle."""
+    out = {"fmt": dl["fmt"], "d": dl["d"], "d_ff": dl["d_ff"]}
+    for n in ("gate", "up", "down", "s_gate", "s_up", "s_down"):
+        if n in dl:
+            out[n] = {e: dl[n][e].cpu() for e in experts}
+    for n in ("sh_gate", "sh_up", "sh_down", "sh_s_gate", "sh_s_up", "sh_s_down"):
+        if n in dl:
+            out[n] = dl[n].cpu()
+    return out
+
+
+FULL_CASES = [
+    ("ds", 64, "exact", 32, [0, 17, 63]),
+    ("ds", 8, "scattered", None, [0, 7]),
+    ("ds", 64, "exact", 256, [5, 40]),
+    ("qwen", 32, "clustered", None, [0, 31]),
+    ("qwen", 64, "scattered", None, [3]),
+    ("gpt", 64, "clustered", None, [0, 50]),
+    ("gpt", 8, "scattered", None, [2, 7]),
+]
+
+
+@pytest.mark.parametrize("name,T,kind,U,rows", FULL_CASES)
+def test_full_shape_sampled_rows(name, T, kind, U, rows):
+    sh = synth.SHAPES[name]
+    note(f"full shape={name} T={T} routing={kind} U={U} rows={rows}")
+    dl = full_layer(name)
+    x = synth.activations(T, sh.d, seed=31)
+    lg = routed_logits(kind, T, sh, seed=31, U=U)
+    y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), dl, sh.k, sh.score)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), sh.k, sh.score)
+    u = oracle.union(idx_o, sh.E)
+    assert int(r.n_unique.item()) == u["n_unique"]
+    if U is not None:
+        assert u["n_unique"] == U
+    assert np.array_equal(r.perm.cpu().numpy(), u["perm"])
+    used = sorted(set(idx_o[rows].reshape(-1).tolist()))
+    hl = host_experts(dl, used)
+    y_ref = oracle.verify_tokens(hl, x, idx_o, w_o, tokens=rows, threads=16)
+    err = y_err(y.float().cpu().numpy()[rows], y_ref)
+    note(f"  U={u['n_unique']} rel err {err:.3e}")
+    assert err <= YTOL
+    # Every row: finite, and equal to a second run bit for bit.
+    y2, _ = moe.moe_verify_step(x.to(DEV), lg.to(DEV), dl, sh.k, sh.score)
+    assert torch.isfinite(y.float()).all()
+    assert torch.equal(y, y2)
