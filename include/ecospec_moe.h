@@ -70,12 +70,14 @@ typedef enum {
     MOE_SEL_COST_DIFF = 3    /* P - lambda * DeltaCost                                      */
 } moe_sel_mode_t;
 
-/* Weights of one MoE layer; all pointers are device pointers.  The scale
- * pointers are NULL for MOE_W_BF16.  The sh_* fields describe one always-on
- * shared expert (same layout, leading dimension 1) with gate weight 1 that
- * every token uses; all sh_* weight pointers NULL means no shared expert.
- * Requirements: d % 64 == 0, d_ff % 32 == 0, and for FP8 d % 128 == 0 and
- * d_ff % 128 == 0.  Each matrix must be 16-byte aligned. */
+/* Weights of one MoE layer, in the streaming layout written by
+ * moe_pack_weights; all pointers are device pointers.  The scale pointers
+ * are NULL for MOE_W_BF16.  The sh_* fields describe one always-on shared
+ * expert (packed the same way, E = 1) with gate weight 1 that every token
+ * uses; all sh_* weight pointers NULL means no shared expert.
+ * Requirements: d % 32 == 0, d_ff % 32 == 0, and for FP8 d % 128 == 0 and
+ * d_ff % 128 == 0; each packed matrix below 2 GiB; 16-byte aligned pointers.
+ * Other shapes return MOE_ERR_UNSUPPORTED. */
 typedef struct {
     int fmt; /* moe_wfmt_t */
     int d, d_ff, E;
@@ -97,6 +99,29 @@ typedef struct {
     const int32_t *offsets;  /* [E+1]  */
     const int32_t *perm;     /* [T*k]  */
 } moe_routing_t;
+
+/*
+ * Weight packing (done once, when a model is loaded).  Converts E stacked
+ * N x K matrices of one tensor (W_gate or W_up: N = d_ff, K = d; W_down:
+ * N = d, K = d_ff) from the interchange layout of moe_wfmt_t into the
+ * streaming layout the verify kernels read:
+ *   K is padded with zero codes to Kp = the next multiple of 128; each
+ *   matrix is a row-major grid of blocks of 16 rows x 128 elements, block
+ *   (rb, kb) at byte offset (rb*Kp/128 + kb) * B, with B = 4096 (bf16), 2048
+ *   (FP8) or 1024 (MXFP4); a block is B/1024 vectors of 1 KiB and the 16
+ *   bytes at offset 16*l of vector i (l = c + 16*g, c < 16, g < 4) hold
+ *   the weights of row rb*16 + c from element kb*128 + 32*g + i*32*1024/B on,
+ *   i.e. exactly the matrix-core operand fragment of lane l.
+ *   FP8 scales keep their [N/128][K/128] layout (copied).  MXFP4 scales
+ *   become [N/16][Kp/128][64] bytes, byte l of a block = the code of row
+ *   rb*16 + c, 32-element chunk kb*4 + g (127 in the padding).
+ * w, s: device pointers in the interchange layout; w_packed, s_packed:
+ * device buffers of the sizes moe_packed_size returns (s may be NULL for
+ * bf16).  Requirements: N % 16 == 0, K % 32 == 0 (FP8: N, K % 128 == 0).
+ */
+moe_status_t moe_packed_size(int fmt, int E, int N, int K, size_t *weight_bytes, size_t *scale_bytes);
+moe_status_t moe_pack_weights(int fmt, int E, int N, int K, const void *w, const void *s, void *w_packed,
+                              void *s_packed, void *stream);
 
 /*
  * Router top-k (Section 1: each token goes to a top-k subset of experts;
@@ -137,7 +162,7 @@ moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, siz
  *   y[t] = sum_j topk_w[t][j] * FFN_{topk_idx[t][j]}(x[t])  (+ FFN_shared(x[t]))
  *   FFN_e(x) = W_down[e] (silu(W_gate[e] x) * (W_up[e] x))
  * Each distinct routed expert (and the shared one) is streamed from HBM once
- * per call, whatever the number of tokens routed to it.
+ * per call for up to 64 of its tokens (once per 64 tokens beyond that).
  *   x  [T][d] bf16 in, y [T][d] bf16 out (may not alias x), device.
  *   r  routing from moe_route_topk + moe_expert_union for the same T, k, E.
  *   workspace: device buffer of at least moe_verify_workspace_size bytes,
@@ -149,6 +174,17 @@ moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, siz
  */
 moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
                               void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * moe_verify_layer with timing marks: identical work and arguments, and in
+ * addition records the caller's events on `stream` around its three kernels:
+ *   events[0] before the gate/up kernel, events[1] before the down kernel,
+ *   events[2] before the combine kernel, events[3] after it.
+ * events is an array of 4 hipEvent_t handles created by the caller (any
+ * entry may be NULL to skip that mark).
+ */
+moe_status_t moe_verify_layer_timed(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
+                                    void *workspace, size_t workspace_bytes, void *stream, void *const *events);
 
 /*
  * Cost-aware draft-tree selection on the host (Section 4.2, Eq. 7-9,

@@ -10,7 +10,8 @@ the library has not been built, importing the functions that need it raises
     moe_route_topk(logits, k, score)            -> (topk_idx, topk_w)
     moe_expert_union(topk_idx, E)               -> Routing
     moe_verify_workspace_size(weights, T, k)    -> bytes
-    moe_verify_layer(x, weights, routing)       -> y
+    moe_pack_weights(fmt, w, s)                 -> (w_packed, s_packed)   once per model load
+    moe_verify_layer(x, weights, routing)       -> y   (weights packed)
     moe_select_tree(parent, P, pred, E, budget) -> (selected, marginal_cost)
     moe_verify_step(x, logits, weights, k, score) = the three device calls in order
 """
@@ -32,7 +33,8 @@ MOE_W_BF16, MOE_W_FP8_E4M3_B128, MOE_W_MXFP4 = 0, 1, 2
 MOE_SEL_COST_RATIO, MOE_SEL_CONFIDENCE, MOE_SEL_GLOBAL_COST, MOE_SEL_COST_DIFF = 0, 1, 2, 3
 
 EXPORTED = ("moe_route_topk", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
-            "moe_select_tree", "moe_status_string", "moe_last_error")
+            "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree",
+            "moe_status_string", "moe_last_error")
 
 
 class MoeError(RuntimeError):
@@ -69,12 +71,16 @@ def lib() -> C.CDLL:
             L.moe_expert_union.argtypes = [p, i, i, i, p, p, p, p, p, p]
             L.moe_verify_workspace_size.argtypes = [C.POINTER(moe_weights_t), i, i, C.POINTER(C.c_size_t)]
             L.moe_verify_layer.argtypes = [p, C.POINTER(moe_weights_t), C.POINTER(moe_routing_t), p, p, C.c_size_t, p]
+            L.moe_verify_layer_timed.argtypes = [p, C.POINTER(moe_weights_t), C.POINTER(moe_routing_t), p, p,
+                                                 C.c_size_t, p, C.POINTER(C.c_void_p)]
+            L.moe_packed_size.argtypes = [i, i, i, i, C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]
+            L.moe_pack_weights.argtypes = [i, i, i, i, p, p, p, p, p]
             L.moe_select_tree.argtypes = [i, p, p, i, i, p, i, p, i, C.c_double, C.c_double, i, p, p, p]
             L.moe_status_string.argtypes = [i]
             L.moe_status_string.restype = C.c_char_p
             L.moe_last_error.restype = C.c_char_p
             for f in ("moe_route_topk", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
-                      "moe_select_tree"):
+                      "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree"):
                 getattr(L, f).restype = i
             _lib = L
     return _lib
@@ -169,13 +175,54 @@ def moe_expert_union(topk_idx, E: int, topk_w=None, out: Routing | None = None) 
     return out
 
 
+# --------------------------------------------------------------------------- weight packing
+
+def moe_packed_size(fmt: int, E: int, N: int, K: int) -> tuple[int, int]:
+    wb, sb = C.c_size_t(), C.c_size_t()
+    _check("moe_packed_size", lib().moe_packed_size(fmt, E, N, K, C.byref(wb), C.byref(sb)))
+    return wb.value, sb.value
+
+
+def moe_pack_weights(fmt: int, w, s=None):
+    """Pack stacked device weights w [E, N, K(/2)] (+ scales) into the streaming layout.
+
+    Returns (w_packed, s_packed) as flat uint8 device tensors (s_packed None for bf16).
+    """
+    torch = _torch()
+    E, N = w.shape[0], w.shape[1]
+    K = w.shape[2] * (2 if fmt == MOE_W_MXFP4 else 1)
+    wb, sb = moe_packed_size(fmt, E, N, K)
+    wp = torch.empty(wb, dtype=torch.uint8, device=w.device)
+    sp = torch.empty(sb, dtype=torch.uint8, device=w.device) if sb else None
+    _check("moe_pack_weights", lib().moe_pack_weights(fmt, E, N, K, _dev_ptr(w, "w"), _dev_ptr(s, "s"),
+                                                        _dev_ptr(wp, "w_packed"), _dev_ptr(sp, "s_packed"),
+                                                        _stream(w)))
+    return wp, sp
+
+
+def pack_layer(layer: dict) -> dict:
+    """A layer dict (interchange layout, device tensors) with every matrix packed."""
+    out = {k: layer[k] for k in ("fmt", "d", "d_ff") if k in layer}
+    out["E"] = int(layer.get("E", layer["gate"].shape[0]))
+    fmt = int(layer["fmt"])
+    for prefix in ("", "sh_"):
+        for name in ("gate", "up", "down"):
+            if layer.get(prefix + name) is None:
+                continue
+            wp, sp = moe_pack_weights(fmt, layer[prefix + name], layer.get(prefix + "s_" + name))
+            out[prefix + name] = wp
+            if sp is not None:
+                out[prefix + "s_" + name] = sp
+    return out
+
+
 # --------------------------------------------------------------------------- verify layer
 
 def weights_struct(w: dict) -> moe_weights_t:
     """moe_weights_t for a layer dict (keys fmt, d, d_ff, E, gate, up, down, optional s_* and sh_*)."""
     s = moe_weights_t()
     s.fmt, s.d, s.d_ff = int(w["fmt"]), int(w["d"]), int(w["d_ff"])
-    s.E = int(w.get("E", w["gate"].shape[0]))
+    s.E = int(w["E"]) if "E" in w else int(w["gate"].shape[0])
     for name in ("gate", "up", "down"):
         setattr(s, "w_" + name, _dev_ptr(w[name], name))
         setattr(s, "s_" + name, _dev_ptr(w.get("s_" + name), "s_" + name))
@@ -206,6 +253,19 @@ def moe_verify_layer(x, weights: dict, routing: Routing, y=None, workspace=None)
     _check("moe_verify_layer", lib().moe_verify_layer(
         _dev_ptr(x, "x"), C.byref(ws), C.byref(rs), _dev_ptr(y, "y"), _dev_ptr(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _stream(x)))
+    return y
+
+
+def moe_verify_layer_timed(x, weights: dict, routing: Routing, y, workspace, events):
+    """moe_verify_layer that also records 4 torch.cuda.Event marks around its kernels
+    (before gate/up, before down, before combine, after combine) on the current stream."""
+    torch = _torch()
+    arr = (C.c_void_p * 4)(*[e.cuda_event if e is not None else None for e in events])
+    ws = weights_struct(weights)
+    rs = routing.c_struct()
+    _check("moe_verify_layer_timed", lib().moe_verify_layer_timed(
+        _dev_ptr(x, "x"), C.byref(ws), C.byref(rs), _dev_ptr(y, "y"), _dev_ptr(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(x), arr))
     return y
 
 

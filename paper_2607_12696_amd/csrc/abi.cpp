@@ -38,8 +38,10 @@ moe_status_t check_weights(const moe_weights_t *w)
         return MOE_ERR_INVALID_ARG;
     // Tile shapes of the kernels: 16-row gate/up bands, 32-row down bands,
     // 32-wide K chunks; FP8 needs whole 128x128 scale blocks.
-    if (w->d % 64 || w->d_ff % 32) return MOE_ERR_UNSUPPORTED;
+    if (w->d % 32 || w->d_ff % 32) return MOE_ERR_UNSUPPORTED;
     if (w->fmt == MOE_W_FP8_E4M3_B128 && (w->d % 128 || w->d_ff % 128)) return MOE_ERR_UNSUPPORTED;
+    // Every packed matrix is addressed through a 32-bit buffer range below 2^31 bytes.
+    if (ecospec::packed_matrix_bytes(w->fmt, w->d_ff, w->d) >= (1UL << 31)) return MOE_ERR_UNSUPPORTED;
     const void *mats[] = {w->w_gate, w->w_up, w->w_down, w->sh_gate, w->sh_up, w->sh_down};
     for (const void *p : mats)
         if (p && !aligned(p, 16)) return MOE_ERR_INVALID_ARG;
@@ -98,8 +100,8 @@ moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, siz
     return MOE_OK;
 }
 
-moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
-                              void *workspace, size_t workspace_bytes, void *stream)
+static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
+                                void *workspace, size_t workspace_bytes, void *stream, void *const *events)
 {
     moe_status_t st = check_weights(w);
     if (st != MOE_OK) return st;
@@ -111,6 +113,8 @@ moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_r
     const bool shared = w->sh_gate != nullptr;
     const ecospec::VerifyWorkspace ws = ecospec::verify_workspace(w->d, w->d_ff, r->T, r->k, shared);
     if (workspace_bytes < ws.total) return MOE_ERR_WORKSPACE;
+    const long rows = (long)r->T * r->k + (shared ? r->T : 0);
+    if ((long)r->T * w->d * 2 >= (1L << 31) || rows * w->d_ff * 2 >= (1L << 31)) return MOE_ERR_UNSUPPORTED;
 
     ecospec::VerifyArgs a{};
     a.fmt = w->fmt;
@@ -140,7 +144,55 @@ moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_r
     a.y = static_cast<uint16_t *>(y);
     a.h = reinterpret_cast<uint16_t *>(static_cast<uint8_t *>(workspace) + ws.h_offset);
     a.o = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + ws.o_offset);
-    return from_hip(ecospec::launch_verify(a, (hipStream_t)stream));
+    a.xg = reinterpret_cast<uint16_t *>(static_cast<uint8_t *>(workspace) + ws.x_offset);
+    a.ip = reinterpret_cast<int32_t *>(static_cast<uint8_t *>(workspace) + ws.i_offset);
+    float *partials = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + ws.p_offset);
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    if (events)
+        for (int i = 0; i < 4; ++i) ev[i] = (hipEvent_t)events[i];
+    int32_t *plan = reinterpret_cast<int32_t *>(static_cast<uint8_t *>(workspace) + ws.plan_offset);
+    return from_hip(ecospec::launch_verify(a, partials, plan, ws.plan_cap, (hipStream_t)stream, events ? ev : nullptr));
+}
+
+moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
+                              void *workspace, size_t workspace_bytes, void *stream)
+{
+    return verify_impl(x, w, r, y, workspace, workspace_bytes, stream, nullptr);
+}
+
+moe_status_t moe_verify_layer_timed(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
+                                    void *workspace, size_t workspace_bytes, void *stream, void *const *events)
+{
+    return verify_impl(x, w, r, y, workspace, workspace_bytes, stream, events);
+}
+
+static moe_status_t check_pack(int fmt, int E, int N, int K)
+{
+    if (fmt < MOE_W_BF16 || fmt > MOE_W_MXFP4 || E < 1 || N < 16 || K < 32) return MOE_ERR_INVALID_ARG;
+    if (N % 16 || K % 32) return MOE_ERR_UNSUPPORTED;
+    if (fmt == MOE_W_FP8_E4M3_B128 && (N % 128 || K % 128)) return MOE_ERR_UNSUPPORTED;
+    if (ecospec::packed_matrix_bytes(fmt, N, K) >= (1UL << 31)) return MOE_ERR_UNSUPPORTED;
+    return MOE_OK;
+}
+
+moe_status_t moe_packed_size(int fmt, int E, int N, int K, size_t *weight_bytes, size_t *scale_bytes)
+{
+    if (!weight_bytes || !scale_bytes) return MOE_ERR_INVALID_ARG;
+    const moe_status_t st = check_pack(fmt, E, N, K);
+    if (st != MOE_OK) return st;
+    *weight_bytes = (size_t)E * ecospec::packed_matrix_bytes(fmt, N, K);
+    *scale_bytes = (size_t)E * ecospec::packed_scale_bytes(fmt, N, K);
+    return MOE_OK;
+}
+
+moe_status_t moe_pack_weights(int fmt, int E, int N, int K, const void *w, const void *s, void *w_packed,
+                              void *s_packed, void *stream)
+{
+    const moe_status_t st = check_pack(fmt, E, N, K);
+    if (st != MOE_OK) return st;
+    if (!w || !w_packed || w == w_packed || !aligned(w, 16) || !aligned(w_packed, 16)) return MOE_ERR_INVALID_ARG;
+    if (fmt != MOE_W_BF16 && (!s || !s_packed || s == s_packed)) return MOE_ERR_INVALID_ARG;
+    return from_hip(ecospec::launch_pack(fmt, E, N, K, w, s, w_packed, s_packed, (hipStream_t)stream));
 }
 
 }  // extern "C"

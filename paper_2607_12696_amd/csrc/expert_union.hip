@@ -17,34 +17,6 @@ namespace ecospec {
 
 constexpr int kUnionThreads = 1024;
 
-// Exclusive scan of one int per thread over the block; returns the total in *total.
-__device__ int block_exclusive_scan(int v, int *wave_tot, int *total)
-{
-    const int lane = lane_id(), wave = threadIdx.x / kWave, nwaves = blockDim.x / kWave;
-    int incl = v;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const int n = __shfl_up(incl, o, kWave);
-        if (lane >= o) incl += n;
-    }
-    if (lane == kWave - 1) wave_tot[wave] = incl;
-    __syncthreads();
-    if (wave == 0) {
-        int w = lane < nwaves ? wave_tot[lane] : 0;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-            const int n = __shfl_up(w, o, kWave);
-            if (lane >= o) w += n;
-        }
-        if (lane < nwaves) wave_tot[lane] = w;  // inclusive wave prefix
-    }
-    __syncthreads();
-    const int before = wave > 0 ? wave_tot[wave - 1] : 0;
-    *total = wave_tot[nwaves - 1];
-    __syncthreads();  // wave_tot is reused by the next scan
-    return before + incl - v;
-}
-
 __global__ __launch_bounds__(kUnionThreads) void expert_union_kernel(
     const int32_t *__restrict__ idx, int S, int E, int32_t *__restrict__ counts, int32_t *__restrict__ union_ids,
     int32_t *__restrict__ n_unique, int32_t *__restrict__ offsets, int32_t *__restrict__ perm)

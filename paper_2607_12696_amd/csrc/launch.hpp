@@ -25,16 +25,33 @@ struct VerifyArgs {
     const int32_t *union_ids, *n_unique, *offsets, *perm;
     const uint16_t *x;  // [T][d] bf16
     uint16_t *y;        // [T][d] bf16
-    uint16_t *h;        // workspace: [T*k + T][d_ff] bf16, grouped positions
-    float *o;           // workspace: [T*k + T][d] fp32, slots
+    uint16_t *h;        // workspace: [T*k (+T)][d_ff] bf16 SwiGLU rows, grouped positions
+    float *o;           // workspace: [T*k (+T)][d] fp32 expert outputs, grouped positions
+    uint16_t *xg;       // workspace: [T*k (+T)][d] bf16 x rows in grouped order
+    int32_t *ip;        // workspace: [T*k] grouped position of each slot (inverse of perm)
 };
 
-// Workspace layout shared by the size query and the launcher.
+// Upper bound on the wavefronts of a verify grid (sizes the partial-sum slots).
+constexpr int kMaxWorkers = 2048;
+
+// Workspace layout shared by the size query and the launcher: H (bf16 SwiGLU
+// rows), O (fp32 per-slot expert outputs), partial sums of cut work items.
 struct VerifyWorkspace {
-    size_t h_offset, h_bytes, o_offset, o_bytes, total;
+    size_t h_offset, h_bytes, o_offset, o_bytes, p_offset, p_bytes, x_offset, x_bytes, i_offset, i_bytes;
+    size_t plan_offset, plan_bytes;
+    int plan_cap;
+    size_t total;
 };
 VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared);
 
-hipError_t launch_verify(const VerifyArgs &a, hipStream_t stream);
+// events: 4 optional marks recorded before gate/up, down, combine and after combine.
+hipError_t launch_verify(const VerifyArgs &a, float *partials, int32_t *plan, int plan_cap, hipStream_t stream,
+                         hipEvent_t const *events = nullptr);
+
+// Packed (streaming) weight layout; see pack.hip.
+size_t packed_matrix_bytes(int fmt, int N, int K);
+size_t packed_scale_bytes(int fmt, int N, int K);
+hipError_t launch_pack(int fmt, int E, int N, int K, const void *w, const void *s, void *wp, void *sp,
+                       hipStream_t stream);
 
 }  // namespace ecospec

@@ -89,7 +89,8 @@ def test_workspace_size_formula():
     rows = 8 * 2
     h = rows * 128 * 2
     o = rows * 256 * 4
-    assert n == ((h + 255) // 256) * 256 + ((o + 255) // 256) * 256
+    partials = 2048 * 2 * (2 * 4 * 4 * 64) * 4
+    assert n == ((h + 255) // 256) * 256 + ((o + 255) // 256) * 256 + partials
     st, n2 = _ws(_weights(1, 7168, 2048, 256, shared=True), 64, 8)
     assert st == moe.MOE_OK and n2 >= (64 * 8 + 64) * (2048 * 2 + 7168 * 4)
 
@@ -98,7 +99,7 @@ def test_workspace_size_formula():
     (dict(fmt=3), moe.MOE_ERR_INVALID_ARG),
     (dict(d=0), moe.MOE_ERR_INVALID_ARG),
     (dict(E=1025), moe.MOE_ERR_INVALID_ARG),
-    (dict(d=96), moe.MOE_ERR_UNSUPPORTED),
+    (dict(d=80), moe.MOE_ERR_UNSUPPORTED),
     (dict(d_ff=48), moe.MOE_ERR_UNSUPPORTED),
     (dict(fmt=1, d=320, d_ff=128), moe.MOE_ERR_UNSUPPORTED),
     (dict(fmt=1, scales=False), moe.MOE_ERR_INVALID_ARG),
@@ -136,6 +137,22 @@ def test_verify_layer_rejects_before_launch():
     assert L.moe_verify_layer(*args()) == moe.MOE_ERR_INVALID_ARG
     r.k, r.perm = 2, None
     assert L.moe_verify_layer(*args()) == moe.MOE_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("fmt,E,N,K,status", [
+    (3, 1, 16, 32, moe.MOE_ERR_INVALID_ARG), (0, 0, 16, 32, moe.MOE_ERR_INVALID_ARG),
+    (0, 1, 24, 32, moe.MOE_ERR_UNSUPPORTED), (0, 1, 16, 48, moe.MOE_ERR_UNSUPPORTED),
+    (1, 1, 64, 128, moe.MOE_ERR_UNSUPPORTED), (1, 1, 128, 160, moe.MOE_ERR_UNSUPPORTED)])
+def test_pack_validation(fmt, E, N, K, status):
+    wb, sb = C.c_size_t(), C.c_size_t()
+    assert moe.lib().moe_packed_size(fmt, E, N, K, C.byref(wb), C.byref(sb)) == status
+    assert moe.lib().moe_pack_weights(fmt, E, N, K, FAKE, FAKE, 2 * FAKE, 3 * FAKE, None) == status
+
+
+def test_packed_sizes():
+    assert moe.moe_packed_size(1, 2, 2048, 7168) == (2 * 2048 * 7168, 2 * 16 * 56 * 4)
+    assert moe.moe_packed_size(0, 1, 32, 96) == (32 * 128 * 2, 0)
+    assert moe.moe_packed_size(2, 1, 2880, 2880) == (2880 * 2944 // 2, 2880 * 23 * 4)
 
 
 def test_binding_refuses_host_tensors():

@@ -31,7 +31,8 @@ def note(msg):
 
 
 def to_dev(layer):
-    return {k: (v.to(DEV) if hasattr(v, "to") else v) for k, v in layer.items()}
+    """Device copy of an interchange-layout layer, packed for the verify kernels."""
+    return moe.pack_layer({k: (v.to(DEV) if hasattr(v, "to") else v) for k, v in layer.items()})
 
 
 def y_err(y_gpu, y_ref):
@@ -92,6 +93,59 @@ def test_union_on_given_routes(T, E, k, U):
     assert int(r.n_unique.item()) == U == u["n_unique"]
     for name in ("counts", "union_ids", "offsets", "perm"):
         assert np.array_equal(getattr(r, name).cpu().numpy(), u[name]), name
+
+
+# ----------------------------------------------------------------------------- weight packing
+
+def _expected_packed(fmt, w, s):
+    """The streaming layout written out with numpy (an independent statement of the format)."""
+    w = w.numpy() if fmt else w.view(torch.int16).numpy().view(np.uint8).reshape(w.shape[0], w.shape[1], -1)
+    E, N = w.shape[0], w.shape[1]
+    esz = {0: 2.0, 1: 1.0, 2: 0.5}[fmt]
+    K = int(round(w.shape[2] / esz))
+    nkb = (K + 127) // 128
+    vecs = {0: 4, 1: 2, 2: 1}[fmt]
+    per = 32 // vecs                      # elements in one 16-byte vector
+    out = np.zeros((E, N // 16, nkb, vecs, 64, 16), np.uint8)
+    for c in range(16):
+        for g in range(4):
+            l = c + 16 * g
+            for kb in range(nkb):
+                for i in range(vecs):
+                    k0 = kb * 128 + 32 * g + i * per
+                    if k0 < K:
+                        b0 = int(k0 * esz)
+                        out[:, :, kb, i, l, :] = w[:, c::16, b0:b0 + 16]
+    sp = None
+    if fmt == 2:
+        s = s.numpy()
+        sp = np.full((E, N // 16, nkb, 64), 127, np.uint8)
+        for c in range(16):
+            for g in range(4):
+                for kb in range(nkb):
+                    ch = kb * 4 + g
+                    if ch < K // 32:
+                        sp[:, :, kb, c + 16 * g] = s[:, c::16, ch]
+    elif fmt == 1:
+        sp = s.numpy().view(np.uint8)
+    return out.reshape(-1), None if sp is None else sp.reshape(-1)
+
+
+@pytest.mark.parametrize("fmt,N,K", [(0, 32, 96), (0, 48, 256), (1, 128, 384), (2, 32, 160), (2, 64, 128)])
+def test_pack_layout(fmt, N, K):
+    note(f"pack fmt={fmt} N={N} K={K}")
+    E = 3
+    if fmt == 0:
+        w, s = synth.weights_bf16(E, N, K, seed=9), None
+    elif fmt == 1:
+        w, s = synth.weights_fp8_b128(E, N, K, seed=9)
+    else:
+        w, s = synth.weights_mxfp4(E, N, K, seed=9)
+    wp, sp = moe.moe_pack_weights(fmt, w.to(DEV), None if s is None else s.to(DEV))
+    ew, es = _expected_packed(fmt, w, s)
+    assert np.array_equal(wp.cpu().numpy(), ew)
+    if es is not None:
+        assert np.array_equal(sp.cpu().numpy(), es)
 
 
 # ----------------------------------------------------------------------------- verify layer, small shapes
@@ -175,12 +229,13 @@ _full = {}
 
 
 def full_layer(name):
-    """Device weights of a full-size layer, generated on the GPU (cached per module)."""
+    """(interchange, packed) device weights of a full-size layer, generated on the GPU (cached)."""
     if name not in _full:
         _full.clear()
         torch.cuda.empty_cache()
         note(f"generating full {name} layer on the GPU")
-        _full[name] = synth.layer_weights(synth.SHAPES[name], seed=0, device=DEV)
+        raw = synth.layer_weights(synth.SHAPES[name], seed=0, device=DEV)
+        _full[name] = (raw, moe.pack_layer(raw))
         torch.cuda.synchronize()
     return _full[name]
 
@@ -212,7 +267,7 @@ FULL_CASES = [
 def test_full_shape_sampled_rows(name, T, kind, U, rows):
     sh = synth.SHAPES[name]
     note(f"full shape={name} T={T} routing={kind} U={U} rows={rows}")
-    dl = full_layer(name)
+    raw, dl = full_layer(name)
     x = synth.activations(T, sh.d, seed=31)
     lg = routed_logits(kind, T, sh, seed=31, U=U)
     y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), dl, sh.k, sh.score)
@@ -224,7 +279,7 @@ def test_full_shape_sampled_rows(name, T, kind, U, rows):
         assert u["n_unique"] == U
     assert np.array_equal(r.perm.cpu().numpy(), u["perm"])
     used = sorted(set(idx_o[rows].reshape(-1).tolist()))
-    hl = host_experts(dl, used)
+    hl = host_experts(raw, used)
     y_ref = oracle.verify_tokens(hl, x, idx_o, w_o, tokens=rows, threads=16)
     err = y_err(y.float().cpu().numpy()[rows], y_ref)
     note(f"  U={u['n_unique']} rel err {err:.3e}")
