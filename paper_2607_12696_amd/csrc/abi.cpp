@@ -144,8 +144,6 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     a.y = static_cast<uint16_t *>(y);
     a.h = reinterpret_cast<uint16_t *>(static_cast<uint8_t *>(workspace) + ws.h_offset);
     a.o = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + ws.o_offset);
-    a.xg = reinterpret_cast<uint16_t *>(static_cast<uint8_t *>(workspace) + ws.x_offset);
-    a.ip = reinterpret_cast<int32_t *>(static_cast<uint8_t *>(workspace) + ws.i_offset);
     float *partials = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + ws.p_offset);
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     if (events)

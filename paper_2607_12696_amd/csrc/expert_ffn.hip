@@ -5,63 +5,57 @@
 // tokens routed to its expert (at most 2*M_u flop per weight).  The kernels
 // are weight streams with a small matrix-core contraction attached.
 //
-// Work decomposition ("stream-K").  An item is one expert, one band of rows
-// and one group of up to 64 of the expert's tokens: gate/up bands are 16
-// rows of W_gate together with the same 16 rows of W_up, down bands are 32
-// rows of W_down.  An item is a sequence of K macro steps of 128 reduction
-// elements.  All (item, step) units of a launch are laid end to end and cut
-// into equal contiguous ranges, one per wavefront of a persistent grid (one
-// wavefront per SIMD), so every wavefront streams the same number of bytes
-// whatever the number of distinct experts.  A wavefront that covers a whole
-// item finishes it in registers; an item cut between wavefronts leaves fp32
-// partial sums in the workspace and a second, small kernel adds them in
-// wavefront order and finishes it (the kernel boundary makes the partials
-// visible across the chip's L2 slices; the fixed order makes the result
-// deterministic).
+// Workgroups.  Four wavefronts share one band of rows of one expert and one
+// group of up to 64 of its tokens (an item): gate/up bands are 64 rows of
+// W_gate with the same 64 rows of W_up (16 + 16 per wavefront), down bands
+// are 128 rows of W_down (32 per wavefront).  All four walk the reduction
+// dimension together in macro steps of 128 elements, so the activation tile
+// of a step (the item's tokens x 128 elements) is fetched from L2 once, by
+// one coalesced 16-byte load per thread, parked in LDS and read by every
+// wavefront: activation traffic is a quarter of the weight traffic at 16
+// tokens instead of equal to it.
 //
 // Streaming.  Weights are read in the packed layout (pack.hip): each macro
 // step of a 16-row tile is 1-4 KiB of contiguous memory, fetched with 16-byte
-// buffer loads that already form the A operand of v_mfma_f32_16x16x32_bf16
+// buffer loads that are already the A operand of v_mfma_f32_16x16x32_bf16
 // (weights on the 16-row side, tokens on the 16-column side).  FP8 and MXFP4
 // codes are decoded exactly to bf16 in registers (v_cvt_scalef32_pk_bf16_fp8
 // with unit scale; v_cvt_scalef32_pk_bf16_fp4 with the e8m0 power of two); FP8
 // 128x128 block scales multiply the fp32 partial sum of each macro step (one
-// step lies inside one scale block).  Several macro steps are in flight per
-// wavefront and the prefetch runs across item boundaries.  Loads that fall
-// outside a buffer's range (padding tokens, K tails, the end of a range)
-// return zeros, so the loop has no data-dependent branches around loads.
+// step lies inside one scale block).  A step's weight, scale and activation
+// loads are issued together, PD-1 steps ahead of its use: the vector-memory
+// counter retires loads in issue order, so consuming them in issue order is
+// what keeps PD-1 steps in flight.  Loads outside a buffer's range (padding
+// tokens, K tails, rows past N) return zeros; the loop has no branches
+// around loads.
 //
-// Everything the streaming kernels index is either arithmetic on the grouped
-// position p (rows of the expert's tokens are contiguous in grouped order) or
-// a wave-uniform value read with scalar loads, so no vector load ever waits
-// on metadata (a vector-memory wait is in order and would drain the weight
-// prefetch).  A gather kernel first copies x into grouped order (xg) and
-// records each slot's grouped position; the B operand is then xg rows for
-// gate/up and rows of the bf16 SwiGLU output H for down.  Down writes one fp32
-// row per grouped position; the combine kernel applies the gate weights and
+// Work split ("stream-K").  All (item, step) units of a launch are laid end
+// to end and cut into equal contiguous ranges, one per workgroup of a
+// persistent grid, so every workgroup streams the same number of bytes
+// whatever the number of distinct experts.  An item fully inside a range is
+// finished in registers; an item cut between workgroups leaves fp32 partial
+// sums in the workspace, and a small second kernel adds them in workgroup
+// order and finishes it (the kernel boundary makes them visible across the
+// chip's L2 slices; the fixed order keeps the result deterministic).
+//
+// Outputs: gate/up writes the bf16 SwiGLU rows H at grouped positions; down
+// writes one fp32 row per (token, slot); combine applies the gate weights and
 // sums a token's k slots, then the shared expert, in a fixed order.
 #include "device.hpp"
 #include "launch.hpp"
 
-// Compile-time tuning: macro steps in flight per wavefront (ring depth) for
-// items of <= 16 tokens (PD1) and of up to 64 tokens (PD4), per format.
-#ifndef ECOSPEC_PD1_BF16
-#define ECOSPEC_PD1_BF16 4
+// Compile-time tuning: macro steps in flight per wavefront, per format.
+#ifndef ECOSPEC_PD_BF16
+#define ECOSPEC_PD_BF16 3
 #endif
-#ifndef ECOSPEC_PD1_FP8
-#define ECOSPEC_PD1_FP8 6
+#ifndef ECOSPEC_PD_FP8
+#define ECOSPEC_PD_FP8 3
 #endif
-#ifndef ECOSPEC_PD1_FP4
-#define ECOSPEC_PD1_FP4 8
+#ifndef ECOSPEC_PD_FP4
+#define ECOSPEC_PD_FP4 6
 #endif
-#ifndef ECOSPEC_PD4_BF16
-#define ECOSPEC_PD4_BF16 2
-#endif
-#ifndef ECOSPEC_PD4_FP8
-#define ECOSPEC_PD4_FP8 3
-#endif
-#ifndef ECOSPEC_PD4_FP4
-#define ECOSPEC_PD4_FP4 3
+#ifndef ECOSPEC_WG_PER_CU
+#define ECOSPEC_WG_PER_CU 2
 #endif
 
 namespace ecospec {
@@ -71,34 +65,39 @@ enum { FMT_BF16 = 0, FMT_FP8 = 1, FMT_MXFP4 = 2 };
 constexpr int kMacroK = 128;            // reduction elements per macro step
 constexpr int kMB = 4;                  // 16-token blocks per item
 constexpr int kTokGroup = 16 * kMB;     // tokens per item
-constexpr int kWavesPerCU = 4;          // one wavefront per SIMD
+constexpr int kWG = 4;                  // wavefronts per workgroup
+constexpr int kThreads = kWG * kWave;
 constexpr uint32_t kOff = 0x80000000u;  // buffer offset beyond every range: the load returns zeros
 constexpr int kAuxNT = 2;               // nontemporal: streamed weights should not displace activations
-constexpr int kPartialFloats = 2 * kMB * 4 * kWave;  // one wavefront's accumulators
+constexpr int kBRow = 256 + 16;         // LDS bytes per activation row of a step (256 + pad against bank conflicts)
+constexpr int kBBuf = kMB * 16 * kBRow; // LDS bytes of one step's activation tile
+constexpr int kPartialFloats = kWG * 2 * kMB * 4 * kWave;  // one workgroup's accumulators
 
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
-// Wave-uniform loads through the constant address space: scalar-memory loads
-// (s_load), counted apart from the vector loads of the weight stream.
-__device__ __forceinline__ int ld_s(const int32_t *p)
-{
-    return *reinterpret_cast<const __attribute__((address_space(4))) int32_t *>(reinterpret_cast<uintptr_t>(p));
-}
-__device__ __forceinline__ float ld_s(const float *p)
-{
-    return *reinterpret_cast<const __attribute__((address_space(4))) float *>(reinterpret_cast<uintptr_t>(p));
-}
-
 // Raw buffer descriptor over [p, p + bytes): loads at offsets >= bytes return 0.
+// The base goes through readfirstlane: descriptors must live in scalar
+// registers, and a descriptor the compiler cannot prove wave-uniform would
+// turn every load into a loop over the distinct values in the wave.
 __device__ __forceinline__ rsrc_t make_rsrc(const void *p, uint32_t bytes)
 {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, (int)bytes, 0x00020000);
+    const uint64_t v = reinterpret_cast<uintptr_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    void *u = reinterpret_cast<void *>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(u, 0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
 }
 
 template <int AUX>
 __device__ __forceinline__ u32x4 load16(rsrc_t r, uint32_t off)
 {
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, AUX));
+}
+
+// Wave-uniform loads through the constant address space (scalar memory).
+__device__ __forceinline__ int ld_s(const int32_t *p)
+{
+    return *reinterpret_cast<const __attribute__((address_space(4))) int32_t *>(reinterpret_cast<uintptr_t>(p));
 }
 
 template <int FMT> struct Fmt;
@@ -144,40 +143,29 @@ __device__ __forceinline__ bf16x8 decode_a(const WFrag<FMT> &f, int s)
     }
 }
 
-// 32 consecutive bf16 activations of one token row: B operand of the 4 sub-steps.
-struct BFrag {
-    u32x4 v[4];
-};
-
 // ----------------------------------------------------------------------------- launch geometry
 
 struct FfnParams {
     VerifyArgs a;
-    int N, K;          // rows and reduction length of one streamed matrix
-    int nsteps;        // macro steps per item: ceil(K / 128)
-    int nbands;        // bands per expert: N / 16 (gate/up) or N / 32 (down)
-    int workers;       // wavefronts of the main kernel's grid
-    float *partials;   // [workers][2][kPartialFloats]
-    const int32_t *plan;  // token groups by class (see gather_kernel)
-    int plan_cap;         // capacity of each group list
+    int N, K;             // rows and reduction length of one streamed matrix
+    int nsteps;           // macro steps per item: ceil(K / 128)
+    int band_rows;        // rows per item: 64 (gate/up) or 128 (down)
+    int nbands;           // bands per expert: ceil(N / band_rows)
+    int workers;          // workgroups of the main kernel's grid
+    float *partials;      // [workers][2][kPartialFloats]
+    const int32_t *plan;  // token groups when T > 64 (else null: one group per expert)
 };
 
-// Token groups of the call, written by the plan block of gather_kernel:
-//   plan[0], plan[1]        number of groups of class 0 (<= 16 tokens) and 1 (17..64 tokens)
-//   plan[8 + c*2*cap + i]   expert position u of group i of class c
-//   plan[8 + c*2*cap + cap + i]  its group index tg within the expert (tokens 64*tg ...)
-// Class-0 groups come first in the unit space, then class-1 groups; a group
-// contributes nbands items of nsteps units each.
+// Distinct experts of the call (+ the shared one) and the number of token groups.
 struct Plan {
-    int U, n0, n1;
+    int U, n_groups;
 };
 
 __device__ __forceinline__ Plan load_plan(const FfnParams &P)
 {
     Plan pl;
     pl.U = ld_s(P.a.n_unique);
-    pl.n0 = ld_s(P.plan);
-    pl.n1 = ld_s(P.plan + 1);
+    pl.n_groups = P.plan ? ld_s(P.plan) : pl.U + (P.a.sh_gate ? 1 : 0);
     return pl;
 }
 
@@ -186,24 +174,24 @@ __device__ __forceinline__ int expert_tokens(const VerifyArgs &a, int u, int U)
     return u < U ? ld_s(a.offsets + u + 1) - ld_s(a.offsets + u) : a.T;
 }
 
-// Unit range [x0, x1) of wavefront w: equal shares of n units.
+// Unit range [x0, x1) of workgroup w: equal shares of n units.
 __device__ __forceinline__ void worker_range(long n, int w, int workers, long &x0, long &x1)
 {
     x0 = n * w / workers;
     x1 = n * (w + 1) / workers;
 }
 
-// Wavefront whose range holds unit x.
+// Workgroup whose range holds unit x.
 __device__ __forceinline__ int owner_of(long n, long x, int workers)
 {
     return (int)(((x + 1) * workers - 1) / n);
 }
 
-// What a wavefront needs to know about one item.
+// What a workgroup needs to know about one item.
 struct ItemDesc {
     const uint8_t *wa, *wb;  // tile 0 / tile 1 matrices of the expert (packed)
     const void *sa, *sb;     // their scales
-    int rb0, rb1;            // block rows of tile 0 / tile 1
+    int n0;                  // first row of the band
     int p0;                  // grouped position of the group's first token
     int M;                   // tokens in the group (<= 64)
     bool shared;
@@ -213,12 +201,12 @@ template <bool DOWN>
 __device__ __forceinline__ ItemDesc describe(const FfnParams &P, const Plan &pl, int item)
 {
     const VerifyArgs &a = P.a;
-    const int i0 = pl.n0 * P.nbands;
-    const int cls = item >= i0 ? 1 : 0;
-    const int local = item - cls * i0;
-    const int gi = local / P.nbands, band = local - gi * P.nbands;
-    const int32_t *lst = P.plan + 8 + cls * 2 * P.plan_cap;
-    const int u = ld_s(lst + gi), tg = ld_s(lst + P.plan_cap + gi);
+    const int gi = item / P.nbands, band = item - gi * P.nbands;
+    int u = gi, tg = 0;
+    if (P.plan) {
+        u = ld_s(P.plan + 8 + 2 * gi);
+        tg = ld_s(P.plan + 8 + 2 * gi + 1);
+    }
     const int fmt = a.fmt;
     const size_t kp = (size_t)P.nsteps * kMacroK;
     const size_t mat = (size_t)P.N * kp * (fmt == FMT_BF16 ? 2 : 1) / (fmt == FMT_MXFP4 ? 2 : 1);
@@ -228,6 +216,7 @@ __device__ __forceinline__ ItemDesc describe(const FfnParams &P, const Plan &pl,
     const int M = expert_tokens(a, u, pl.U);
     d.p0 = (d.shared ? a.T * a.k : ld_s(a.offsets + u)) + tg * kTokGroup;
     d.M = min(kTokGroup, M - tg * kTokGroup);
+    d.n0 = band * P.band_rows;
     const size_t e = d.shared ? 0 : (size_t)ld_s(a.union_ids + u);
     auto sptr = [&](const void *base) {
         return base ? static_cast<const void *>(static_cast<const uint8_t *>(base) + e * sc) : nullptr;
@@ -237,29 +226,36 @@ __device__ __forceinline__ ItemDesc describe(const FfnParams &P, const Plan &pl,
         d.wb = (d.shared ? a.sh_up : a.w_up) + e * mat;
         d.sa = d.shared ? a.sh_s_gate : sptr(a.s_gate);
         d.sb = d.shared ? a.sh_s_up : sptr(a.s_up);
-        d.rb0 = d.rb1 = band;
     } else {
         d.wa = d.wb = (d.shared ? a.sh_down : a.w_down) + e * mat;
         d.sa = d.sb = d.shared ? a.sh_s_down : sptr(a.s_down);
-        d.rb0 = 2 * band;
-        d.rb1 = 2 * band + 1;
     }
     return d;
 }
 
+// Rows of wavefront `wave`'s two tiles within an item (the same 16 rows of
+// gate and up, or 32 consecutive rows of down).
+template <bool DOWN>
+__device__ __forceinline__ int tile_row(const ItemDesc &d, int wave, int t)
+{
+    return DOWN ? d.n0 + 32 * wave + 16 * t : d.n0 + 16 * wave;
+}
+
 // ----------------------------------------------------------------------------- epilogue
 
-// Finishes the (tile 0, tile 1) accumulators of an item: gate/up -> bf16
-// SwiGLU rows of H; down -> fp32 rows of O (both at grouped positions).
-// Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for token column col.
-template <bool DOWN, int MB>
-__device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &d, int band,
-                                            const f32x4 (&acc)[2][MB])
+// Finishes a wavefront's (tile 0, tile 1) accumulators of an item: gate/up ->
+// bf16 SwiGLU rows of H at grouped positions; down -> fp32 rows of O at the
+// token's slot.  Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for
+// token column col of each 16-token block.
+template <bool DOWN>
+__device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &d, int wave,
+                                            const f32x4 (&acc)[2][kMB])
 {
     const VerifyArgs &a = P.a;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
+    if (tile_row<DOWN>(d, wave, 0) >= P.N) return;  // rows past the last band
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
+    for (int mb = 0; mb < kMB; ++mb) {
         const int r = mb * 16 + col;
         if (r >= d.M) continue;
         const int p = d.p0 + r;
@@ -271,216 +267,208 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
                 const float g0 = g[2 * i], g1 = g[2 * i + 1];
                 h2[i] = pack_bf16x2(g0 / (1.f + expf(-g0)) * v[2 * i], g1 / (1.f + expf(-g1)) * v[2 * i + 1]);
             }
-            *reinterpret_cast<u32x2 *>(a.h + (size_t)p * a.d_ff + band * 16 + 4 * grp) = u32x2{h2[0], h2[1]};
+            *reinterpret_cast<u32x2 *>(a.h + (size_t)p * a.d_ff + tile_row<DOWN>(d, wave, 0) + 4 * grp) =
+                u32x2{h2[0], h2[1]};
         } else {
+            const int slot = d.shared ? p : a.perm[p];
 #pragma unroll
             for (int t = 0; t < 2; ++t)
-                *reinterpret_cast<f32x4 *>(a.o + (size_t)p * a.d + band * 32 + t * 16 + 4 * grp) = acc[t][mb];
+                *reinterpret_cast<f32x4 *>(a.o + (size_t)slot * a.d + tile_row<DOWN>(d, wave, t) + 4 * grp) =
+                    acc[t][mb];
         }
     }
 }
 
 // ----------------------------------------------------------------------------- main kernel
 
-// Streams units [xs, xe) (all in one token-group class, MB 16-token blocks)
-// of wavefront w, whose whole range is [x0, x1).  A and B operands of a unit
-// are issued together, PD-1 units ahead of the unit being computed: the
-// vector-memory counter retires loads in issue order, so loads must be
-// consumed in the order they were issued for the prefetch to stay deep.
-template <int FMT, bool DOWN, int MB, int PD>
-__device__ __forceinline__ void run_range(const FfnParams &P, const Plan &pl, long xs, long xe, long x0, long x1,
-                                          int w)
+// One item's steps [s0, s1): every wavefront streams its two weight tiles;
+// the workgroup stages each step's activation tile in LDS.
+template <int FMT, bool DOWN, int PD>
+__device__ __forceinline__ void run_item(const FfnParams &P, const ItemDesc &d, int s0, int s1,
+                                         f32x4 (&acc)[2][kMB], uint8_t *lds)
 {
     constexpr int NV = Fmt<FMT>::kVecs;
     constexpr uint32_t BLK = 1024u * NV;  // bytes of one 16 x 128 block
     const VerifyArgs &a = P.a;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int K = P.K, nsteps = P.nsteps;
+    const int nmb = (d.M + 15) / 16;
 
-    // B rows at grouped positions: xg (gate/up) or H (down).
-    const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
-    const uint32_t n_rows = (uint32_t)(a.T * a.k + (a.sh_gate ? a.T : 0));
-    const rsrc_t rbuf = make_rsrc(DOWN ? (const void *)a.h : (const void *)a.xg, n_rows * brow_bytes);
+    // A: this wavefront's two tiles (zeros if past the last row).
     const uint32_t mat_bytes =
         (uint32_t)((size_t)P.N * nsteps * kMacroK * (FMT == FMT_BF16 ? 2 : 1) / (FMT == FMT_MXFP4 ? 2 : 1));
-    const uint32_t msc_bytes = (uint32_t)((size_t)P.N * nsteps * 4);  // MXFP4 packed scales
+    const rsrc_t ra0 = make_rsrc(d.wa, mat_bytes), ra1 = make_rsrc(d.wb, mat_bytes);
+    const int row0 = tile_row<DOWN>(d, wave, 0), row1 = tile_row<DOWN>(d, wave, 1);
+    const bool arow_ok = row0 < P.N;
+    const uint32_t a0 = arow_ok ? (uint32_t)(row0 / 16) * nsteps * BLK + lane * 16u : kOff;
+    const uint32_t a1 = arow_ok ? (uint32_t)(row1 / 16) * nsteps * BLK + lane * 16u : kOff;
+    // Scales: FP8 one word per tile and step (every lane reads the same word),
+    // MXFP4 one byte per lane and step.
+    const uint32_t sc_bytes = FMT == FMT_FP8 ? (uint32_t)((P.N / 128) * (K / 128) * 4)
+                                             : (uint32_t)((size_t)P.N * nsteps * 4);
+    const rsrc_t rs0 = make_rsrc(FMT == FMT_BF16 ? d.wa : d.sa, FMT == FMT_BF16 ? 0u : sc_bytes);
+    const rsrc_t rs1 = make_rsrc(FMT == FMT_BF16 ? d.wb : d.sb, FMT == FMT_BF16 ? 0u : sc_bytes);
+    uint32_t q0 = 0, q1 = 0;
+    if constexpr (FMT == FMT_FP8) {
+        q0 = arow_ok ? (uint32_t)(row0 / 128) * (K / 128) * 4u : kOff;
+        q1 = arow_ok ? (uint32_t)(row1 / 128) * (K / 128) * 4u : kOff;
+    } else if constexpr (FMT == FMT_MXFP4) {
+        q0 = arow_ok ? (uint32_t)(row0 / 16) * nsteps * 64u + lane : kOff;
+        q1 = arow_ok ? (uint32_t)(row1 / 16) * nsteps * 64u + lane : kOff;
+    }
 
-    // Load cursor (PD-1 units ahead of the compute cursor).  The descriptor of
-    // the item after the load cursor's is fetched one item early, so that its
-    // scalar loads have long landed when the cursor gets there.
-    long xl = xs;
-    int il = (int)(xs / nsteps), sl = (int)(xs - (long)il * nsteps);
-    const int i_last = (int)((xe - 1) / nsteps);
-    ItemDesc dl = describe<DOWN>(P, pl, il);
-    ItemDesc dn = il < i_last ? describe<DOWN>(P, pl, il + 1) : dl;
-    ItemDesc dprev = dl;  // the load cursor's previous item (the compute cursor may still be in it)
-    const uint32_t fsc_bytes = (uint32_t)((P.N / 128) * (K / 128) * 4);  // FP8 scales of one matrix
-    rsrc_t ra0 = make_rsrc(dl.wa, mat_bytes), ra1 = make_rsrc(dl.wb, mat_bytes);
-    rsrc_t rs0 = make_rsrc(dl.sa, FMT == FMT_FP8 ? fsc_bytes : msc_bytes);
-    rsrc_t rs1 = make_rsrc(dl.sb, FMT == FMT_FP8 ? fsc_bytes : msc_bytes);
-    uint32_t boff[MB];
-    auto b_rows = [&]() {
+    // B staging: thread (br, bc) = (tid / 16, tid % 16) loads the 16 bytes bc of
+    // token row mb*16 + br of each step's 256-byte activation chunk.
+    const int tid = threadIdx.x, br = tid >> 4, bc = tid & 15;
+    const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
+    const rsrc_t rb = DOWN ? make_rsrc(a.h, (uint32_t)(a.T * a.k + (a.sh_gate ? a.T : 0)) * brow_bytes)
+                           : make_rsrc(a.x, (uint32_t)a.T * brow_bytes);
+    uint32_t boff[kMB];
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-            const int r = mb * 16 + col;
-            boff[mb] = r < dl.M ? (uint32_t)(dl.p0 + r) * brow_bytes + (uint32_t)grp * 64u : kOff;
+    for (int mb = 0; mb < kMB; ++mb) {
+        const int r = mb * 16 + br;
+        uint32_t row = 0;
+        if (r < d.M) {
+            const int p = d.p0 + r;
+            row = DOWN ? (uint32_t)p : (uint32_t)(d.shared ? p - a.T * a.k : a.perm[p] / a.k);
         }
-    };
-    b_rows();
-    // Compute cursor.
-    int ic = il, sc = sl;
-    ItemDesc dc = dl;
+        boff[mb] = r < d.M ? row * brow_bytes + (uint32_t)bc * 16u : kOff;
+    }
 
     WFrag<FMT> wf[PD][2];
-    BFrag bf[PD][MB];
-    f32x4 acc[2][MB];
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // A, scale and B loads of the load cursor's unit into ring slot `slot`
-    // (all vector-memory loads, retired in issue order); advance the cursor.
-    auto issue = [&](int slot) {
-        const bool ok = xl < xe;
-        const uint32_t o0 = ok ? ((uint32_t)dl.rb0 * nsteps + sl) * BLK + lane * 16u : kOff;
-        const uint32_t o1 = ok ? ((uint32_t)dl.rb1 * nsteps + sl) * BLK + lane * 16u : kOff;
+    u32x4 bst[PD][kMB];
+    auto issue = [&](int slot, int step) {
+        const bool ok = step < s1;
+        const uint32_t so = (uint32_t)step * BLK;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
-            wf[slot][0].v[i] = load16<kAuxNT>(ra0, o0 + 1024u * i);
-            wf[slot][1].v[i] = load16<kAuxNT>(ra1, o1 + 1024u * i);
+            wf[slot][0].v[i] = load16<kAuxNT>(ra0, ok ? a0 + so + 1024u * i : kOff);
+            wf[slot][1].v[i] = load16<kAuxNT>(ra1, ok ? a1 + so + 1024u * i : kOff);
         }
         if constexpr (FMT == FMT_FP8) {
-            // One block scale per tile and step; every lane reads the same word.
-            const uint32_t q0 = ok ? ((uint32_t)(dl.rb0 / 8) * (K / 128) + sl) * 4u : kOff;
-            const uint32_t q1 = ok ? ((uint32_t)(dl.rb1 / 8) * (K / 128) + sl) * 4u : kOff;
-            wf[slot][0].scale = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs0, (int)q0, 0, 0));
-            wf[slot][1].scale = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs1, (int)q1, 0, 0));
+            const uint32_t sso = (uint32_t)step * 4u;
+            wf[slot][0].scale = __builtin_bit_cast(float,
+                                                   __builtin_amdgcn_raw_buffer_load_b32(rs0, (int)(ok ? q0 + sso : kOff), 0, 0));
+            wf[slot][1].scale = __builtin_bit_cast(float,
+                                                   __builtin_amdgcn_raw_buffer_load_b32(rs1, (int)(ok ? q1 + sso : kOff), 0, 0));
         } else if constexpr (FMT == FMT_MXFP4) {
-            const uint32_t q0 = ok ? ((uint32_t)dl.rb0 * nsteps + sl) * 64u + lane : kOff;
-            const uint32_t q1 = ok ? ((uint32_t)dl.rb1 * nsteps + sl) * 64u + lane : kOff;
-            wf[slot][0].scale = e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(rs0, (int)q0, 0, 0));
-            wf[slot][1].scale = e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(rs1, (int)q1, 0, 0));
+            const uint32_t sso = (uint32_t)step * 64u;
+            wf[slot][0].scale = e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(rs0, (int)(ok ? q0 + sso : kOff), 0, 0));
+            wf[slot][1].scale = e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(rs1, (int)(ok ? q1 + sso : kOff), 0, 0));
         }
-        const int k = sl * kMacroK + grp * 32;
+        const bool kok = ok && step * kMacroK + bc * 8 < K;
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-            const uint32_t o = (ok && k < K && boff[mb] != kOff) ? boff[mb] + (uint32_t)sl * (kMacroK * 2) : kOff;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) bf[slot][mb].v[i] = load16<0>(rbuf, o + 16u * i);
-        }
-        ++xl;
-        if (++sl == nsteps && xl < xe) {  // entering the next item
-            sl = 0;
-            ++il;
-            dprev = dl;
-            dl = dn;
-            if (il < i_last) dn = describe<DOWN>(P, pl, il + 1);
-            ra0 = make_rsrc(dl.wa, mat_bytes);
-            ra1 = make_rsrc(dl.wb, mat_bytes);
-            rs0 = make_rsrc(dl.sa, FMT == FMT_FP8 ? fsc_bytes : msc_bytes);
-            rs1 = make_rsrc(dl.sb, FMT == FMT_FP8 ? fsc_bytes : msc_bytes);
-            b_rows();
-        }
+        for (int mb = 0; mb < kMB; ++mb)
+            bst[slot][mb] = load16<0>(rb, (kok && boff[mb] != kOff) ? boff[mb] + (uint32_t)step * 256u : kOff);
     };
 
 #pragma unroll
-    for (int s = 0; s < PD - 1; ++s) issue(s);
+    for (int j = 0; j < PD - 1; ++j) issue(j, s0 + j);
 
-    for (long xc0 = xs; xc0 < xe; xc0 += PD) {
+    for (int st0 = s0; st0 < s1; st0 += PD) {
 #pragma unroll
         for (int j = 0; j < PD; ++j) {
-            const long xc = xc0 + j;
-            if (xc < xe) {
-                issue((j + PD - 1) % PD);
+            const int step = st0 + j;
+            if (step < s1) {
+                issue((j + PD - 1) % PD, step + PD - 1);
+                // Park this step's activation tile: after the barrier of the
+                // previous step no wavefront still reads this buffer.
+                uint8_t *buf = lds + (step & 1) * kBBuf;
+#pragma unroll
+                for (int mb = 0; mb < kMB; ++mb)
+                    *reinterpret_cast<u32x4 *>(buf + (mb * 16 + br) * kBRow + bc * 16) = bst[j][mb];
+                __syncthreads();
                 const WFrag<FMT>(&wv)[2] = wf[j];
-                const BFrag(&bv)[MB] = bf[j];
-                const int nmb = (dc.M + 15) / 16;
-                if constexpr (FMT == FMT_FP8) {
-                    f32x4 part[2][MB];
+                f32x4 part[2][kMB];
 #pragma unroll
-                    for (int s = 0; s < 4; ++s)
+                for (int t = 0; t < 2; ++t)
 #pragma unroll
-                        for (int t = 0; t < 2; ++t) {
-                            const bf16x8 av = decode_a<FMT>(wv[t], s);
+                    for (int mb = 0; mb < kMB; ++mb) part[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                            for (int mb = 0; mb < MB; ++mb)
-                                if (MB == 1 || mb < nmb)
-                                    part[t][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                        av, __builtin_bit_cast(bf16x8, bv[mb].v[s]),
-                                        s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : part[t][mb], 0, 0, 0);
+                for (int s = 0; s < 4; ++s) {
+                    const bf16x8 av0 = decode_a<FMT>(wv[0], s), av1 = decode_a<FMT>(wv[1], s);
+#pragma unroll
+                    for (int mb = 0; mb < kMB; ++mb) {
+                        if (mb < nmb) {
+                            const bf16x8 bv = __builtin_bit_cast(
+                                bf16x8, *reinterpret_cast<const u32x4 *>(buf + (mb * 16 + col) * kBRow + grp * 64 + s * 16));
+                            if constexpr (FMT == FMT_FP8) {
+                                part[0][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av0, bv, part[0][mb], 0, 0, 0);
+                                part[1][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av1, bv, part[1][mb], 0, 0, 0);
+                            } else {
+                                acc[0][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av0, bv, acc[0][mb], 0, 0, 0);
+                                acc[1][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av1, bv, acc[1][mb], 0, 0, 0);
+                            }
                         }
-#pragma unroll
-                    for (int t = 0; t < 2; ++t)
-#pragma unroll
-                        for (int mb = 0; mb < MB; ++mb)
-                            if (MB == 1 || mb < nmb) acc[t][mb] += wv[t].scale * part[t][mb];
-                } else {
-#pragma unroll
-                    for (int s = 0; s < 4; ++s)
-#pragma unroll
-                        for (int t = 0; t < 2; ++t) {
-                            const bf16x8 av = decode_a<FMT>(wv[t], s);
-#pragma unroll
-                            for (int mb = 0; mb < MB; ++mb)
-                                if (MB == 1 || mb < nmb)
-                                    acc[t][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                        av, __builtin_bit_cast(bf16x8, bv[mb].v[s]), acc[t][mb], 0, 0, 0);
-                        }
+                    }
+                    // Keep one sub-step's decoded weights and activations live at a time.
+                    __builtin_amdgcn_sched_barrier(0);
                 }
-                // Last unit of the item inside this range: finish it, or park the partial sums.
-                if (sc == nsteps - 1 || xc == xe - 1) {
-                    const long ib = (long)ic * nsteps;
-                    if (ib >= x0 && ib + nsteps <= x1) {
-                        finish_item<DOWN, MB>(P, dc, ic % P.nbands, acc);
-                    } else {
-                        float *dst = P.partials + ((size_t)w * 2 + (ib <= x0 ? 0 : 1)) * kPartialFloats;
+                if constexpr (FMT == FMT_FP8) {
 #pragma unroll
-                        for (int t = 0; t < 2; ++t)
-#pragma unroll
-                            for (int mb = 0; mb < MB; ++mb)
-                                *reinterpret_cast<f32x4 *>(dst + ((t * kMB + mb) * kWave + lane) * 4) = acc[t][mb];
-                    }
-#pragma unroll
-                    for (int t = 0; t < 2; ++t)
-#pragma unroll
-                        for (int mb = 0; mb < MB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-                    if (xc < xe - 1) {
-                        ++ic;
-                        sc = 0;
-                        dc = ic == il ? dl : ic + 1 == il ? dprev : describe<DOWN>(P, pl, ic);
-                    }
-                } else {
-                    ++sc;
+                    for (int mb = 0; mb < kMB; ++mb)
+                        if (mb < nmb) {
+                            acc[0][mb] += wv[0].scale * part[0][mb];
+                            acc[1][mb] += wv[1].scale * part[1][mb];
+                        }
                 }
             }
         }
     }
+    __syncthreads();  // LDS is reused by the next item
 }
 
-template <int FMT, bool DOWN, int PD1, int PD4>
-__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(1, 1))) void expert_ffn_kernel(FfnParams P)
+template <int FMT, bool DOWN, int PD>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void expert_ffn_kernel(FfnParams P)
 {
+    __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kBBuf];
     const int w = blockIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int lane = lane_id();
     const Plan pl = load_plan(P);
-    const long bound = (long)pl.n0 * P.nbands * P.nsteps;  // first unit of class 1
-    const long n_units = (long)(pl.n0 + pl.n1) * P.nbands * P.nsteps;
+    const long n_units = (long)pl.n_groups * P.nbands * P.nsteps;
     long x0, x1;
     worker_range(n_units, w, P.workers, x0, x1);
-    if (x0 < x1 && x0 < bound) run_range<FMT, DOWN, 1, PD1>(P, pl, x0, x1 < bound ? x1 : bound, x0, x1, w);
-    if (x0 < x1 && x1 > bound) run_range<FMT, DOWN, kMB, PD4>(P, pl, x0 > bound ? x0 : bound, x1, x0, x1, w);
+    const int nsteps = P.nsteps;
+    for (long x = x0; x < x1;) {
+        const int item = (int)(x / nsteps);
+        const long ib = (long)item * nsteps;
+        const int s0 = (int)(x - ib);
+        const int s1 = (int)min((long)nsteps, x1 - ib);
+        const ItemDesc d = describe<DOWN>(P, pl, item);
+        f32x4 acc[2][kMB];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        run_item<FMT, DOWN, PD>(P, d, s0, s1, acc, lds);
+        if (s0 == 0 && s1 == nsteps) {
+            finish_item<DOWN>(P, d, wave, acc);
+        } else {
+            // Cut item: park the partial sums (slot 0: the item holds x0; slot 1: it holds x1-1).
+            float *dst = P.partials + ((size_t)w * 2 + (ib <= x0 ? 0 : 1)) * kPartialFloats;
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int mb = 0; mb < kMB; ++mb)
+                    *reinterpret_cast<f32x4 *>(dst + (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4) = acc[t][mb];
+        }
+        x = ib + s1;
+    }
 }
 
-// Finishes the items cut between wavefronts: the wavefront whose range holds
+// Finishes the items cut between workgroups: the workgroup whose range holds
 // an item's last unit (but not its first) sums the parked partial sums of
-// every owner of the item, in wavefront order.
+// every owner of the item, in workgroup order.
 template <bool DOWN>
-__global__ __launch_bounds__(kWave) void expert_ffn_fixup_kernel(FfnParams P)
+__global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
 {
     const int lane = lane_id();
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int w = blockIdx.x;
     const Plan pl = load_plan(P);
-    const long n_units = (long)(pl.n0 + pl.n1) * P.nbands * P.nsteps;
+    const long n_units = (long)pl.n_groups * P.nbands * P.nsteps;
     long x0, x1;
     worker_range(n_units, w, P.workers, x0, x1);
     if (x0 >= x1) return;
@@ -503,84 +491,49 @@ __global__ __launch_bounds__(kWave) void expert_ffn_fixup_kernel(FfnParams P)
         for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int mb = 0; mb < kMB; ++mb)
-                acc[t][mb] += *reinterpret_cast<const f32x4 *>(src + ((t * kMB + mb) * kWave + lane) * 4);
+                acc[t][mb] += *reinterpret_cast<const f32x4 *>(src + (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4);
     }
-    finish_item<DOWN, kMB>(P, describe<DOWN>(P, pl, item), item % P.nbands, acc);
+    finish_item<DOWN>(P, describe<DOWN>(P, pl, item), wave, acc);
 }
 
-// xg[p] = x[token of the slot at grouped position p] and ip[slot] = p for
-// the routed rows; xg[T*k + t] = x[t] for the shared expert's rows.  One
-// workgroup per row, 16 bytes per thread.  The extra last workgroup writes
-// the token-group plan read by the expert kernels: every expert's tokens in
-// groups of 64, the groups of <= 16 tokens (class 0) listed apart from the
-// others (class 1), each list in expert order.
-__global__ __launch_bounds__(256) void gather_kernel(VerifyArgs a, int32_t *plan, int cap)
+// Token groups when some expert may have more than 64 tokens (T > 64):
+// plan[0] = number of groups; plan[8 + 2i], plan[8 + 2i + 1] = (expert
+// position, group index within the expert) of group i, in expert order.
+__global__ __launch_bounds__(256) void plan_kernel(VerifyArgs a, int32_t *plan)
 {
-    const int routed = a.T * a.k;
-    const int U = ld_s(a.n_unique);
-    if (blockIdx.x == gridDim.x - 1) {
-        __shared__ int wave_tot[256 / kWave];
-        const int n_exp = U + (a.sh_gate ? 1 : 0);
-        int32_t *l0u = plan + 8, *l0t = l0u + cap, *l1u = l0t + cap, *l1t = l1u + cap;
-        int run0 = 0, run1 = 0;
-        for (int base = 0; base < n_exp; base += blockDim.x) {
-            const int u = base + threadIdx.x;
-            int c0 = 0, c1 = 0, ntg = 0;
-            if (u < n_exp) {
-                const int M = u < U ? a.offsets[u + 1] - a.offsets[u] : a.T;
-                ntg = (M + kTokGroup - 1) / kTokGroup;
-                const int last = M - kTokGroup * (ntg - 1);
-                c0 = last <= 16 ? 1 : 0;
-                c1 = ntg - c0;
-            }
-            int t0 = 0, t1 = 0;
-            const int p0 = block_exclusive_scan(c0, wave_tot, &t0);
-            const int p1 = block_exclusive_scan(c1, wave_tot, &t1);
-            if (c0) {
-                l0u[run0 + p0] = u;
-                l0t[run0 + p0] = ntg - 1;
-            }
-            for (int g = 0; g < c1; ++g) {
-                l1u[run1 + p1 + g] = u;
-                l1t[run1 + p1 + g] = g;
-            }
-            run0 += t0;
-            run1 += t1;
+    __shared__ int wave_tot[256 / kWave];
+    const int U = *a.n_unique;
+    const int n_exp = U + (a.sh_gate ? 1 : 0);
+    int run = 0;
+    for (int base = 0; base < n_exp; base += blockDim.x) {
+        const int u = base + threadIdx.x;
+        int n = 0;
+        if (u < n_exp) {
+            const int M = u < U ? a.offsets[u + 1] - a.offsets[u] : a.T;
+            n = (M + kTokGroup - 1) / kTokGroup;
         }
-        if (threadIdx.x == 0) {
-            plan[0] = run0;
-            plan[1] = run1;
+        int tot = 0;
+        const int pos = block_exclusive_scan(n, wave_tot, &tot);
+        for (int g = 0; g < n; ++g) {
+            plan[8 + 2 * (run + pos + g)] = u;
+            plan[8 + 2 * (run + pos + g) + 1] = g;
         }
-        return;
+        run += tot;
     }
-    const int p = blockIdx.x;
-    int t;
-    if (p < routed) {
-        if (p >= a.offsets[U]) return;  // unfilled position (out-of-range routing entries)
-        const int slot = a.perm[p];
-        t = slot / a.k;
-        if (threadIdx.x == 0) a.ip[slot] = p;
-    } else {
-        t = p - routed;
-    }
-    const u32x4 *src = reinterpret_cast<const u32x4 *>(a.x + (size_t)t * a.d);
-    u32x4 *dst = reinterpret_cast<u32x4 *>(a.xg + (size_t)p * a.d);
-    for (int i = threadIdx.x; i < a.d / 8; i += blockDim.x) dst[i] = src[i];
+    if (threadIdx.x == 0) plan[0] = run;
 }
 
-// y[t] = sum_j w[t][j] * O[ip[t*k + j]] (+ O[T*k + t]) -> bf16; 4 columns per thread.
+// y[t] = sum_j w[t][j] * O[t*k + j] (+ O[T*k + t]) -> bf16; 4 columns per thread.
 __global__ __launch_bounds__(256) void combine_kernel(VerifyArgs a)
 {
     const int per_row = a.d / 4;
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= a.T * per_row) return;
     const int t = i / per_row, c = (i - t * per_row) * 4;
-    const uint32_t rows = (uint32_t)(a.T * a.k + (a.sh_gate ? a.T : 0));
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int j = 0; j < a.k; ++j) {
         const int slot = t * a.k + j;
-        const uint32_t p = (uint32_t)a.ip[slot];
-        if (p < rows) s += a.topk_w[slot] * *reinterpret_cast<const f32x4 *>(a.o + (size_t)p * a.d + c);
+        s += a.topk_w[slot] * *reinterpret_cast<const f32x4 *>(a.o + (size_t)slot * a.d + c);
     }
     if (a.sh_gate) s += *reinterpret_cast<const f32x4 *>(a.o + (size_t)(a.T * a.k + t) * a.d + c);
     *reinterpret_cast<u32x2 *>(a.y + (size_t)t * a.d + c) = u32x2{pack_bf16x2(s[0], s[1]), pack_bf16x2(s[2], s[3])};
@@ -605,12 +558,12 @@ static int device_cus()
 
 static int workers()
 {
-    const int w = device_cus() * kWavesPerCU;
+    const int w = device_cus() * ECOSPEC_WG_PER_CU;
     return w < kMaxWorkers ? w : kMaxWorkers;
 }
 
-// Token groups an expert list can hold: one per expert (<= 1024 routed + 1
-// shared) plus one per extra 64 tokens.
+// Token groups a plan can hold: one per expert (<= 1024 routed + 1 shared)
+// plus one per extra 64 tokens.
 static int plan_capacity(int T, int k, bool shared)
 {
     const long rows = (long)T * k + (shared ? T : 0);
@@ -628,13 +581,9 @@ VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared)
     w.o_bytes = rows * d * 4;
     w.p_offset = w.o_offset + align(w.o_bytes);
     w.p_bytes = (size_t)kMaxWorkers * 2 * kPartialFloats * 4;
-    w.x_offset = w.p_offset + align(w.p_bytes);
-    w.x_bytes = rows * d * 2;
-    w.i_offset = w.x_offset + align(w.x_bytes);
-    w.i_bytes = (size_t)T * k * 4;
     w.plan_cap = plan_capacity(T, k, shared);
-    w.plan_offset = w.i_offset + align(w.i_bytes);
-    w.plan_bytes = (8 + 4 * (size_t)w.plan_cap) * 4;
+    w.plan_offset = w.p_offset + align(w.p_bytes);
+    w.plan_bytes = (8 + 2 * (size_t)w.plan_cap) * 4;
     w.total = w.plan_offset + align(w.plan_bytes);
     return w;
 }
@@ -645,42 +594,44 @@ static hipError_t mark(hipEvent_t const *events, int i, hipStream_t stream)
 }
 
 template <int FMT>
-static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan, int plan_cap, hipStream_t stream,
+static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan, hipStream_t stream,
                              hipEvent_t const *events)
 {
-    constexpr int PD1 = FMT == FMT_BF16 ? ECOSPEC_PD1_BF16 : FMT == FMT_FP8 ? ECOSPEC_PD1_FP8 : ECOSPEC_PD1_FP4;
-    constexpr int PD4 = FMT == FMT_BF16 ? ECOSPEC_PD4_BF16 : FMT == FMT_FP8 ? ECOSPEC_PD4_FP8 : ECOSPEC_PD4_FP4;
+    constexpr int PD = FMT == FMT_BF16 ? ECOSPEC_PD_BF16 : FMT == FMT_FP8 ? ECOSPEC_PD_FP8 : ECOSPEC_PD_FP4;
     const int G = workers();
+    const bool grouped = a.T > kTokGroup;  // some expert may need several token groups
     hipError_t err;
 
+    if ((err = mark(events, 0, stream)) != hipSuccess) return err;
+    if (grouped) {
+        hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(256), 0, stream, a, plan);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
     FfnParams g{};
     g.a = a;
     g.N = a.d_ff;
     g.K = a.d;
     g.nsteps = (a.d + kMacroK - 1) / kMacroK;
-    g.nbands = a.d_ff / 16;
+    g.band_rows = 16 * kWG;
+    g.nbands = (a.d_ff + g.band_rows - 1) / g.band_rows;
     g.workers = G;
     g.partials = partials;
-    g.plan = plan;
-    g.plan_cap = plan_cap;
-    const int rows = a.T * a.k + (a.sh_gate ? a.T : 0);
-    if ((err = mark(events, 0, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL(gather_kernel, dim3(rows + 1), dim3(256), 0, stream, a, plan, plan_cap);
+    g.plan = grouped ? plan : nullptr;
+    hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD1, PD4>), dim3(G), dim3(kWave), 0, stream, g);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false>), dim3(G), dim3(kWave), 0, stream, g);
+    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     FfnParams dn = g;
     dn.N = a.d;
     dn.K = a.d_ff;
     dn.nsteps = (a.d_ff + kMacroK - 1) / kMacroK;
-    dn.nbands = a.d / 32;
+    dn.band_rows = 32 * kWG;
+    dn.nbands = (a.d + dn.band_rows - 1) / dn.band_rows;
     if ((err = mark(events, 1, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD1, PD4>), dim3(G), dim3(kWave), 0, stream, dn);
+    hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<true>), dim3(G), dim3(kWave), 0, stream, dn);
+    hipLaunchKernelGGL((expert_ffn_fixup_kernel<true>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     const int n = a.T * (a.d / 4);
@@ -693,10 +644,11 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
 hipError_t launch_verify(const VerifyArgs &a, float *partials, int32_t *plan, int plan_cap, hipStream_t stream,
                          hipEvent_t const *events)
 {
+    (void)plan_cap;
     switch (a.fmt) {
-    case FMT_BF16: return launch_fmt<FMT_BF16>(a, partials, plan, plan_cap, stream, events);
-    case FMT_FP8: return launch_fmt<FMT_FP8>(a, partials, plan, plan_cap, stream, events);
-    case FMT_MXFP4: return launch_fmt<FMT_MXFP4>(a, partials, plan, plan_cap, stream, events);
+    case FMT_BF16: return launch_fmt<FMT_BF16>(a, partials, plan, stream, events);
+    case FMT_FP8: return launch_fmt<FMT_FP8>(a, partials, plan, stream, events);
+    case FMT_MXFP4: return launch_fmt<FMT_MXFP4>(a, partials, plan, stream, events);
     default: return hipErrorInvalidValue;
     }
 }

@@ -25,20 +25,17 @@ struct VerifyArgs {
     const int32_t *union_ids, *n_unique, *offsets, *perm;
     const uint16_t *x;  // [T][d] bf16
     uint16_t *y;        // [T][d] bf16
-    uint16_t *h;        // workspace: [T*k (+T)][d_ff] bf16 SwiGLU rows, grouped positions
-    float *o;           // workspace: [T*k (+T)][d] fp32 expert outputs, grouped positions
-    uint16_t *xg;       // workspace: [T*k (+T)][d] bf16 x rows in grouped order
-    int32_t *ip;        // workspace: [T*k] grouped position of each slot (inverse of perm)
+    uint16_t *h;        // workspace: [T*k (+T)][d_ff] bf16 SwiGLU rows at grouped positions
+    float *o;           // workspace: [T*k (+T)][d] fp32 expert outputs at slots (shared: T*k + t)
 };
 
-// Upper bound on the wavefronts of a verify grid (sizes the partial-sum slots).
-constexpr int kMaxWorkers = 2048;
+// Upper bound on the workgroups of a verify grid (sizes the partial-sum slots).
+constexpr int kMaxWorkers = 1024;
 
 // Workspace layout shared by the size query and the launcher: H (bf16 SwiGLU
 // rows), O (fp32 per-slot expert outputs), partial sums of cut work items.
 struct VerifyWorkspace {
-    size_t h_offset, h_bytes, o_offset, o_bytes, p_offset, p_bytes, x_offset, x_bytes, i_offset, i_bytes;
-    size_t plan_offset, plan_bytes;
+    size_t h_offset, h_bytes, o_offset, o_bytes, p_offset, p_bytes, plan_offset, plan_bytes;
     int plan_cap;
     size_t total;
 };
