@@ -5,15 +5,17 @@
 // tokens routed to its expert (at most 2*M_u flop per weight).  The kernels
 // are weight streams with a small matrix-core contraction attached.
 //
-// Workgroups.  Four wavefronts share one band of rows of one expert and one
-// group of up to 64 of its tokens (an item): gate/up bands are 64 rows of
-// W_gate with the same 64 rows of W_up (16 + 16 per wavefront), down bands
-// are 128 rows of W_down (32 per wavefront).  All four walk the reduction
-// dimension together in macro steps of 128 elements, so the activation tile
-// of a step (the item's tokens x 128 elements) is fetched from L2 once, by
-// one coalesced 16-byte load per thread, parked in LDS and read by every
-// wavefront: activation traffic is a quarter of the weight traffic at 16
-// tokens instead of equal to it.
+// Workgroups.  One workgroup per compute unit, eight wavefronts (two per
+// SIMD), all on one band of rows of one expert and one group of up to 64 of
+// its tokens (an item): gate/up bands are 128 rows of W_gate with the same
+// 128 rows of W_up (16 + 16 per wavefront), down bands are 256 rows of W_down
+// (32 per wavefront).  All eight walk the reduction dimension together in
+// macro steps of 128 elements, so the activation tile of a step (the item's
+// tokens x 128 elements) is fetched from L2 once, by coalesced 16-byte loads,
+// parked in LDS and read by every wavefront.  A single workgroup per CU keeps
+// the CU's waves in lockstep: two workgroups sharing a CU drift apart (the
+// older one wins instruction issue), which leaves the younger one's share of
+// an equal split running alone at the end of the launch.
 //
 // Streaming.  Weights are read in the packed layout (pack.hip): each macro
 // step of a 16-row tile is 1-4 KiB of contiguous memory, fetched with 16-byte
@@ -46,16 +48,19 @@
 
 // Compile-time tuning: macro steps in flight per wavefront, per format.
 #ifndef ECOSPEC_PD_BF16
-#define ECOSPEC_PD_BF16 3
+#define ECOSPEC_PD_BF16 2
 #endif
 #ifndef ECOSPEC_PD_FP8
 #define ECOSPEC_PD_FP8 3
 #endif
 #ifndef ECOSPEC_PD_FP4
-#define ECOSPEC_PD_FP4 6
+#define ECOSPEC_PD_FP4 3
+#endif
+#ifndef ECOSPEC_WG_WAVES
+#define ECOSPEC_WG_WAVES 8
 #endif
 #ifndef ECOSPEC_WG_PER_CU
-#define ECOSPEC_WG_PER_CU 2
+#define ECOSPEC_WG_PER_CU 1
 #endif
 
 namespace ecospec {
@@ -65,8 +70,10 @@ enum { FMT_BF16 = 0, FMT_FP8 = 1, FMT_MXFP4 = 2 };
 constexpr int kMacroK = 128;            // reduction elements per macro step
 constexpr int kMB = 4;                  // 16-token blocks per item
 constexpr int kTokGroup = 16 * kMB;     // tokens per item
-constexpr int kWG = 4;                  // wavefronts per workgroup
+constexpr int kWG = ECOSPEC_WG_WAVES;   // wavefronts per workgroup
 constexpr int kThreads = kWG * kWave;
+constexpr int kBRowsPerPass = kThreads / 16;         // activation rows staged per pass (16 threads per row)
+constexpr int kBPass = kTokGroup / kBRowsPerPass;    // passes per step
 constexpr uint32_t kOff = 0x80000000u;  // buffer offset beyond every range: the load returns zeros
 constexpr int kAuxNT = 2;               // nontemporal: streamed weights should not displace activations
 constexpr int kBRow = 256 + 16;         // LDS bytes per activation row of a step (256 + pad against bank conflicts)
@@ -119,6 +126,9 @@ __device__ __forceinline__ float e8m0_to_f32(uint32_t code)
 }
 
 // bf16 A operand of sub-step s (the lane's weights 8s .. 8s+7 of the step).
+// Exact: FP8 codes as they are (the converter's scale operand only takes a
+// power of two, so the 128x128 block scale multiplies the fp32 partial sum of
+// the step instead); MXFP4 codes times their 2^e8m0 group scale.
 template <int FMT>
 __device__ __forceinline__ bf16x8 decode_a(const WFrag<FMT> &f, int s)
 {
@@ -243,6 +253,19 @@ __device__ __forceinline__ int tile_row(const ItemDesc &d, int wave, int t)
 
 // ----------------------------------------------------------------------------- epilogue
 
+// v[c] for c = `col` (0..15), from wave-uniform scalar loads of v[0 .. n-1]
+// (entries c >= n read as 0).
+__device__ __forceinline__ int lane_select16(const int32_t *v, int n, int col)
+{
+    int r = 0;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+        const int s = c < n ? ld_s(v + c) : 0;
+        r = col == c ? s : r;
+    }
+    return r;
+}
+
 // Finishes a wavefront's (tile 0, tile 1) accumulators of an item: gate/up ->
 // bf16 SwiGLU rows of H at grouped positions; down -> fp32 rows of O at the
 // token's slot.  Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for
@@ -254,6 +277,14 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
     const VerifyArgs &a = P.a;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
     if (tile_row<DOWN>(d, wave, 0) >= P.N) return;  // rows past the last band
+    // Down: the slot of each token column, read through the scalar unit (a
+    // vector load here would wait behind every weight load in flight).
+    int slots[kMB] = {};
+    if (DOWN && !d.shared) {
+#pragma unroll
+        for (int mb = 0; mb < kMB; ++mb)
+            if (mb * 16 < d.M) slots[mb] = lane_select16(a.perm + d.p0 + mb * 16, d.M - mb * 16, col);
+    }
 #pragma unroll
     for (int mb = 0; mb < kMB; ++mb) {
         const int r = mb * 16 + col;
@@ -270,7 +301,7 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
             *reinterpret_cast<u32x2 *>(a.h + (size_t)p * a.d_ff + tile_row<DOWN>(d, wave, 0) + 4 * grp) =
                 u32x2{h2[0], h2[1]};
         } else {
-            const int slot = d.shared ? p : a.perm[p];
+            const int slot = d.shared ? p : slots[mb];
 #pragma unroll
             for (int t = 0; t < 2; ++t)
                 *reinterpret_cast<f32x4 *>(a.o + (size_t)slot * a.d + tile_row<DOWN>(d, wave, t) + 4 * grp) =
@@ -281,180 +312,240 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
 
 // ----------------------------------------------------------------------------- main kernel
 
-// One item's steps [s0, s1): every wavefront streams its two weight tiles;
-// the workgroup stages each step's activation tile in LDS.
-template <int FMT, bool DOWN, int PD>
-__device__ __forceinline__ void run_item(const FfnParams &P, const ItemDesc &d, int s0, int s1,
-                                         f32x4 (&acc)[2][kMB], uint8_t *lds)
+// Where the loads of one item come from.  Wave-uniform except the lane offsets.
+struct Source {
+    rsrc_t ra0, ra1, rs0, rs1;  // weight tiles 0 / 1 and their scales
+    uint32_t a0, a1;            // lane offsets of the two tiles at step 0 (kOff: rows past N)
+    uint32_t q0, q1;            // scale offsets at step 0
+    uint32_t boff[kBPass];      // lane offsets of this thread's activation rows at step 0 (kOff: no token)
+    long ib, ie;                // the item's units [ib, ie)
+    int item;
+};
+
+template <int FMT, bool DOWN>
+__device__ __forceinline__ void set_source(Source &src, const FfnParams &P, const Plan &pl, int item)
 {
     constexpr int NV = Fmt<FMT>::kVecs;
-    constexpr uint32_t BLK = 1024u * NV;  // bytes of one 16 x 128 block
+    constexpr uint32_t BLK = 1024u * NV;
     const VerifyArgs &a = P.a;
-    const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
+    const int lane = lane_id(), tid = threadIdx.x, bc = tid & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int K = P.K, nsteps = P.nsteps;
-    const int nmb = (d.M + 15) / 16;
+    const ItemDesc d = describe<DOWN>(P, pl, item);
+    src.item = item;
+    src.ib = (long)item * nsteps;
+    src.ie = src.ib + nsteps;
 
-    // A: this wavefront's two tiles (zeros if past the last row).
     const uint32_t mat_bytes =
         (uint32_t)((size_t)P.N * nsteps * kMacroK * (FMT == FMT_BF16 ? 2 : 1) / (FMT == FMT_MXFP4 ? 2 : 1));
-    const rsrc_t ra0 = make_rsrc(d.wa, mat_bytes), ra1 = make_rsrc(d.wb, mat_bytes);
+    src.ra0 = make_rsrc(d.wa, mat_bytes);
+    src.ra1 = make_rsrc(d.wb, mat_bytes);
     const int row0 = tile_row<DOWN>(d, wave, 0), row1 = tile_row<DOWN>(d, wave, 1);
     const bool arow_ok = row0 < P.N;
-    const uint32_t a0 = arow_ok ? (uint32_t)(row0 / 16) * nsteps * BLK + lane * 16u : kOff;
-    const uint32_t a1 = arow_ok ? (uint32_t)(row1 / 16) * nsteps * BLK + lane * 16u : kOff;
-    // Scales: FP8 one word per tile and step (every lane reads the same word),
-    // MXFP4 one byte per lane and step.
+    src.a0 = arow_ok ? (uint32_t)(row0 / 16) * nsteps * BLK + lane * 16u : kOff;
+    src.a1 = arow_ok ? (uint32_t)(row1 / 16) * nsteps * BLK + lane * 16u : kOff;
     const uint32_t sc_bytes = FMT == FMT_FP8 ? (uint32_t)((P.N / 128) * (K / 128) * 4)
                                              : (uint32_t)((size_t)P.N * nsteps * 4);
-    const rsrc_t rs0 = make_rsrc(FMT == FMT_BF16 ? d.wa : d.sa, FMT == FMT_BF16 ? 0u : sc_bytes);
-    const rsrc_t rs1 = make_rsrc(FMT == FMT_BF16 ? d.wb : d.sb, FMT == FMT_BF16 ? 0u : sc_bytes);
-    uint32_t q0 = 0, q1 = 0;
+    src.rs0 = make_rsrc(FMT == FMT_BF16 ? d.wa : d.sa, FMT == FMT_BF16 ? 0u : sc_bytes);
+    src.rs1 = make_rsrc(FMT == FMT_BF16 ? d.wb : d.sb, FMT == FMT_BF16 ? 0u : sc_bytes);
+    src.q0 = src.q1 = 0;
     if constexpr (FMT == FMT_FP8) {
-        q0 = arow_ok ? (uint32_t)(row0 / 128) * (K / 128) * 4u : kOff;
-        q1 = arow_ok ? (uint32_t)(row1 / 128) * (K / 128) * 4u : kOff;
+        src.q0 = arow_ok ? (uint32_t)(row0 / 128) * (K / 128) * 4u : kOff;
+        src.q1 = arow_ok ? (uint32_t)(row1 / 128) * (K / 128) * 4u : kOff;
     } else if constexpr (FMT == FMT_MXFP4) {
-        q0 = arow_ok ? (uint32_t)(row0 / 16) * nsteps * 64u + lane : kOff;
-        q1 = arow_ok ? (uint32_t)(row1 / 16) * nsteps * 64u + lane : kOff;
+        src.q0 = arow_ok ? (uint32_t)(row0 / 16) * nsteps * 64u + lane : kOff;
+        src.q1 = arow_ok ? (uint32_t)(row1 / 16) * nsteps * 64u + lane : kOff;
     }
 
-    // B staging: thread (br, bc) = (tid / 16, tid % 16) loads the 16 bytes bc of
-    // token row mb*16 + br of each step's 256-byte activation chunk.
-    const int tid = threadIdx.x, br = tid >> 4, bc = tid & 15;
+    // Activation rows: in pass i this wavefront stages rows i*kBRowsPerPass +
+    // 4*wave + q, q = lane / 16.  Their source rows (token of a grouped
+    // position for gate/up, the grouped position itself for down) are read
+    // through the scalar unit.
     const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
-    const rsrc_t rb = DOWN ? make_rsrc(a.h, (uint32_t)(a.T * a.k + (a.sh_gate ? a.T : 0)) * brow_bytes)
-                           : make_rsrc(a.x, (uint32_t)a.T * brow_bytes);
-    uint32_t boff[kMB];
+    const int q = lane >> 4;
 #pragma unroll
-    for (int mb = 0; mb < kMB; ++mb) {
-        const int r = mb * 16 + br;
-        uint32_t row = 0;
-        if (r < d.M) {
-            const int p = d.p0 + r;
-            row = DOWN ? (uint32_t)p : (uint32_t)(d.shared ? p - a.T * a.k : a.perm[p] / a.k);
-        }
-        boff[mb] = r < d.M ? row * brow_bytes + (uint32_t)bc * 16u : kOff;
-    }
-
-    WFrag<FMT> wf[PD][2];
-    u32x4 bst[PD][kMB];
-    auto issue = [&](int slot, int step) {
-        const bool ok = step < s1;
-        const uint32_t so = (uint32_t)step * BLK;
+    for (int i = 0; i < kBPass; ++i) {
+        int row = -1;
 #pragma unroll
-        for (int i = 0; i < NV; ++i) {
-            wf[slot][0].v[i] = load16<kAuxNT>(ra0, ok ? a0 + so + 1024u * i : kOff);
-            wf[slot][1].v[i] = load16<kAuxNT>(ra1, ok ? a1 + so + 1024u * i : kOff);
-        }
-        if constexpr (FMT == FMT_FP8) {
-            const uint32_t sso = (uint32_t)step * 4u;
-            wf[slot][0].scale = __builtin_bit_cast(float,
-                                                   __builtin_amdgcn_raw_buffer_load_b32(rs0, (int)(ok ? q0 + sso : kOff), 0, 0));
-            wf[slot][1].scale = __builtin_bit_cast(float,
-                                                   __builtin_amdgcn_raw_buffer_load_b32(rs1, (int)(ok ? q1 + sso : kOff), 0, 0));
-        } else if constexpr (FMT == FMT_MXFP4) {
-            const uint32_t sso = (uint32_t)step * 64u;
-            wf[slot][0].scale = e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(rs0, (int)(ok ? q0 + sso : kOff), 0, 0));
-            wf[slot][1].scale = e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(rs1, (int)(ok ? q1 + sso : kOff), 0, 0));
-        }
-        const bool kok = ok && step * kMacroK + bc * 8 < K;
-#pragma unroll
-        for (int mb = 0; mb < kMB; ++mb)
-            bst[slot][mb] = load16<0>(rb, (kok && boff[mb] != kOff) ? boff[mb] + (uint32_t)step * 256u : kOff);
-    };
-
-#pragma unroll
-    for (int j = 0; j < PD - 1; ++j) issue(j, s0 + j);
-
-    for (int st0 = s0; st0 < s1; st0 += PD) {
-#pragma unroll
-        for (int j = 0; j < PD; ++j) {
-            const int step = st0 + j;
-            if (step < s1) {
-                issue((j + PD - 1) % PD, step + PD - 1);
-                // Park this step's activation tile: after the barrier of the
-                // previous step no wavefront still reads this buffer.
-                uint8_t *buf = lds + (step & 1) * kBBuf;
-#pragma unroll
-                for (int mb = 0; mb < kMB; ++mb)
-                    *reinterpret_cast<u32x4 *>(buf + (mb * 16 + br) * kBRow + bc * 16) = bst[j][mb];
-                __syncthreads();
-                const WFrag<FMT>(&wv)[2] = wf[j];
-                f32x4 part[2][kMB];
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int mb = 0; mb < kMB; ++mb) part[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    const bf16x8 av0 = decode_a<FMT>(wv[0], s), av1 = decode_a<FMT>(wv[1], s);
-#pragma unroll
-                    for (int mb = 0; mb < kMB; ++mb) {
-                        if (mb < nmb) {
-                            const bf16x8 bv = __builtin_bit_cast(
-                                bf16x8, *reinterpret_cast<const u32x4 *>(buf + (mb * 16 + col) * kBRow + grp * 64 + s * 16));
-                            if constexpr (FMT == FMT_FP8) {
-                                part[0][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av0, bv, part[0][mb], 0, 0, 0);
-                                part[1][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av1, bv, part[1][mb], 0, 0, 0);
-                            } else {
-                                acc[0][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av0, bv, acc[0][mb], 0, 0, 0);
-                                acc[1][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av1, bv, acc[1][mb], 0, 0, 0);
-                            }
-                        }
-                    }
-                    // Keep one sub-step's decoded weights and activations live at a time.
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-                if constexpr (FMT == FMT_FP8) {
-#pragma unroll
-                    for (int mb = 0; mb < kMB; ++mb)
-                        if (mb < nmb) {
-                            acc[0][mb] += wv[0].scale * part[0][mb];
-                            acc[1][mb] += wv[1].scale * part[1][mb];
-                        }
-                }
+        for (int qq = 0; qq < 4; ++qq) {
+            const int r = i * kBRowsPerPass + 4 * wave + qq;
+            int v = -1;
+            if (r < d.M) {
+                const int p = d.p0 + r;
+                v = DOWN ? p : d.shared ? p - a.T * a.k : (int)((uint32_t)ld_s(a.perm + p) / (uint32_t)a.k);
             }
+            row = q == qq ? v : row;
         }
+        src.boff[i] = row >= 0 ? (uint32_t)row * brow_bytes + (uint32_t)bc * 16u : kOff;
     }
-    __syncthreads();  // LDS is reused by the next item
 }
 
+// One macro step of a wavefront: its two 16 x 128 weight tiles against the
+// NMB 16-token blocks of the activation tile in LDS.  The activation reads of
+// sub-step s + 1 are issued before the matrix-core work of sub-step s.
+template <int FMT, int NMB>
+__device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_t *buf, f32x4 (&acc)[2][kMB])
+{
+    const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
+    const uint8_t *bp = buf + col * kBRow + grp * 64;
+    bf16x8 b[2][NMB];
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb)
+        b[0][mb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kBRow));
+    // FP8 accumulates the step in `part` and adds scale * part at the end.
+    f32x4 part[2][NMB];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) part[t][mb] = FMT == FMT_FP8 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[t][mb];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        if (s < 3) {
+#pragma unroll
+            for (int mb = 0; mb < NMB; ++mb)
+                b[(s + 1) & 1][mb] =
+                    __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kBRow + (s + 1) * 16));
+        }
+        const bf16x8 av0 = decode_a<FMT>(wv[0], s), av1 = decode_a<FMT>(wv[1], s);
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) {
+            part[0][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av0, b[s & 1][mb], part[0][mb], 0, 0, 0);
+            part[1][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av1, b[s & 1][mb], part[1][mb], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+        if constexpr (FMT == FMT_FP8) {
+            acc[0][mb] += wv[0].scale * part[0][mb];
+            acc[1][mb] += wv[1].scale * part[1][mb];
+        } else {
+            acc[0][mb] = part[0][mb];
+            acc[1][mb] = part[1][mb];
+        }
+    }
+}
+
+// Persistent stream over the workgroup's unit range [x0, x1).  The loads of
+// unit u + PD - 1 are issued while unit u is contracted, across item
+// boundaries: one pipeline for the whole range, never drained in between.
 template <int FMT, bool DOWN, int PD>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void expert_ffn_kernel(FfnParams P)
 {
     __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kBBuf];
+    constexpr int NV = Fmt<FMT>::kVecs;
+    constexpr uint32_t BLK = 1024u * NV;
+    const VerifyArgs &a = P.a;
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int lane = lane_id();
+    const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
+    const int tid = threadIdx.x, br = tid >> 4, bc = tid & 15;
     const Plan pl = load_plan(P);
-    const long n_units = (long)pl.n_groups * P.nbands * P.nsteps;
+    const int nsteps = P.nsteps, K = P.K;
+    const long n_units = (long)pl.n_groups * P.nbands * nsteps;
     long x0, x1;
     worker_range(n_units, w, P.workers, x0, x1);
-    const int nsteps = P.nsteps;
-    for (long x = x0; x < x1;) {
-        const int item = (int)(x / nsteps);
-        const long ib = (long)item * nsteps;
-        const int s0 = (int)(x - ib);
-        const int s1 = (int)min((long)nsteps, x1 - ib);
-        const ItemDesc d = describe<DOWN>(P, pl, item);
-        f32x4 acc[2][kMB];
+    if (x0 >= x1) return;
+
+    const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
+    const rsrc_t rb = DOWN ? make_rsrc(a.h, (uint32_t)(a.T * a.k + (a.sh_gate ? a.T : 0)) * brow_bytes)
+                           : make_rsrc(a.x, (uint32_t)a.T * brow_bytes);
+
+    Source src;
+    set_source<FMT, DOWN>(src, P, pl, (int)(x0 / nsteps));
+
+    WFrag<FMT> wf[PD][2];
+    u32x4 bst[PD][kBPass];
+    // Loads of unit v into ring slot `slot`; a unit past the range loads zeros
+    // (offsets beyond every buffer), so every path issues the same loads and
+    // the compiler's wait counts stay exact.
+    auto issue = [&](int slot, long v) {
+        if (v >= src.ie && v < x1) set_source<FMT, DOWN>(src, P, pl, src.item + 1);
+        const bool ok = v < x1;
+        const uint32_t step = (uint32_t)(v - src.ib);
+        const uint32_t so = step * BLK;
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int i = 0; i < NV; ++i) {
+            wf[slot][0].v[i] = load16<kAuxNT>(src.ra0, ok ? src.a0 + so + 1024u * i : kOff);
+            wf[slot][1].v[i] = load16<kAuxNT>(src.ra1, ok ? src.a1 + so + 1024u * i : kOff);
+        }
+        if constexpr (FMT == FMT_FP8) {
+            const uint32_t sso = step * 4u;
+            wf[slot][0].scale = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(src.rs0, (int)(ok ? src.q0 + sso : kOff), 0, 0));
+            wf[slot][1].scale = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(src.rs1, (int)(ok ? src.q1 + sso : kOff), 0, 0));
+        } else if constexpr (FMT == FMT_MXFP4) {
+            const uint32_t sso = step * 64u;
+            wf[slot][0].scale =
+                e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(src.rs0, (int)(ok ? src.q0 + sso : kOff), 0, 0));
+            wf[slot][1].scale =
+                e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(src.rs1, (int)(ok ? src.q1 + sso : kOff), 0, 0));
+        }
+        const bool kok = ok && (int)step * kMacroK + bc * 8 < K;
 #pragma unroll
-            for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-        run_item<FMT, DOWN, PD>(P, d, s0, s1, acc, lds);
-        if (s0 == 0 && s1 == nsteps) {
-            finish_item<DOWN>(P, d, wave, acc);
-        } else {
-            // Cut item: park the partial sums (slot 0: the item holds x0; slot 1: it holds x1-1).
-            float *dst = P.partials + ((size_t)w * 2 + (ib <= x0 ? 0 : 1)) * kPartialFloats;
+        for (int i = 0; i < kBPass; ++i)
+            bst[slot][i] = load16<0>(rb, (kok && src.boff[i] != kOff) ? src.boff[i] + step * 256u : kOff);
+    };
+
+    // The item being contracted.
+    int citem = (int)(x0 / nsteps);
+    ItemDesc cd = describe<DOWN>(P, pl, citem);
+    long cib = (long)citem * nsteps;
+    f32x4 acc[2][kMB];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto body = [&](int slot, int par, long u) {
+        issue((slot + PD - 1) % PD, u + PD - 1);
+        if (u >= x1) return;  // the last round of the unrolled loop runs past the range
+        const int nmb = (cd.M + 15) / 16;
+        uint8_t *buf = lds + par * kBBuf;
+        // After the previous step's barrier no wavefront still reads this buffer.
+#pragma unroll
+        for (int i = 0; i < kBPass; ++i)
+            *reinterpret_cast<u32x4 *>(buf + (i * kBRowsPerPass + br) * kBRow + bc * 16) = bst[slot][i];
+        __syncthreads();
+        switch (nmb) {
+        case 1: contract<FMT, 1>(wf[slot], buf, acc); break;
+        case 2: contract<FMT, 2>(wf[slot], buf, acc); break;
+        case 3: contract<FMT, 3>(wf[slot], buf, acc); break;
+        default: contract<FMT, 4>(wf[slot], buf, acc); break;
+        }
+        // Item boundary: finish the item (or park its partial sums if it is
+        // cut at either end of the range) and move on to the next one.
+        if (u + 1 == cib + nsteps || u + 1 == x1) {
+            if (cib >= x0 && cib + nsteps <= x1) {
+                finish_item<DOWN>(P, cd, wave, acc);
+            } else {
+                float *dst = P.partials + ((size_t)w * 2 + (cib <= x0 ? 0 : 1)) * kPartialFloats;
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int mb = 0; mb < kMB; ++mb)
+                        if (mb < nmb)
+                            *reinterpret_cast<f32x4 *>(dst + (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4) =
+                                acc[t][mb];
+            }
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
-                for (int mb = 0; mb < kMB; ++mb)
-                    *reinterpret_cast<f32x4 *>(dst + (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4) = acc[t][mb];
+                for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (u + 1 < x1) {
+                ++citem;
+                cib += nsteps;
+                cd = describe<DOWN>(P, pl, citem);
+            }
         }
-        x = ib + s1;
+    };
+
+#pragma unroll
+    for (int j = 0; j < PD - 1; ++j) issue(j, x0 + j);
+    constexpr int UN = PD % 2 ? 2 * PD : PD;  // ring slots and LDS parity repeat together
+    for (long u = x0; u < x1; u += UN) {
+#pragma unroll
+        for (int j = 0; j < UN; ++j) body(j % PD, j & 1, u + j);
     }
 }
 
@@ -476,6 +567,8 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
     const long ib = (long)item * P.nsteps, ie = ib + P.nsteps;
     if (ib >= x0 || ie > x1) return;  // not cut before this range, or its end lies beyond it
     const int w0 = owner_of(n_units, ib, P.workers);
+    const ItemDesc d = describe<DOWN>(P, pl, item);
+    const int nmb = (d.M + 15) / 16;  // only the live token blocks were parked
     f32x4 acc[2][kMB];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -491,9 +584,11 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
         for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int mb = 0; mb < kMB; ++mb)
-                acc[t][mb] += *reinterpret_cast<const f32x4 *>(src + (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4);
+                if (mb < nmb)
+                    acc[t][mb] +=
+                        *reinterpret_cast<const f32x4 *>(src + (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4);
     }
-    finish_item<DOWN>(P, describe<DOWN>(P, pl, item), wave, acc);
+    finish_item<DOWN>(P, d, wave, acc);
 }
 
 // Token groups when some expert may have more than 64 tokens (T > 64):
@@ -602,11 +697,11 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
     const bool grouped = a.T > kTokGroup;  // some expert may need several token groups
     hipError_t err;
 
-    if ((err = mark(events, 0, stream)) != hipSuccess) return err;
     if (grouped) {
         hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(256), 0, stream, a, plan);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
+    if ((err = mark(events, 0, stream)) != hipSuccess) return err;
     FfnParams g{};
     g.a = a;
     g.N = a.d_ff;
@@ -619,6 +714,7 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
     g.plan = grouped ? plan : nullptr;
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
+    if ((err = mark(events, 1, stream)) != hipSuccess) return err;
     hipLaunchKernelGGL((expert_ffn_fixup_kernel<false>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
@@ -628,17 +724,18 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
     dn.nsteps = (a.d_ff + kMacroK - 1) / kMacroK;
     dn.band_rows = 32 * kWG;
     dn.nbands = (a.d + dn.band_rows - 1) / dn.band_rows;
-    if ((err = mark(events, 1, stream)) != hipSuccess) return err;
+    if ((err = mark(events, 2, stream)) != hipSuccess) return err;
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
+    if ((err = mark(events, 3, stream)) != hipSuccess) return err;
     hipLaunchKernelGGL((expert_ffn_fixup_kernel<true>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     const int n = a.T * (a.d / 4);
-    if ((err = mark(events, 2, stream)) != hipSuccess) return err;
+    if ((err = mark(events, 4, stream)) != hipSuccess) return err;
     hipLaunchKernelGGL(combine_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    return mark(events, 3, stream);
+    return mark(events, 5, stream);
 }
 
 hipError_t launch_verify(const VerifyArgs &a, float *partials, int32_t *plan, int plan_cap, hipStream_t stream,

@@ -30,7 +30,8 @@ struct VerifyArgs {
 };
 
 // Upper bound on the workgroups of a verify grid (sizes the partial-sum slots).
-constexpr int kMaxWorkers = 1024;
+constexpr int kMaxWorkers = 512;
+constexpr int kTimingMarks = 6;  // events recorded by the timed entry point
 
 // Workspace layout shared by the size query and the launcher: H (bf16 SwiGLU
 // rows), O (fp32 per-slot expert outputs), partial sums of cut work items.
@@ -41,7 +42,7 @@ struct VerifyWorkspace {
 };
 VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared);
 
-// events: 4 optional marks recorded before gate/up, down, combine and after combine.
+// events: kTimingMarks optional marks around the expert kernels, their fix-ups and combine.
 hipError_t launch_verify(const VerifyArgs &a, float *partials, int32_t *plan, int plan_cap, hipStream_t stream,
                          hipEvent_t const *events = nullptr);
 
