@@ -153,7 +153,12 @@ moe_status_t moe_expert_union(const int32_t *topk_idx, int T, int k, int E, int3
                               int32_t *union_ids, int32_t *n_unique, int32_t *offsets, int32_t *perm,
                               void *stream);
 
-/* Bytes of device workspace moe_verify_layer needs for T tokens and top-k. */
+/*
+ * Bytes of device workspace moe_verify_layer needs for T tokens and top-k.
+ * MOE_ERR_UNSUPPORTED when a call could hold more than 4096 token groups
+ * (one per distinct expert, plus one per further 64 tokens of an expert):
+ * 1025 + ceil((T*k + T) / 64) > 4096.
+ */
 moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, size_t *bytes);
 
 /*

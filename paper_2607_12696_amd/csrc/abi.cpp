@@ -96,7 +96,9 @@ moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, siz
     const moe_status_t st = check_weights(w);
     if (st != MOE_OK) return st;
     if (T < 1 || k < 1 || k > kMaxK || k > w->E || (long)T * k > kMaxSlots) return MOE_ERR_INVALID_ARG;
-    *bytes = ecospec::verify_workspace(w->d, w->d_ff, T, k, w->sh_gate != nullptr).total;
+    const ecospec::VerifyWorkspace ws = ecospec::verify_workspace(w->d, w->d_ff, T, k, w->sh_gate != nullptr);
+    if (ws.plan_cap > ecospec::kMaxGroups) return MOE_ERR_UNSUPPORTED;
+    *bytes = ws.total;
     return MOE_OK;
 }
 
@@ -112,6 +114,7 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     if (!r->topk_w || !r->union_ids || !r->n_unique || !r->offsets || !r->perm) return MOE_ERR_INVALID_ARG;
     const bool shared = w->sh_gate != nullptr;
     const ecospec::VerifyWorkspace ws = ecospec::verify_workspace(w->d, w->d_ff, r->T, r->k, shared);
+    if (ws.plan_cap > ecospec::kMaxGroups) return MOE_ERR_UNSUPPORTED;
     if (workspace_bytes < ws.total) return MOE_ERR_WORKSPACE;
     const long rows = (long)r->T * r->k + (shared ? r->T : 0);
     if ((long)r->T * w->d * 2 >= (1L << 31) || rows * w->d_ff * 2 >= (1L << 31)) return MOE_ERR_UNSUPPORTED;

@@ -184,17 +184,95 @@ __device__ __forceinline__ int expert_tokens(const VerifyArgs &a, int u, int U)
     return u < U ? ld_s(a.offsets + u + 1) - ld_s(a.offsets + u) : a.T;
 }
 
-// Unit range [x0, x1) of workgroup w: equal shares of n units.
-__device__ __forceinline__ void worker_range(long n, int w, int workers, long &x0, long &x1)
+// ----------------------------------------------------------------------------- cost-weighted split
+//
+// A unit is one macro step of one item.  Units of a token group with more
+// 16-token blocks cost more (the contraction grows with the blocks, the weight
+// bytes do not), so the units are split over the workgroups by cost: group g
+// costs c_g per unit, unit x of g (offset r in the group) starts at cost
+// P_x = CW_g * K + r * c_g, where CW_g is the exclusive prefix of c over the
+// groups and K the units per group, and workgroup w of W takes the units with
+// C * w <= P_x * W < C * (w + 1), C being the total cost.  The ranges are
+// contiguous, cover every unit once and cut each group's items at most at
+// the range ends, as an equal split does.
+
+// Relative per-step cost of a token group: a weight part set by the bytes a
+// step streams and a contraction part per 16-token block (measured on the FP8
+// kernels, scaled by bytes per weight for the other formats).
+template <int FMT>
+__device__ __forceinline__ int group_cost(int M)
 {
-    x0 = n * w / workers;
-    x1 = n * (w + 1) / workers;
+    constexpr int A = FMT == FMT_BF16 ? 29 : FMT == FMT_FP8 ? 13 : 5;
+    return A + 3 * ((M + 15) / 16);
+}
+
+struct Split {
+    int cw[kMaxGroups + 1];  // exclusive cost prefix over token groups; cw[n_groups] = total
+    long long found;         // result slot of first_unit
+    int wave_tot[kWG];
+};
+
+__device__ __forceinline__ int group_tokens(const FfnParams &P, const Plan &pl, int g)
+{
+    const VerifyArgs &a = P.a;
+    if (!P.plan) return g < pl.U ? a.offsets[g + 1] - a.offsets[g] : a.T;
+    const int u = P.plan[8 + 2 * g], tg = P.plan[8 + 2 * g + 1];
+    const int M = u < pl.U ? a.offsets[u + 1] - a.offsets[u] : a.T;
+    return min(kTokGroup, M - tg * kTokGroup);
+}
+
+// Fills sp.cw for the launch's token groups (whole workgroup).
+template <int FMT>
+__device__ __forceinline__ void build_costs(const FfnParams &P, const Plan &pl, Split &sp)
+{
+    int run = 0;
+    for (int base = 0; base < pl.n_groups; base += kThreads) {
+        const int g = base + (int)threadIdx.x;
+        const int c = g < pl.n_groups ? group_cost<FMT>(group_tokens(P, pl, g)) : 0;
+        int tot = 0;
+        const int ex = block_exclusive_scan(c, sp.wave_tot, &tot);
+        if (g < pl.n_groups) sp.cw[g] = run + ex;
+        run += tot;
+    }
+    if (threadIdx.x == 0) sp.cw[pl.n_groups] = run;
+    __syncthreads();
+}
+
+// First unit x with P_x * W >= target (whole workgroup; 0 <= target <= C * W).
+__device__ __forceinline__ long first_unit(Split &sp, int n_groups, long K, long W, long long target)
+{
+    const long long C = (long long)sp.cw[n_groups] * K;
+    if (target <= 0) return 0;
+    if (target >= C * W) return (long)n_groups * K;
+    for (int g = threadIdx.x; g < n_groups; g += kThreads) {
+        const long long lo = (long long)sp.cw[g] * K * W, hi = (long long)sp.cw[g + 1] * K * W;
+        if (lo < target && target <= hi) {
+            const long long cg = sp.cw[g + 1] - sp.cw[g];
+            const long long r = (target - lo + cg * W - 1) / (cg * W);
+            sp.found = r >= K ? (long long)(g + 1) * K : (long long)g * K + r;
+        }
+    }
+    __syncthreads();
+    const long x = (long)sp.found;
+    __syncthreads();  // sp.found is reused by the next search
+    return x;
+}
+
+// Unit range [x0, x1) of workgroup w.
+__device__ __forceinline__ void worker_range(Split &sp, int n_groups, long K, int w, int W, long &x0, long &x1)
+{
+    const long long C = (long long)sp.cw[n_groups] * K;
+    x0 = first_unit(sp, n_groups, K, W, C * w);
+    x1 = first_unit(sp, n_groups, K, W, C * (w + 1));
 }
 
 // Workgroup whose range holds unit x.
-__device__ __forceinline__ int owner_of(long n, long x, int workers)
+__device__ __forceinline__ int owner_of(const Split &sp, int n_groups, long K, int W, long x)
 {
-    return (int)(((x + 1) * workers - 1) / n);
+    const int g = (int)(x / K);
+    const long long cg = sp.cw[g + 1] - sp.cw[g];
+    const long long px = (long long)sp.cw[g] * K + (x - (long long)g * K) * cg;
+    return (int)(px * W / ((long long)sp.cw[n_groups] * K));
 }
 
 // What a workgroup needs to know about one item.
@@ -441,9 +519,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int tid = threadIdx.x, br = tid >> 4, bc = tid & 15;
     const Plan pl = load_plan(P);
     const int nsteps = P.nsteps, K = P.K;
-    const long n_units = (long)pl.n_groups * P.nbands * nsteps;
+    __shared__ Split sp;
+    build_costs<FMT>(P, pl, sp);
     long x0, x1;
-    worker_range(n_units, w, P.workers, x0, x1);
+    worker_range(sp, pl.n_groups, (long)P.nbands * nsteps, w, P.workers, x0, x1);
     if (x0 >= x1) return;
 
     const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
@@ -552,21 +631,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 // Finishes the items cut between workgroups: the workgroup whose range holds
 // an item's last unit (but not its first) sums the parked partial sums of
 // every owner of the item, in workgroup order.
-template <bool DOWN>
+template <int FMT, bool DOWN>
 __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
 {
     const int lane = lane_id();
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int w = blockIdx.x;
     const Plan pl = load_plan(P);
-    const long n_units = (long)pl.n_groups * P.nbands * P.nsteps;
+    const long KU = (long)P.nbands * P.nsteps;  // units per token group
+    __shared__ Split sp;
+    build_costs<FMT>(P, pl, sp);
     long x0, x1;
-    worker_range(n_units, w, P.workers, x0, x1);
+    worker_range(sp, pl.n_groups, KU, w, P.workers, x0, x1);
     if (x0 >= x1) return;
     const int item = (int)(x0 / P.nsteps);
     const long ib = (long)item * P.nsteps, ie = ib + P.nsteps;
     if (ib >= x0 || ie > x1) return;  // not cut before this range, or its end lies beyond it
-    const int w0 = owner_of(n_units, ib, P.workers);
+    const int w0 = owner_of(sp, pl.n_groups, KU, P.workers, ib);
     const ItemDesc d = describe<DOWN>(P, pl, item);
     const int nmb = (d.M + 15) / 16;  // only the live token blocks were parked
     f32x4 acc[2][kMB];
@@ -576,7 +657,7 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
         for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int v = w0; v <= w; ++v) {
         long v0, v1;
-        worker_range(n_units, v, P.workers, v0, v1);
+        worker_range(sp, pl.n_groups, KU, v, P.workers, v0, v1);
         if (v0 >= v1) continue;
         const int slot = (ib <= v0 && v0 < ie) ? 0 : 1;  // the item holds v's first unit, or is v's last item
         const float *src = P.partials + ((size_t)v * 2 + slot) * kPartialFloats;
@@ -715,7 +796,7 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = mark(events, 1, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false>), dim3(G), dim3(kThreads), 0, stream, g);
+    hipLaunchKernelGGL((expert_ffn_fixup_kernel<FMT, false>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     FfnParams dn = g;
@@ -728,7 +809,7 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = mark(events, 3, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<true>), dim3(G), dim3(kThreads), 0, stream, dn);
+    hipLaunchKernelGGL((expert_ffn_fixup_kernel<FMT, true>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     const int n = a.T * (a.d / 4);

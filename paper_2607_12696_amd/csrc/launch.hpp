@@ -31,6 +31,7 @@ struct VerifyArgs {
 
 // Upper bound on the workgroups of a verify grid (sizes the partial-sum slots).
 constexpr int kMaxWorkers = 512;
+constexpr int kMaxGroups = 4096;  // token groups of one launch (one per expert and 64 of its tokens)
 constexpr int kTimingMarks = 6;  // events recorded by the timed entry point
 
 // Workspace layout shared by the size query and the launcher: H (bf16 SwiGLU

@@ -95,6 +95,12 @@ def test_workspace_size_formula():
     assert st == moe.MOE_OK and n2 >= (64 * 8 + 64) * (2048 * 2 + 7168 * 4)
 
 
+def test_workspace_rejects_too_many_token_groups():
+    # 1025 + ceil((T*k + T) / 64) token groups at most 4096.
+    assert _ws(_weights(), 21000, 8)[0] == moe.MOE_OK
+    assert _ws(_weights(), 32768, 8)[0] == moe.MOE_ERR_UNSUPPORTED
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(fmt=3), moe.MOE_ERR_INVALID_ARG),
     (dict(d=0), moe.MOE_ERR_INVALID_ARG),
