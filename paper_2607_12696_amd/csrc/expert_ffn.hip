@@ -107,6 +107,11 @@ __device__ __forceinline__ int ld_s(const int32_t *p)
     return *reinterpret_cast<const __attribute__((address_space(4))) int32_t *>(reinterpret_cast<uintptr_t>(p));
 }
 
+__device__ __forceinline__ long long ld_s64(const long long *p)
+{
+    return *reinterpret_cast<const __attribute__((address_space(4))) long long *>(reinterpret_cast<uintptr_t>(p));
+}
+
 template <int FMT> struct Fmt;
 template <> struct Fmt<FMT_BF16>  { static constexpr int kVecs = 4; };
 template <> struct Fmt<FMT_FP8>   { static constexpr int kVecs = 2; };
@@ -163,6 +168,7 @@ struct FfnParams {
     int nbands;           // bands per expert: ceil(N / band_rows)
     int workers;          // workgroups of the main kernel's grid
     float *partials;      // [workers][2][kPartialFloats]
+    long long *ranges;    // [workers][2]: unit range [x0, x1) of each workgroup, written by the expert kernel
     const int32_t *plan;  // token groups when T > 64 (else null: one group per expert)
 };
 
@@ -523,6 +529,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     build_costs<FMT>(P, pl, sp);
     long x0, x1;
     worker_range(sp, pl.n_groups, (long)P.nbands * nsteps, w, P.workers, x0, x1);
+    if (threadIdx.x == 0) {  // for the fix-up kernel
+        P.ranges[2 * w] = x0;
+        P.ranges[2 * w + 1] = x1;
+    }
     if (x0 >= x1) return;
 
     const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
@@ -629,25 +639,31 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 }
 
 // Finishes the items cut between workgroups: the workgroup whose range holds
-// an item's last unit (but not its first) sums the parked partial sums of
-// every owner of the item, in workgroup order.
-template <int FMT, bool DOWN>
+// an item's last unit (but not its first) adds the parked partial sums of
+// every contributor, in workgroup order, and finishes the item.  The ranges
+// come from the expert kernel; the kernel boundary makes its partial sums
+// visible here.
+template <bool DOWN>
 __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
 {
     const int lane = lane_id();
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int w = blockIdx.x;
-    const Plan pl = load_plan(P);
-    const long KU = (long)P.nbands * P.nsteps;  // units per token group
-    __shared__ Split sp;
-    build_costs<FMT>(P, pl, sp);
-    long x0, x1;
-    worker_range(sp, pl.n_groups, KU, w, P.workers, x0, x1);
+    const long x0 = (long)ld_s64(P.ranges + 2 * w), x1 = (long)ld_s64(P.ranges + 2 * w + 1);
     if (x0 >= x1) return;
-    const int item = (int)(x0 / P.nsteps);
-    const long ib = (long)item * P.nsteps, ie = ib + P.nsteps;
+    const long ns = P.nsteps;
+    const int item = (int)(x0 / ns);
+    const long ib = (long)item * ns, ie = ib + ns;
     if (ib >= x0 || ie > x1) return;  // not cut before this range, or its end lies beyond it
-    const int w0 = owner_of(sp, pl.n_groups, KU, P.workers, ib);
+    // First contributor: walk back over the ranges that reach into the item.
+    int wf = w;
+    for (int v = w - 1; v >= 0; --v) {
+        const long v0 = (long)ld_s64(P.ranges + 2 * v), v1 = (long)ld_s64(P.ranges + 2 * v + 1);
+        if (v0 >= v1) continue;  // empty range
+        if (v1 <= ib) break;
+        wf = v;
+    }
+    const Plan pl = load_plan(P);
     const ItemDesc d = describe<DOWN>(P, pl, item);
     const int nmb = (d.M + 15) / 16;  // only the live token blocks were parked
     f32x4 acc[2][kMB];
@@ -655,9 +671,8 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
     for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int v = w0; v <= w; ++v) {
-        long v0, v1;
-        worker_range(sp, pl.n_groups, KU, v, P.workers, v0, v1);
+    for (int v = wf; v <= w; ++v) {
+        const long v0 = (long)ld_s64(P.ranges + 2 * v), v1 = (long)ld_s64(P.ranges + 2 * v + 1);
         if (v0 >= v1) continue;
         const int slot = (ib <= v0 && v0 < ie) ? 0 : 1;  // the item holds v's first unit, or is v's last item
         const float *src = P.partials + ((size_t)v * 2 + slot) * kPartialFloats;
@@ -756,7 +771,7 @@ VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared)
     w.o_offset = align(w.h_bytes);
     w.o_bytes = rows * d * 4;
     w.p_offset = w.o_offset + align(w.o_bytes);
-    w.p_bytes = (size_t)kMaxWorkers * 2 * kPartialFloats * 4;
+    w.p_bytes = (size_t)kMaxWorkers * 2 * kPartialFloats * 4 + (size_t)kMaxWorkers * 2 * 8;  // + unit ranges
     w.plan_cap = plan_capacity(T, k, shared);
     w.plan_offset = w.p_offset + align(w.p_bytes);
     w.plan_bytes = (8 + 2 * (size_t)w.plan_cap) * 4;
@@ -792,11 +807,12 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
     g.nbands = (a.d_ff + g.band_rows - 1) / g.band_rows;
     g.workers = G;
     g.partials = partials;
+    g.ranges = reinterpret_cast<long long *>(partials + (size_t)kMaxWorkers * 2 * kPartialFloats);
     g.plan = grouped ? plan : nullptr;
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = mark(events, 1, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<FMT, false>), dim3(G), dim3(kThreads), 0, stream, g);
+    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     FfnParams dn = g;
@@ -809,7 +825,7 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = mark(events, 3, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<FMT, true>), dim3(G), dim3(kThreads), 0, stream, dn);
+    hipLaunchKernelGGL((expert_ffn_fixup_kernel<true>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     const int n = a.T * (a.d / 4);
