@@ -258,7 +258,7 @@ def summarize_pmc(fetch_dir, write_dir, out_path):
 
     is_gu = lambda n: (GATEUP_KERNEL.replace(" ", "") in n.replace(" ", "")
                        or "_ZN7ecospec17expert_ffn_kernelILi1ELb0E" in n)
-    is_copy = lambda n: "MulFunctor" in n
+    is_copy = lambda n: "bitwise_not" in n
     fr, wr = load(fetch_dir, "FETCH_SIZE"), load(write_dir, "WRITE_SIZE")
     f_gu, nf = mean_for(fr, is_gu)
     w_gu, nw = mean_for(wr, is_gu)
@@ -269,7 +269,12 @@ def summarize_pmc(fetch_dir, write_dir, out_path):
     hbm = f_gu * 1024.0 * cal_f + w_gu * 1024.0 * cal_w
     with open(out_path, "w") as f:
         f.write("# rocprofv3 counter summary: FP8 gate/up kernel, DeepSeek-V3.1 layer, T=64, U=32\n")
-        f.write("# commands: rocprofv3 --pmc FETCH_SIZE -d <dir> -- python3 bench.py --profile ; same with WRITE_SIZE\n")
+        f.write("# commands (repository root, TMPDIR=/tmp):\n")
+        f.write("#   rocprofv3 --pmc FETCH_SIZE -d FETCH_DIR --output-format csv -- python3 bench.py --profile\n")
+        f.write("#   rocprofv3 --pmc WRITE_SIZE -d WRITE_DIR --output-format csv -- python3 bench.py --profile\n")
+        f.write("#   python3 bench.py --summarize-pmc FETCH_DIR WRITE_DIR\n")
+        f.write("# counters are KiB per dispatch; each is scaled by COPY_BYTES / (its reading for the calibration\n")
+        f.write("# kernel, torch.bitwise_not over 1 GiB of int32, which reads and writes 1 GiB each)\n")
         f.write(f"kernel_source_sha: {source_sha()}\n")
         f.write(f"gateup_dispatches: fetch {nf}, write {nw}\n")
         f.write(f"fetch_kib_per_dispatch: {f_gu:.1f}\n")
@@ -295,10 +300,11 @@ def main():
     ap.add_argument("--cpu-tokens", type=int, default=8)
     ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 plus a calibration copy")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--pmc-out", default=PMC_SUMMARY, help="where --summarize-pmc writes its summary")
     args = ap.parse_args()
 
     if args.summarize_pmc:
-        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], PMC_SUMMARY)
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.pmc_out)
         return 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
@@ -321,9 +327,11 @@ def main():
         torch.cuda.synchronize()
         for i in range(10):
             wl.step(args.U, 3 + i)
-        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=wl.dev).fill_(1.0)
+        # Calibration copy for the HBM counters: one elementwise kernel that reads and
+        # writes COPY_BYTES each, with a name nothing else in the run uses.
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.int32, device=wl.dev)
         dst = torch.empty_like(src)
-        torch.mul(src, 2.0, out=dst)
+        torch.bitwise_not(src, out=dst)
         torch.cuda.synchronize()
         log("profile run done")
         return 0
