@@ -183,12 +183,10 @@ moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_r
 /*
  * moe_verify_layer with timing marks: identical work and arguments, and in
  * addition records the caller's events on `stream` around its kernels:
- *   events[0] before the gate/up expert kernel, events[1] after it,
- *   events[2] after the gate/up fix-up kernel (before the down expert kernel),
- *   events[3] after the down expert kernel,
- *   events[4] after the down fix-up kernel (before the combine kernel),
- *   events[5] after the combine kernel.
- * events is an array of 6 hipEvent_t handles created by the caller (any
+ *   events[0] before the gate/up expert kernel, events[1] after it (before
+ *   its fix-up kernel), events[2] before the down expert kernel, events[3]
+ *   after it (before the combine kernel), events[4] after the combine kernel.
+ * events is an array of 5 hipEvent_t handles created by the caller (any
  * entry may be NULL to skip that mark).
  */
 moe_status_t moe_verify_layer_timed(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,

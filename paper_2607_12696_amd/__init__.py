@@ -257,12 +257,12 @@ def moe_verify_layer(x, weights: dict, routing: Routing, y=None, workspace=None)
 
 
 def moe_verify_layer_timed(x, weights: dict, routing: Routing, y, workspace, events):
-    """moe_verify_layer that also records 6 torch.cuda.Event marks on the current stream:
-    before / after the gate/up expert kernel, after its fix-up, after the down expert
-    kernel, after its fix-up, after the combine kernel."""
-    if len(events) != 6:
-        raise ValueError("moe_verify_layer_timed takes 6 events")
-    arr = (C.c_void_p * 6)(*[e.cuda_event if e is not None else None for e in events])
+    """moe_verify_layer that also records 5 torch.cuda.Event marks on the current stream:
+    before the gate/up expert kernel, after it, before the down expert kernel, after it,
+    after the combine kernel."""
+    if len(events) != 5:
+        raise ValueError("moe_verify_layer_timed takes 5 events")
+    arr = (C.c_void_p * 5)(*[e.cuda_event if e is not None else None for e in events])
     ws = weights_struct(weights)
     rs = routing.c_struct()
     _check("moe_verify_layer_timed", lib().moe_verify_layer_timed(

@@ -145,14 +145,10 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     a.perm = r->perm;
     a.x = static_cast<const uint16_t *>(x);
     a.y = static_cast<uint16_t *>(y);
-    a.h = reinterpret_cast<uint16_t *>(static_cast<uint8_t *>(workspace) + ws.h_offset);
-    a.o = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + ws.o_offset);
-    float *partials = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + ws.p_offset);
     hipEvent_t ev[ecospec::kTimingMarks] = {};
     if (events)
         for (int i = 0; i < ecospec::kTimingMarks; ++i) ev[i] = (hipEvent_t)events[i];
-    int32_t *plan = reinterpret_cast<int32_t *>(static_cast<uint8_t *>(workspace) + ws.plan_offset);
-    return from_hip(ecospec::launch_verify(a, partials, plan, ws.plan_cap, (hipStream_t)stream, events ? ev : nullptr));
+    return from_hip(ecospec::launch_verify(a, workspace, ws, (hipStream_t)stream, events ? ev : nullptr));
 }
 
 moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,

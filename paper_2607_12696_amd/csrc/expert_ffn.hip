@@ -164,11 +164,12 @@ struct FfnParams {
     VerifyArgs a;
     int N, K;             // rows and reduction length of one streamed matrix
     int nsteps;           // macro steps per item: ceil(K / 128)
-    int band_rows;        // rows per item: 64 (gate/up) or 128 (down)
+    int band_rows;        // rows per item: 16 * kWG (gate/up) or 32 * kWG (down)
     int nbands;           // bands per expert: ceil(N / band_rows)
     int workers;          // workgroups of the main kernel's grid
     float *partials;      // [workers][2][kPartialFloats]
     long long *ranges;    // [workers][2]: unit range [x0, x1) of each workgroup, written by the expert kernel
+    long long *cut;       // down only: [groups * nbands] how combine reads each item (see record_cuts)
     const int32_t *plan;  // token groups when T > 64 (else null: one group per expert)
 };
 
@@ -213,8 +214,8 @@ __device__ __forceinline__ int group_cost(int M)
 }
 
 struct Split {
-    int cw[kMaxGroups + 1];  // exclusive cost prefix over token groups; cw[n_groups] = total
-    long long found;         // result slot of first_unit
+    int cw[kMaxGroups + 1];             // exclusive cost prefix over token groups; cw[n_groups] = total
+    long long bound[kMaxWorkers + 1];   // bound[w] = first unit of workgroup w; bound[W] = all units
     int wave_tot[kWG];
 };
 
@@ -244,32 +245,36 @@ __device__ __forceinline__ void build_costs(const FfnParams &P, const Plan &pl, 
     __syncthreads();
 }
 
-// First unit x with P_x * W >= target (whole workgroup; 0 <= target <= C * W).
-__device__ __forceinline__ long first_unit(Split &sp, int n_groups, long K, long W, long long target)
+// First unit x with P_x * W >= target (0 <= target <= C * W), by binary
+// search over the groups' cost prefix.
+__device__ __forceinline__ long first_unit(const Split &sp, int n_groups, long K, long W, long long target)
 {
     const long long C = (long long)sp.cw[n_groups] * K;
     if (target <= 0) return 0;
     if (target >= C * W) return (long)n_groups * K;
-    for (int g = threadIdx.x; g < n_groups; g += kThreads) {
-        const long long lo = (long long)sp.cw[g] * K * W, hi = (long long)sp.cw[g + 1] * K * W;
-        if (lo < target && target <= hi) {
-            const long long cg = sp.cw[g + 1] - sp.cw[g];
-            const long long r = (target - lo + cg * W - 1) / (cg * W);
-            sp.found = r >= K ? (long long)(g + 1) * K : (long long)g * K + r;
-        }
+    int lo = 0, hi = n_groups - 1;  // last group g with cw[g] * K * W < target
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if ((long long)sp.cw[mid] * K * W < target) lo = mid; else hi = mid - 1;
     }
-    __syncthreads();
-    const long x = (long)sp.found;
-    __syncthreads();  // sp.found is reused by the next search
-    return x;
+    const long long base = (long long)sp.cw[lo] * K * W, cg = sp.cw[lo + 1] - sp.cw[lo];
+    const long long r = (target - base + cg * W - 1) / (cg * W);
+    return r >= K ? (long)(lo + 1) * K : (long)lo * K + (long)r;
 }
 
-// Unit range [x0, x1) of workgroup w.
-__device__ __forceinline__ void worker_range(Split &sp, int n_groups, long K, int w, int W, long &x0, long &x1)
+// Every workgroup's first unit, into sp.bound (whole workgroup).
+__device__ __forceinline__ void build_bounds(Split &sp, int n_groups, long K, int W)
 {
     const long long C = (long long)sp.cw[n_groups] * K;
-    x0 = first_unit(sp, n_groups, K, W, C * w);
-    x1 = first_unit(sp, n_groups, K, W, C * (w + 1));
+    for (int v = threadIdx.x; v <= W; v += kThreads) sp.bound[v] = first_unit(sp, n_groups, K, W, C * v);
+    __syncthreads();
+}
+
+// Unit range [x0, x1) of workgroup w (after build_bounds).
+__device__ __forceinline__ void worker_range(const Split &sp, int w, long &x0, long &x1)
+{
+    x0 = (long)sp.bound[w];
+    x1 = (long)sp.bound[w + 1];
 }
 
 // Workgroup whose range holds unit x.
@@ -337,22 +342,8 @@ __device__ __forceinline__ int tile_row(const ItemDesc &d, int wave, int t)
 
 // ----------------------------------------------------------------------------- epilogue
 
-// v[c] for c = `col` (0..15), from wave-uniform scalar loads of v[0 .. n-1]
-// (entries c >= n read as 0).
-__device__ __forceinline__ int lane_select16(const int32_t *v, int n, int col)
-{
-    int r = 0;
-#pragma unroll
-    for (int c = 0; c < 16; ++c) {
-        const int s = c < n ? ld_s(v + c) : 0;
-        r = col == c ? s : r;
-    }
-    return r;
-}
-
 // Finishes a wavefront's (tile 0, tile 1) accumulators of an item: gate/up ->
-// bf16 SwiGLU rows of H at grouped positions; down -> fp32 rows of O at the
-// token's slot.  Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for
+// bf16 SwiGLU rows of H, down -> fp32 rows of O, both at grouped positions.  Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for
 // token column col of each 16-token block.
 template <bool DOWN>
 __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &d, int wave,
@@ -361,14 +352,6 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
     const VerifyArgs &a = P.a;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
     if (tile_row<DOWN>(d, wave, 0) >= P.N) return;  // rows past the last band
-    // Down: the slot of each token column, read through the scalar unit (a
-    // vector load here would wait behind every weight load in flight).
-    int slots[kMB] = {};
-    if (DOWN && !d.shared) {
-#pragma unroll
-        for (int mb = 0; mb < kMB; ++mb)
-            if (mb * 16 < d.M) slots[mb] = lane_select16(a.perm + d.p0 + mb * 16, d.M - mb * 16, col);
-    }
 #pragma unroll
     for (int mb = 0; mb < kMB; ++mb) {
         const int r = mb * 16 + col;
@@ -385,10 +368,9 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
             *reinterpret_cast<u32x2 *>(a.h + (size_t)p * a.d_ff + tile_row<DOWN>(d, wave, 0) + 4 * grp) =
                 u32x2{h2[0], h2[1]};
         } else {
-            const int slot = d.shared ? p : slots[mb];
 #pragma unroll
             for (int t = 0; t < 2; ++t)
-                *reinterpret_cast<f32x4 *>(a.o + (size_t)slot * a.d + tile_row<DOWN>(d, wave, t) + 4 * grp) =
+                *reinterpret_cast<f32x4 *>(a.o + (size_t)p * a.d + tile_row<DOWN>(d, wave, t) + 4 * grp) =
                     acc[t][mb];
         }
     }
@@ -509,6 +491,52 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
     }
 }
 
+// Down launch: for the combine kernel, how each item this range touches is to
+// be read (every item is touched by some range, so the table is rewritten
+// whole on every launch): -1 if it is whole (its rows are in O); if it is cut,
+// the partial-sum slots (workgroup * 2 + slot) of its contributors in
+// workgroup order, 20 bits each, their count in bits 60..61 (bit 62 set); or,
+// past 3 contributors, bit 63 clear, bit 62 clear and (w0 << 16 | w1).
+__device__ __forceinline__ void record_cuts(const FfnParams &P, const Plan &pl, Split &sp, long x0, long x1)
+{
+    const long ns = P.nsteps, KU = (long)P.nbands * ns;
+    const long i0 = x0 / ns, i1 = (x1 - 1) / ns;
+    for (long item = i0 + threadIdx.x; item <= i1; item += kThreads)
+        if (item * ns >= x0 && (item + 1) * ns <= x1) P.cut[item] = -1;
+    long it[2];
+    int n = 0;
+    if (i0 * ns < x0 || (i0 + 1) * ns > x1) it[n++] = i0;
+    if (i1 != i0 && (i1 + 1) * ns > x1) it[n++] = i1;
+    for (int i = 0; i < n; ++i) {
+        const long ib = it[i] * ns, ie = ib + ns;
+        const int w0 = owner_of(sp, pl.n_groups, KU, P.workers, ib);
+        const int w1 = owner_of(sp, pl.n_groups, KU, P.workers, ie - 1);
+        long long packed = 0;
+        int cnt = 0;
+        for (int v = w0; v <= w1; ++v) {
+            long v0, v1;
+            worker_range(sp, v, v0, v1);
+            if (v0 >= v1) continue;
+            if (cnt < 3) packed |= (long long)(2 * v + ((ib <= v0 && v0 < ie) ? 0 : 1)) << (20 * cnt);
+            ++cnt;
+        }
+        if (threadIdx.x == 0)
+            P.cut[it[i]] = cnt <= 3 ? ((1ll << 62) | ((long long)cnt << 60) | packed) : (long long)((w0 << 16) | w1);
+    }
+}
+
+// Where a wavefront's accumulator (tile t, token block mb) is parked in a
+// partial-sum slot: gate/up in accumulator order (only its fix-up reads it);
+// down as [64 tokens][band rows] fp32, the layout of O, so the combine
+// kernel's reads are coalesced.
+template <bool DOWN>
+__device__ __forceinline__ int partial_offset(int wave, int t, int mb, int lane)
+{
+    if (!DOWN) return (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4;
+    const int col = lane & 15, grp = lane >> 4;
+    return (mb * 16 + col) * (32 * kWG) + 32 * wave + 16 * t + 4 * grp;
+}
+
 // Persistent stream over the workgroup's unit range [x0, x1).  The loads of
 // unit u + PD - 1 are issued while unit u is contracted, across item
 // boundaries: one pipeline for the whole range, never drained in between.
@@ -527,14 +555,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int nsteps = P.nsteps, K = P.K;
     __shared__ Split sp;
     build_costs<FMT>(P, pl, sp);
+    build_bounds(sp, pl.n_groups, (long)P.nbands * nsteps, P.workers);
     long x0, x1;
-    worker_range(sp, pl.n_groups, (long)P.nbands * nsteps, w, P.workers, x0, x1);
-    if (threadIdx.x == 0) {  // for the fix-up kernel
+    worker_range(sp, w, x0, x1);
+    if (threadIdx.x == 0) {  // for the fix-up (gate/up) and combine (down) kernels
         P.ranges[2 * w] = x0;
         P.ranges[2 * w + 1] = x1;
     }
     if (x0 >= x1) return;
-
     const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
     const rsrc_t rb = DOWN ? make_rsrc(a.h, (uint32_t)(a.T * a.k + (a.sh_gate ? a.T : 0)) * brow_bytes)
                            : make_rsrc(a.x, (uint32_t)a.T * brow_bytes);
@@ -614,8 +642,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
                     for (int mb = 0; mb < kMB; ++mb)
                         if (mb < nmb)
-                            *reinterpret_cast<f32x4 *>(dst + (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4) =
-                                acc[t][mb];
+                            *reinterpret_cast<f32x4 *>(dst + partial_offset<DOWN>(wave, t, mb, lane)) = acc[t][mb];
             }
 #pragma unroll
             for (int t = 0; t < 2; ++t)
@@ -636,6 +663,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
         for (int j = 0; j < UN; ++j) body(j % PD, j & 1, u + j);
     }
+    if (DOWN) record_cuts(P, pl, sp, x0, x1);
 }
 
 // Finishes the items cut between workgroups: the workgroup whose range holds
@@ -649,6 +677,27 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
     const int lane = lane_id();
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int w = blockIdx.x;
+    if (!DOWN && w == (int)gridDim.x - 1) {
+        // For the combine kernel: each routed slot's grouped position and its
+        // (token group, row within the group), one grouped position per thread.
+        __shared__ int off_s[1025];
+        const VerifyArgs &a = P.a;
+        const int U = *a.n_unique;
+        for (int u = threadIdx.x; u <= U; u += kThreads) off_s[u] = a.offsets[u];
+        __syncthreads();
+        for (int p = threadIdx.x; p < a.T * a.k; p += kThreads) {
+            int lo = 0, hi = U - 1;  // the union member u with off_s[u] <= p < off_s[u + 1]
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (off_s[mid] <= p) lo = mid; else hi = mid - 1;
+            }
+            const int o0 = off_s[lo];
+            const int g0 = P.plan ? P.plan[8 + 2 * kMaxGroups + lo] : lo;  // first token group of u
+            const int slot = a.perm[p];
+            a.inv[slot] = p;
+            a.gidx[slot] = ((g0 + (p - o0) / kTokGroup) << 6) | ((p - o0) % kTokGroup);
+        }
+    }
     const long x0 = (long)ld_s64(P.ranges + 2 * w), x1 = (long)ld_s64(P.ranges + 2 * w + 1);
     if (x0 >= x1) return;
     const long ns = P.nsteps;
@@ -689,7 +738,8 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
 
 // Token groups when some expert may have more than 64 tokens (T > 64):
 // plan[0] = number of groups; plan[8 + 2i], plan[8 + 2i + 1] = (expert
-// position, group index within the expert) of group i, in expert order.
+// position, group index within the expert) of group i, in expert order;
+// plan[8 + 2 * kMaxGroups + u] = first group of expert position u.
 __global__ __launch_bounds__(256) void plan_kernel(VerifyArgs a, int32_t *plan)
 {
     __shared__ int wave_tot[256 / kWave];
@@ -705,6 +755,7 @@ __global__ __launch_bounds__(256) void plan_kernel(VerifyArgs a, int32_t *plan)
         }
         int tot = 0;
         const int pos = block_exclusive_scan(n, wave_tot, &tot);
+        if (u < n_exp) plan[8 + 2 * kMaxGroups + u] = run + pos;  // first group of expert position u
         for (int g = 0; g < n; ++g) {
             plan[8 + 2 * (run + pos + g)] = u;
             plan[8 + 2 * (run + pos + g) + 1] = g;
@@ -714,19 +765,75 @@ __global__ __launch_bounds__(256) void plan_kernel(VerifyArgs a, int32_t *plan)
     if (threadIdx.x == 0) plan[0] = run;
 }
 
-// y[t] = sum_j w[t][j] * O[t*k + j] (+ O[T*k + t]) -> bf16; 4 columns per thread.
-__global__ __launch_bounds__(256) void combine_kernel(VerifyArgs a)
+// Where expert output O[p][c .. c+3] (row r of a token group, item `item` of
+// the down launch) comes from: the down kernel's O row if the item was whole,
+// else the partial sums of its contributors added in workgroup order (what a
+// fix-up would have stored).  `cut` is the item's record_cuts entry.
+__device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, long item, int p, int r, int c)
 {
+    if (cut < 0) return *reinterpret_cast<const f32x4 *>(D.a.o + (size_t)p * D.a.d + c);
+    const int off = r * D.band_rows + c % D.band_rows;  // partial_offset<true>
+    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (cut >> 62) {
+        const int cnt = (int)((cut >> 60) & 3);
+        for (int i = 0; i < cnt; ++i) {
+            const long ps = (cut >> (20 * i)) & 0xfffff;
+            s += *reinterpret_cast<const f32x4 *>(D.partials + (size_t)ps * kPartialFloats + off);
+        }
+        return s;
+    }
+    // More than three contributors: each one's slot follows from its range.
+    const long ib = item * D.nsteps, ie = ib + D.nsteps;
+    for (int v = (int)(cut >> 16) & 0xffff, w1 = (int)cut & 0xffff; v <= w1; ++v) {
+        const long v0 = D.ranges[2 * v], v1 = D.ranges[2 * v + 1];
+        if (v0 >= v1) continue;
+        const int slot = (ib <= v0 && v0 < ie) ? 0 : 1;
+        s += *reinterpret_cast<const f32x4 *>(D.partials + ((size_t)v * 2 + slot) * kPartialFloats + off);
+    }
+    return s;
+}
+
+// y[t] = sum_j w[t][j] * O[slot t*k + j] (+ shared) -> bf16, summed in the
+// order j = 0..k-1, then the shared expert; 4 columns per thread.  D is the
+// down launch's geometry.  The k slots are handled 8 at a time, each stage's
+// loads issued together.
+__global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
+{
+    constexpr int CH = 8;
+    const VerifyArgs &a = D.a;
     const int per_row = a.d / 4;
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= a.T * per_row) return;
     const int t = i / per_row, c = (i - t * per_row) * 4;
+    const int band = c / D.band_rows;
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < a.k; ++j) {
-        const int slot = t * a.k + j;
-        s += a.topk_w[slot] * *reinterpret_cast<const f32x4 *>(a.o + (size_t)slot * a.d + c);
+    for (int j0 = 0; j0 < a.k; j0 += CH) {
+        int pj[CH], gj[CH];
+        float wj[CH];
+        long long cj[CH];
+        f32x4 vj[CH];
+#pragma unroll
+        for (int q = 0; q < CH; ++q) {
+            const int slot = t * a.k + min(j0 + q, a.k - 1);
+            pj[q] = a.inv[slot];
+            gj[q] = a.gidx[slot];
+            wj[q] = a.topk_w[slot];
+        }
+#pragma unroll
+        for (int q = 0; q < CH; ++q) cj[q] = D.cut[(long)(gj[q] >> 6) * D.nbands + band];
+#pragma unroll
+        for (int q = 0; q < CH; ++q) vj[q] = expert_out(D, cj[q], (long)(gj[q] >> 6) * D.nbands + band, pj[q], gj[q] & 63, c);
+#pragma unroll
+        for (int q = 0; q < CH; ++q)
+            if (j0 + q < a.k) s += wj[q] * vj[q];
     }
-    if (a.sh_gate) s += *reinterpret_cast<const f32x4 *>(a.o + (size_t)(a.T * a.k + t) * a.d + c);
+    if (a.sh_gate) {
+        // The shared expert's token groups are the last ceil(T / 64).
+        const int n_groups = D.plan ? D.plan[0] : *a.n_unique + 1;
+        const int g = n_groups - (a.T + kTokGroup - 1) / kTokGroup + t / kTokGroup;
+        const long item = (long)g * D.nbands + band;
+        s += expert_out(D, D.cut[item], item, a.T * a.k + t, t % kTokGroup, c);
+    }
     *reinterpret_cast<u32x2 *>(a.y + (size_t)t * a.d + c) = u32x2{pack_bf16x2(s[0], s[1]), pack_bf16x2(s[2], s[3])};
 }
 
@@ -774,8 +881,12 @@ VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared)
     w.p_bytes = (size_t)kMaxWorkers * 2 * kPartialFloats * 4 + (size_t)kMaxWorkers * 2 * 8;  // + unit ranges
     w.plan_cap = plan_capacity(T, k, shared);
     w.plan_offset = w.p_offset + align(w.p_bytes);
-    w.plan_bytes = (8 + 2 * (size_t)w.plan_cap) * 4;
-    w.total = w.plan_offset + align(w.plan_bytes);
+    w.plan_bytes = (8 + 2 * (size_t)kMaxGroups + 1026) * 4;  // groups, then first group per expert
+    w.map_offset = w.plan_offset + align(w.plan_bytes);
+    w.map_bytes = (size_t)T * k * 4 * 2;  // grouped position, (group, row) per routed slot
+    w.cut_offset = w.map_offset + align(w.map_bytes);
+    w.cut_bytes = (size_t)w.plan_cap * ((d + 32 * kWG - 1) / (32 * kWG)) * 8;
+    w.total = w.cut_offset + align(w.cut_bytes);
     return w;
 }
 
@@ -785,12 +896,19 @@ static hipError_t mark(hipEvent_t const *events, int i, hipStream_t stream)
 }
 
 template <int FMT>
-static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan, hipStream_t stream,
+static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const VerifyWorkspace &ws, hipStream_t stream,
                              hipEvent_t const *events)
 {
     constexpr int PD = FMT == FMT_BF16 ? ECOSPEC_PD_BF16 : FMT == FMT_FP8 ? ECOSPEC_PD_FP8 : ECOSPEC_PD_FP4;
     const int G = workers();
-    const bool grouped = a.T > kTokGroup;  // some expert may need several token groups
+    const bool grouped = args.T > kTokGroup;  // some expert may need several token groups
+    VerifyArgs a = args;
+    a.h = reinterpret_cast<uint16_t *>(ws_base + ws.h_offset);
+    a.o = reinterpret_cast<float *>(ws_base + ws.o_offset);
+    a.inv = reinterpret_cast<int32_t *>(ws_base + ws.map_offset);
+    a.gidx = a.inv + (size_t)a.T * a.k;
+    float *partials = reinterpret_cast<float *>(ws_base + ws.p_offset);
+    int32_t *plan = reinterpret_cast<int32_t *>(ws_base + ws.plan_offset);
     hipError_t err;
 
     if (grouped) {
@@ -808,6 +926,7 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
     g.workers = G;
     g.partials = partials;
     g.ranges = reinterpret_cast<long long *>(partials + (size_t)kMaxWorkers * 2 * kPartialFloats);
+    g.cut = reinterpret_cast<long long *>(ws_base + ws.cut_offset);
     g.plan = grouped ? plan : nullptr;
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
@@ -824,25 +943,23 @@ static hipError_t launch_fmt(const VerifyArgs &a, float *partials, int32_t *plan
     if ((err = mark(events, 2, stream)) != hipSuccess) return err;
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    if ((err = mark(events, 3, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<true>), dim3(G), dim3(kThreads), 0, stream, dn);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
 
+    // Combine also adds up the down items cut between workgroups.
     const int n = a.T * (a.d / 4);
-    if ((err = mark(events, 4, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL(combine_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a);
+    if ((err = mark(events, 3, stream)) != hipSuccess) return err;
+    hipLaunchKernelGGL(combine_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    return mark(events, 5, stream);
+    return mark(events, 4, stream);
 }
 
-hipError_t launch_verify(const VerifyArgs &a, float *partials, int32_t *plan, int plan_cap, hipStream_t stream,
+hipError_t launch_verify(const VerifyArgs &a, void *workspace, const VerifyWorkspace &ws, hipStream_t stream,
                          hipEvent_t const *events)
 {
-    (void)plan_cap;
+    uint8_t *base = static_cast<uint8_t *>(workspace);
     switch (a.fmt) {
-    case FMT_BF16: return launch_fmt<FMT_BF16>(a, partials, plan, stream, events);
-    case FMT_FP8: return launch_fmt<FMT_FP8>(a, partials, plan, stream, events);
-    case FMT_MXFP4: return launch_fmt<FMT_MXFP4>(a, partials, plan, stream, events);
+    case FMT_BF16: return launch_fmt<FMT_BF16>(a, base, ws, stream, events);
+    case FMT_FP8: return launch_fmt<FMT_FP8>(a, base, ws, stream, events);
+    case FMT_MXFP4: return launch_fmt<FMT_MXFP4>(a, base, ws, stream, events);
     default: return hipErrorInvalidValue;
     }
 }

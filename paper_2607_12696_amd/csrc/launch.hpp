@@ -26,25 +26,31 @@ struct VerifyArgs {
     const uint16_t *x;  // [T][d] bf16
     uint16_t *y;        // [T][d] bf16
     uint16_t *h;        // workspace: [T*k (+T)][d_ff] bf16 SwiGLU rows at grouped positions
-    float *o;           // workspace: [T*k (+T)][d] fp32 expert outputs at slots (shared: T*k + t)
+    float *o;           // workspace: [T*k (+T)][d] fp32 expert outputs at grouped positions (shared: T*k + t)
+    int32_t *inv;       // workspace: [T*k] grouped position of each routed slot
+    int32_t *gidx;      // workspace: [T*k] (token group << 6 | row in the group) of each routed slot
 };
 
 // Upper bound on the workgroups of a verify grid (sizes the partial-sum slots).
 constexpr int kMaxWorkers = 512;
 constexpr int kMaxGroups = 4096;  // token groups of one launch (one per expert and 64 of its tokens)
-constexpr int kTimingMarks = 6;  // events recorded by the timed entry point
+constexpr int kTimingMarks = 5;  // events recorded by the timed entry point
 
 // Workspace layout shared by the size query and the launcher: H (bf16 SwiGLU
-// rows), O (fp32 per-slot expert outputs), partial sums of cut work items.
+// rows) and O (fp32 expert outputs), both at grouped positions; partial sums
+// and unit ranges of work items cut between workgroups; the token-group plan;
+// per-slot maps for the combine kernel; the cut-item table of the down launch.
 struct VerifyWorkspace {
-    size_t h_offset, h_bytes, o_offset, o_bytes, p_offset, p_bytes, plan_offset, plan_bytes;
+    size_t h_offset, h_bytes, o_offset, o_bytes, p_offset, p_bytes, plan_offset, plan_bytes, map_offset, map_bytes,
+        cut_offset, cut_bytes;
     int plan_cap;
     size_t total;
 };
 VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared);
 
-// events: kTimingMarks optional marks around the expert kernels, their fix-ups and combine.
-hipError_t launch_verify(const VerifyArgs &a, float *partials, int32_t *plan, int plan_cap, hipStream_t stream,
+// events: kTimingMarks optional marks (before gate/up, before its fix-up, before
+// down, before combine, after combine).
+hipError_t launch_verify(const VerifyArgs &a, void *workspace, const VerifyWorkspace &ws, hipStream_t stream,
                          hipEvent_t const *events = nullptr);
 
 // Packed (streaming) weight layout; see pack.hip.
