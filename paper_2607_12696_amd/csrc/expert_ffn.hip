@@ -213,9 +213,18 @@ __device__ __forceinline__ int group_cost(int M)
     return A + 3 * ((M + 15) / 16);
 }
 
+constexpr int kMaxTokLds = 4096;  // routed slots whose token rows are staged in LDS
+
+// Per-launch schedule, built in LDS by every workgroup at start: the split,
+// and the token groups' metadata so that moving to a new item reads LDS
+// instead of waiting on global memory.
 struct Split {
     int cw[kMaxGroups + 1];             // exclusive cost prefix over token groups; cw[n_groups] = total
     long long bound[kMaxWorkers + 1];   // bound[w] = first unit of workgroup w; bound[W] = all units
+    int gp0[kMaxGroups];                // grouped position of each group's first token
+    int gM[kMaxGroups];                 // tokens in each group (<= 64)
+    int ge[kMaxGroups];                 // expert id of each group (-1: the shared expert)
+    int tok[kMaxTokLds];                // token of each grouped position (if T*k <= kMaxTokLds)
     int wave_tot[kWG];
 };
 
@@ -228,14 +237,27 @@ __device__ __forceinline__ int group_tokens(const FfnParams &P, const Plan &pl, 
     return min(kTokGroup, M - tg * kTokGroup);
 }
 
-// Fills sp.cw for the launch's token groups (whole workgroup).
+// Fills sp.cw and the groups' metadata for the launch (whole workgroup).
 template <int FMT>
 __device__ __forceinline__ void build_costs(const FfnParams &P, const Plan &pl, Split &sp)
 {
+    const VerifyArgs &a = P.a;
+    const int S = a.T * a.k;
+    if (S <= kMaxTokLds)
+        for (int p = threadIdx.x; p < S; p += kThreads) sp.tok[p] = a.perm[p] / a.k;
     int run = 0;
     for (int base = 0; base < pl.n_groups; base += kThreads) {
         const int g = base + (int)threadIdx.x;
-        const int c = g < pl.n_groups ? group_cost<FMT>(group_tokens(P, pl, g)) : 0;
+        int c = 0;
+        if (g < pl.n_groups) {
+            const int u = P.plan ? P.plan[8 + 2 * g] : g, tg = P.plan ? P.plan[8 + 2 * g + 1] : 0;
+            const bool shared = u >= pl.U;
+            const int Mu = shared ? a.T : a.offsets[u + 1] - a.offsets[u];
+            sp.gM[g] = min(kTokGroup, Mu - tg * kTokGroup);
+            sp.gp0[g] = (shared ? S : a.offsets[u]) + tg * kTokGroup;
+            sp.ge[g] = shared ? -1 : a.union_ids[u];
+            c = group_cost<FMT>(sp.gM[g]);
+        }
         int tot = 0;
         const int ex = block_exclusive_scan(c, sp.wave_tot, &tot);
         if (g < pl.n_groups) sp.cw[g] = run + ex;
@@ -332,6 +354,38 @@ __device__ __forceinline__ ItemDesc describe(const FfnParams &P, const Plan &pl,
     return d;
 }
 
+// describe() from the schedule in LDS.
+template <bool DOWN>
+__device__ __forceinline__ ItemDesc describe_lds(const FfnParams &P, const Split &sp, int item)
+{
+    const VerifyArgs &a = P.a;
+    const int gi = item / P.nbands, band = item - gi * P.nbands;
+    const int fmt = a.fmt;
+    const size_t kp = (size_t)P.nsteps * kMacroK;
+    const size_t mat = (size_t)P.N * kp * (fmt == FMT_BF16 ? 2 : 1) / (fmt == FMT_MXFP4 ? 2 : 1);
+    const size_t sc = fmt == FMT_FP8 ? (size_t)(P.N / 128) * (P.K / 128) * 4 : fmt == FMT_MXFP4 ? (size_t)P.N * kp / 32 : 0;
+    ItemDesc d;
+    const int e0 = __builtin_amdgcn_readfirstlane(sp.ge[gi]);
+    d.shared = e0 < 0;
+    d.p0 = __builtin_amdgcn_readfirstlane(sp.gp0[gi]);
+    d.M = __builtin_amdgcn_readfirstlane(sp.gM[gi]);
+    d.n0 = band * P.band_rows;
+    const size_t e = d.shared ? 0 : (size_t)e0;
+    auto sptr = [&](const void *base) {
+        return base ? static_cast<const void *>(static_cast<const uint8_t *>(base) + e * sc) : nullptr;
+    };
+    if (!DOWN) {
+        d.wa = (d.shared ? a.sh_gate : a.w_gate) + e * mat;
+        d.wb = (d.shared ? a.sh_up : a.w_up) + e * mat;
+        d.sa = d.shared ? a.sh_s_gate : sptr(a.s_gate);
+        d.sb = d.shared ? a.sh_s_up : sptr(a.s_up);
+    } else {
+        d.wa = d.wb = (d.shared ? a.sh_down : a.w_down) + e * mat;
+        d.sa = d.sb = d.shared ? a.sh_s_down : sptr(a.s_down);
+    }
+    return d;
+}
+
 // Rows of wavefront `wave`'s two tiles within an item (the same 16 rows of
 // gate and up, or 32 consecutive rows of down).
 template <bool DOWN>
@@ -389,7 +443,7 @@ struct Source {
 };
 
 template <int FMT, bool DOWN>
-__device__ __forceinline__ void set_source(Source &src, const FfnParams &P, const Plan &pl, int item)
+__device__ __forceinline__ void set_source(Source &src, const FfnParams &P, const Split &sp, int item)
 {
     constexpr int NV = Fmt<FMT>::kVecs;
     constexpr uint32_t BLK = 1024u * NV;
@@ -397,7 +451,7 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
     const int lane = lane_id(), tid = threadIdx.x, bc = tid & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int K = P.K, nsteps = P.nsteps;
-    const ItemDesc d = describe<DOWN>(P, pl, item);
+    const ItemDesc d = describe_lds<DOWN>(P, sp, item);
     src.item = item;
     src.ib = (long)item * nsteps;
     src.ie = src.ib + nsteps;
@@ -438,7 +492,10 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
             int v = -1;
             if (r < d.M) {
                 const int p = d.p0 + r;
-                v = DOWN ? p : d.shared ? p - a.T * a.k : (int)((uint32_t)ld_s(a.perm + p) / (uint32_t)a.k);
+                v = DOWN ? p
+                    : d.shared ? p - a.T * a.k
+                    : a.T * a.k <= kMaxTokLds ? __builtin_amdgcn_readfirstlane(sp.tok[p])
+                                              : (int)((uint32_t)ld_s(a.perm + p) / (uint32_t)a.k);
             }
             row = q == qq ? v : row;
         }
@@ -568,7 +625,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                            : make_rsrc(a.x, (uint32_t)a.T * brow_bytes);
 
     Source src;
-    set_source<FMT, DOWN>(src, P, pl, (int)(x0 / nsteps));
+    set_source<FMT, DOWN>(src, P, sp, (int)(x0 / nsteps));
 
     WFrag<FMT> wf[PD][2];
     u32x4 bst[PD][kBPass];
@@ -576,7 +633,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // (offsets beyond every buffer), so every path issues the same loads and
     // the compiler's wait counts stay exact.
     auto issue = [&](int slot, long v) {
-        if (v >= src.ie && v < x1) set_source<FMT, DOWN>(src, P, pl, src.item + 1);
+        if (v >= src.ie && v < x1) set_source<FMT, DOWN>(src, P, sp, src.item + 1);
         const bool ok = v < x1;
         const uint32_t step = (uint32_t)(v - src.ib);
         const uint32_t so = step * BLK;
@@ -606,7 +663,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 
     // The item being contracted.
     int citem = (int)(x0 / nsteps);
-    ItemDesc cd = describe<DOWN>(P, pl, citem);
+    ItemDesc cd = describe_lds<DOWN>(P, sp, citem);
     long cib = (long)citem * nsteps;
     f32x4 acc[2][kMB];
 #pragma unroll
@@ -651,7 +708,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             if (u + 1 < x1) {
                 ++citem;
                 cib += nsteps;
-                cd = describe<DOWN>(P, pl, citem);
+                cd = describe_lds<DOWN>(P, sp, citem);
             }
         }
     };
