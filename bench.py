@@ -31,6 +31,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -187,6 +189,53 @@ class Workload:
         return None, per
 
 
+class TSweep:
+    """Steps at T tokens with i.i.d. router logits, on a Workload's resident weights."""
+
+    def __init__(self, wl, T, n_pool=8):
+        import torch
+        import synth
+        moe, sh = wl.moe, wl.sh
+        self.wl, self.T, self.torch = wl, T, torch
+        self.logits = [synth.logits_scattered(T, sh.E, seed=7000 + 31 * T + i).to(wl.dev) for i in range(n_pool)]
+        i32 = dict(dtype=torch.int32, device=wl.dev)
+        self.r = moe.Routing(T, sh.k, sh.E, torch.empty(T, sh.k, **i32),
+                             torch.empty(T, sh.k, dtype=torch.float32, device=wl.dev), torch.empty(sh.E, **i32),
+                             torch.empty(sh.E, **i32), torch.empty(1, **i32), torch.empty(sh.E + 1, **i32),
+                             torch.empty(T * sh.k, **i32))
+        self.x = synth.activations(T, sh.d, seed=9, device=wl.dev)
+        self.y = torch.empty_like(self.x)
+        self.ws = torch.empty(moe.moe_verify_workspace_size(wl.wdicts[0], T, sh.k), dtype=torch.uint8,
+                              device=wl.dev)
+
+    def step(self, i):
+        wl, sh = self.wl, self.wl.sh
+        wl.moe.moe_route_topk(self.logits[i % len(self.logits)], sh.k, sh.score, self.r.topk_idx, self.r.topk_w)
+        wl.moe.moe_expert_union(self.r.topk_idx, sh.E, topk_w=self.r.topk_w, out=self.r)
+        wl.moe.moe_verify_layer(self.x, wl.wdicts[i % len(wl.wdicts)], self.r, y=self.y, workspace=self.ws)
+
+    def time(self, steps, warmup):
+        torch = self.torch
+        uniq = []
+        for i in range(warmup):
+            self.step(i)
+        for i in range(len(self.logits)):
+            self.step(i)
+            uniq.append(int(self.r.n_unique.item()))
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(steps):
+            self.step(i)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / steps, float(np.median(uniq))
+
+    def alg_bytes(self, U):
+        sh = self.wl.sh
+        return step_alg_bytes(sh, self.T, U)
+
+
 def pct(v, q):
     s = sorted(v)
     return s[min(len(s) - 1, max(0, int(round(q * (len(s) - 1)))))]
@@ -238,6 +287,131 @@ def cpu_baseline(wl, U, n_tokens):
                       f"{n_tokens * (sh.k + 1)} expert FFNs in {dt:.2f}s; scaled x{wl.T / n_tokens:g} to the "
                       f"whole step ({full:.1f}s)"}
     return base, err
+
+
+# --------------------------------------------------------------------------- 8-layer verification step
+
+class Stack:
+    """Eight DeepSeek-V3.1-shaped FP8 MoE layers verifying T=16 tokens of a synthetic
+    64-node draft tree (branching 4, per-node scores ~ Beta(2,2), children inherit a
+    parent expert per slot with probability 0.7), the tokens chosen once by
+    confidence (highest path score first) and once by the cost-aware selector
+    (Algorithm 1).  Each layer's routing comes from synthetic router logits whose
+    top-8 are the nodes' expert sets, and each layer gets its own synthetic N(0,1)
+    hidden states (there is no model around the MoE layers to carry them: no norm
+    or residual, without which stacked random layers overflow bf16)."""
+
+    L, N_NODES, BRANCH, BUDGET, P_INHERIT = 8, 64, 4, 16, 0.7
+
+    def __init__(self, seed=0):
+        import torch
+        import synth
+        import paper_2607_12696_amd as moe
+        self.torch, self.moe = torch, moe
+        self.dev = torch.device("cuda:0")
+        sh = self.sh = synth.SHAPES["ds"]
+        t0 = time.time()
+        self.layers = []
+        for l in range(self.L):
+            raw = synth.layer_weights(sh, seed=seed + 17, device=self.dev, layer=l)
+            self.layers.append(moe.pack_layer(raw))
+            del raw
+        torch.cuda.synchronize()
+        log(f"stack: {self.L} layers packed in {time.time() - t0:.1f}s")
+        self.parent, self.P = synth.draft_tree(self.N_NODES, self.BRANCH, seed=seed)
+        self.pred = synth.tree_expert_sets(self.parent, self.L, sh.E, sh.k, self.P_INHERIT, seed=seed)
+        self.sel = {
+            "confidence": moe.moe_select_tree(self.parent, self.P, self.pred, sh.E, self.BUDGET,
+                                              mode=moe.MOE_SEL_CONFIDENCE)[0],
+            "cost_aware": moe.moe_select_tree(self.parent, self.P, self.pred, sh.E, self.BUDGET,
+                                              mode=moe.MOE_SEL_COST_RATIO)[0],
+            "global_cost": moe.moe_select_tree(self.parent, self.P, self.pred, sh.E, self.BUDGET,
+                                               mode=moe.MOE_SEL_GLOBAL_COST)[0],
+        }
+        T = self.BUDGET
+        i32 = dict(dtype=torch.int32, device=self.dev)
+        self.xs = [synth.activations(T, sh.d, seed=seed + 5 + l, device=self.dev) for l in range(self.L)]
+        self.ys = [torch.empty_like(x) for x in self.xs]
+        self.ws = torch.empty(moe.moe_verify_workspace_size(self.layers[0], T, sh.k), dtype=torch.uint8,
+                              device=self.dev)
+        self.plans = {}
+        for name, nodes in self.sel.items():
+            logits, routs = [], []
+            for l in range(self.L):
+                routes = self.pred[nodes, l, :]
+                logits.append(synth.routes_to_logits(routes, sh.E, seed=seed + 100 * l + 1, device=self.dev))
+                routs.append(moe.Routing(T, sh.k, sh.E, torch.empty(T, sh.k, **i32),
+                                         torch.empty(T, sh.k, dtype=torch.float32, device=self.dev),
+                                         torch.empty(sh.E, **i32), torch.empty(sh.E, **i32), torch.empty(1, **i32),
+                                         torch.empty(sh.E + 1, **i32), torch.empty(T * sh.k, **i32)))
+            self.plans[name] = (logits, routs)
+
+    def run(self, name):
+        """The 8-layer pass for one selection; returns the stacked layer outputs [L, T, d]."""
+        moe, sh = self.moe, self.sh
+        logits, routs = self.plans[name]
+        for l in range(self.L):
+            moe.moe_route_topk(logits[l], sh.k, sh.score, routs[l].topk_idx, routs[l].topk_w)
+            moe.moe_expert_union(routs[l].topk_idx, sh.E, topk_w=routs[l].topk_w, out=routs[l])
+            moe.moe_verify_layer(self.xs[l], self.layers[l], routs[l], y=self.ys[l], workspace=self.ws)
+        return self.ys
+
+    def measure(self, steps, warmup):
+        torch = self.torch
+        out = {"layers": self.L, "T": self.BUDGET, "tree_nodes": self.N_NODES, "branching": self.BRANCH,
+               "p_inherit": self.P_INHERIT}
+        for name in self.sel:
+            for _ in range(warmup):
+                self.run(name)
+            torch.cuda.synchronize()
+            ref = torch.stack(self.run(name))
+            uniq = [int(r.n_unique.item()) for r in self.plans[name][1]]
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(steps):
+                self.run(name)
+            b.record()
+            torch.cuda.synchronize()
+            eager_us = a.elapsed_time(b) * 1e3 / steps
+            # The same pass captured once as a graph and replayed; every replay is
+            # checked bit for bit against the eager result, with eager work between.
+            g = torch.cuda.CUDAGraph()
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                self.run(name)
+            torch.cuda.current_stream().wait_stream(s)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g):
+                self.run(name)
+            gout = self.ys
+            graph_ok, diffs = True, []
+            for _ in range(3):
+                g.replay()
+                torch.cuda.synchronize()
+                graph_ok &= bool(torch.equal(torch.stack(gout), ref))
+                diffs.append(float((torch.stack(gout).float() - ref.float()).abs().max()))
+                self.run(name)
+                torch.cuda.synchronize()
+            a.record()
+            for _ in range(steps):
+                g.replay()
+            b.record()
+            torch.cuda.synchronize()
+            graph_us = a.elapsed_time(b) * 1e3 / steps
+            graph_ok &= bool(torch.equal(torch.stack(gout), ref))
+            finite = bool(torch.isfinite(ref.float()).all())
+            del g
+            out[name] = {"nodes": [int(v) for v in self.sel[name]], "unique_experts_per_layer": uniq,
+                         "unique_experts_total": sum(uniq), "eager_us": eager_us, "graph_us": graph_us,
+                         "graph_replays_match_eager": graph_ok, "outputs_finite": finite,
+                         "weight_bytes": sum(u + 1 for u in uniq) * expert_bytes(self.sh.d, self.sh.d_ff)}
+            log(f"stack {name}: unique/layer {uniq} (sum {sum(uniq)}), eager {eager_us:.0f} us, "
+                f"graph {graph_us:.0f} us, replays match: {graph_ok}")
+        out["speedup_cost_aware_vs_confidence"] = out["confidence"]["eager_us"] / out["cost_aware"]["eager_us"]
+        out["unique_experts_saved_vs_confidence"] = (out["confidence"]["unique_experts_total"]
+                                                     - out["cost_aware"]["unique_experts_total"])
+        return out
 
 
 # --------------------------------------------------------------------------- PMC summary
@@ -298,11 +472,18 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=8)
+    ap.add_argument("--no-stack", action="store_true", help="skip the 8-layer draft-tree verification step")
+    ap.add_argument("--stack-only", action="store_true", help="only the 8-layer draft-tree verification step")
     ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 plus a calibration copy")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--pmc-out", default=PMC_SUMMARY, help="where --summarize-pmc writes its summary")
     args = ap.parse_args()
 
+    if args.stack_only:
+        import torch
+        st = Stack()
+        print(json.dumps(st.measure(max(10, args.steps // 2), 3)))
+        return 0
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.pmc_out)
         return 0
@@ -369,10 +550,31 @@ def main():
         fit = {"us_intercept": a, "us_per_expert": b, "r2": r2,
                "GB_s_marginal": expert_bytes(sh.d, sh.d_ff) / (b * 1e-6) / 1e9 if b > 0 else None}
 
+    # Batch scaling: scattered routing (i.i.d. logits), T = 8 .. 256 (T > 64 splits an
+    # expert's tokens into groups of 64, each streaming the expert once).
+    sweep_t = []
+    if not args.no_sweep:
+        for T in (8, 16, 32, 64, 128, 256):
+            wt = TSweep(wl, T)
+            med, uniq = wt.time(max(10, args.steps // 2), 3)
+            sweep_t.append({"T": T, "unique_experts_median": uniq, "step_us": med,
+                            "GB_s": wt.alg_bytes(uniq) / (med * 1e-6) / 1e9})
+            log(f"  T={T:4d}: U~{uniq:5.0f} step {med:8.1f} us")
+            del wt
+
     cpu, err = (None, None)
     if not args.no_cpu:
         log("timing the oracle on the host ...")
         cpu, err = cpu_baseline(wl, args.U, args.cpu_tokens)
+
+    stack = None
+    if not args.no_stack:
+        del wl
+        torch.cuda.empty_cache()
+        st = Stack()
+        stack = st.measure(max(10, args.steps // 2), 3)
+        del st
+        torch.cuda.empty_cache()
 
     traffic = read_pmc_summary()
     out = {
@@ -393,6 +595,8 @@ def main():
         "kernels_us": {k: 1e3 * sum(v) / len(v) for k, v in per.items()},
         "sweep_T64": sweep,
         "linear_fit_us_vs_U": fit,
+        "sweep_T_scattered": sweep_t,
+        "stack_8_layers_T16": stack,
     }
     print(json.dumps(out))
     return 0

@@ -209,6 +209,26 @@ def test_all_experts_routed_k_equals_E():
     assert y_err(y.float().cpu().numpy(), oracle.verify_tokens(layer, x, idx_o, w_o)) <= YTOL
 
 
+def test_two_layer_chain_matches_oracle():
+    """Two stacked toy layers: the first layer's bf16 output is the second's input."""
+    sh = synth.SHAPES["toy"]
+    T = 8
+    x = synth.activations(T, sh.d, seed=21)
+    xg = x.to(DEV)
+    xo = x
+    for l in range(2):
+        layer = synth.layer_weights(sh, seed=3, layer=l)
+        lg = synth.logits_scattered(T, sh.E, seed=30 + l)
+        note(f"chain layer {l}")
+        yg, r = moe.moe_verify_step(xg, lg.to(DEV), to_dev(layer), sh.k, sh.score)
+        idx_o, w_o = oracle.route(lg.numpy(), sh.k, sh.score)
+        assert np.array_equal(r.topk_idx.cpu().numpy(), idx_o)
+        yo = oracle.verify_tokens(layer, xo, idx_o, w_o)
+        assert y_err(yg.float().cpu().numpy(), yo) <= YTOL
+        xg = yg
+        xo = torch.from_numpy(yo).to(torch.bfloat16)   # the layer boundary is bf16 on both sides
+
+
 def test_workspace_contents_do_not_matter():
     sh = SMALL["fp8"]
     T = 9
