@@ -1,49 +1,83 @@
 // Expert union, histogram, scans and stable grouping on gfx950, in one
 // workgroup of 1024 threads (E <= 1024, so thread e owns expert e).
 //
-//  1. LDS histogram of the T*k routed slots (integer atomics: exact).
+// The routed slots are taken 1024 at a time, one per thread, in slot order
+// (wavefront w holds slots 64w .. 64w + 63 of a pass).  Within a wavefront,
+// lanes holding the same expert find each other with one ballot per bit of
+// the expert id; a lane's rank among the lower such lanes orders equal
+// experts by slot, and the highest lane of each expert records the
+// wavefront's count in LDS.  A pass then adds, per expert, the counts of the
+// earlier wavefronts (and passes): that prefix plus the rank places every slot
+// of the pass at once.  So the grouping is a stable counting sort by expert.
+//
+//  1. Counts per expert: the sum of the per-wavefront counts of all passes.
 //  2. Two block-wide exclusive scans over the experts: of the "used" flags
 //     (position of each expert in the ascending union) and of the counts
 //     (first grouped position of each expert).
-//  3. Stable counting sort of the slots into perm: wavefront 0 walks the
-//     slots 64 at a time; lanes holding the same expert find each other with
-//     one ballot per bit of the expert id, take their rank among the lower
-//     lanes, and the highest such lane advances that expert's cursor.  Slots
-//     therefore land in ascending order within each expert.
+//  3. The passes again, placing each slot at first position of its expert +
+//     slots of that expert in earlier passes and wavefronts + rank.
 #include "device.hpp"
 #include "launch.hpp"
 
 namespace ecospec {
 
 constexpr int kUnionThreads = 1024;
+constexpr int kUnionWaves = kUnionThreads / kWave;
+
+// Rank of this lane's expert e among the lower lanes holding e, and whether
+// this lane is the highest lane holding e (ok: the lane holds a valid expert).
+__device__ __forceinline__ void wave_match(int e, bool ok, int nbits, int &rank, bool &top, int &count)
+{
+    const int lane = lane_id();
+    uint64_t peers = __ballot(ok);
+    for (int b = 0; b < nbits; ++b) {
+        const bool bit = ok && ((e >> b) & 1);
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    rank = __popcll(peers & ((1ull << lane) - 1ull));
+    count = __popcll(peers);
+    top = ok && lane == 63 - __clzll(peers);
+}
 
 __global__ __launch_bounds__(kUnionThreads) void expert_union_kernel(
     const int32_t *__restrict__ idx, int S, int E, int32_t *__restrict__ counts, int32_t *__restrict__ union_ids,
     int32_t *__restrict__ n_unique, int32_t *__restrict__ offsets, int32_t *__restrict__ perm)
 {
-    __shared__ int cnt[kUnionThreads];
-    __shared__ int cursor[kUnionThreads];
+    __shared__ int wcnt[kUnionWaves][kUnionThreads];  // per-wavefront counts of the current pass
     __shared__ int member_id[kUnionThreads];
     __shared__ int member_start[kUnionThreads];
-    __shared__ int wave_tot[kUnionThreads / kWave];
-    const int tid = threadIdx.x;
+    __shared__ int wave_tot[kUnionWaves];
+    const int tid = threadIdx.x, wave = tid / kWave;
+    int nbits = 0;
+    while ((1 << nbits) < E) ++nbits;
+    const int passes = (S + kUnionThreads - 1) / kUnionThreads;
 
-    cnt[tid] = 0;
-    __syncthreads();
-    for (int s = tid; s < S; s += kUnionThreads) {
-        const int e = idx[s];
-        if ((unsigned)e < (unsigned)E) atomicAdd(&cnt[e], 1);
+    // 1. Counts: per-wavefront matches, summed per expert over wavefronts and passes.
+    int total = 0;  // thread e: slots routed to expert e
+    for (int ps = 0; ps < passes; ++ps) {
+        for (int w = 0; w < kUnionWaves; ++w) wcnt[w][tid] = 0;
+        __syncthreads();
+        const int s = ps * kUnionThreads + tid;
+        const int e = s < S ? idx[s] : -1;
+        const bool ok = (unsigned)e < (unsigned)E;
+        int rank, cnt;
+        bool top;
+        wave_match(e, ok, nbits, rank, top, cnt);
+        if (top) wcnt[wave][e] = cnt;
+        __syncthreads();
+        if (tid < E)
+            for (int w = 0; w < kUnionWaves; ++w) total += wcnt[w][tid];
+        __syncthreads();
     }
-    __syncthreads();
 
-    const int c = tid < E ? cnt[tid] : 0;
+    // 2. Union positions and first grouped positions.
+    const int c = tid < E ? total : 0;
     int U = 0, placed = 0;
     const int pos = block_exclusive_scan(c > 0 ? 1 : 0, wave_tot, &U);
     const int start = block_exclusive_scan(c, wave_tot, &placed);
-
     if (tid < E) {
         counts[tid] = c;
-        cursor[tid] = start;
         if (c > 0) {
             member_id[pos] = tid;
             member_start[pos] = start;
@@ -56,29 +90,30 @@ __global__ __launch_bounds__(kUnionThreads) void expert_union_kernel(
     }
     if (tid == 0) *n_unique = U;
 
-    if (tid < kWave) {
-        const int lane = tid;
-        const uint64_t below = (1ull << lane) - 1ull;
-        int nbits = 0;
-        while ((1 << nbits) < E) ++nbits;
-        for (int base = 0; base < S; base += kWave) {
-            const int s = base + lane;
-            const int e = s < S ? idx[s] : -1;
-            const bool ok = (unsigned)e < (unsigned)E;
-            uint64_t peers = __ballot(ok);
-            for (int b = 0; b < nbits; ++b) {
-                const bool bit = ok && ((e >> b) & 1);
-                const uint64_t m = __ballot(bit);
-                peers &= bit ? m : ~m;
+    // 3. Placement, pass by pass: thread e turns the per-wavefront counts into
+    //    first positions (in place), then every slot of the pass is placed.
+    int run = start;  // thread e: next position of expert e
+    for (int ps = 0; ps < passes; ++ps) {
+        for (int w = 0; w < kUnionWaves; ++w) wcnt[w][tid] = 0;
+        __syncthreads();
+        const int s = ps * kUnionThreads + tid;
+        const int e = s < S ? idx[s] : -1;
+        const bool ok = (unsigned)e < (unsigned)E;
+        int rank, cnt;
+        bool top;
+        wave_match(e, ok, nbits, rank, top, cnt);
+        if (top) wcnt[wave][e] = cnt;
+        __syncthreads();
+        if (tid < E) {
+            for (int w = 0; w < kUnionWaves; ++w) {
+                const int n = wcnt[w][tid];
+                wcnt[w][tid] = run;
+                run += n;
             }
-            if (ok) {
-                const int rank = __popcll(peers & below);
-                const int at = cursor[e];
-                perm[at + rank] = s;
-                if (lane == 63 - __clzll(peers)) cursor[e] = at + __popcll(peers);
-            }
-            __threadfence_block();  // cursor updates precede the next chunk's reads
         }
+        __syncthreads();
+        if (ok) perm[wcnt[wave][e] + rank] = s;
+        __syncthreads();
     }
 }
 
