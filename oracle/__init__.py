@@ -9,6 +9,7 @@ marshals numpy arrays into it.
 Public functions
 ----------------
 route(logits, k, score)          -> idx int32 [T,k], w float64 [T,k]
+router_logits(x, w_router)       -> float64 [T,E] = x . W_r^T of bf16 inputs
 union(idx, E)                    -> dict(counts, union_ids, n_unique, offsets, perm)
 verify_tokens(layer, x, idx, w, tokens, threads) -> y float64 [len(tokens), d]
 decode_table(kind)               -> float64 array of every code's value
@@ -58,6 +59,7 @@ def lib():
             L = C.CDLL(_LIB)
             p = C.c_void_p
             L.orc_route.argtypes = [p, C.c_int, C.c_int, C.c_int, C.c_int, p, p]
+            L.orc_router_logits.argtypes = [p, p, C.c_int, C.c_int, C.c_int, p]
             L.orc_union.argtypes = [p, C.c_int, C.c_int, C.c_int, p, p, p, p, p]
             L.orc_verify_tokens.argtypes = [C.POINTER(_Layer), p, C.c_int, C.c_int, p, p, C.c_int, p, p,
                                             C.c_int]
@@ -100,6 +102,19 @@ def route(logits, k: int, score: int):
     if rc:
         raise ValueError(f"orc_route rc={rc}")
     return idx, w
+
+
+def router_logits(x, w_router):
+    """fp64 x . W_r^T of bf16 x [T, d] and W_r [E, d] (torch bf16 tensors or uint16 bit arrays)."""
+    xb = _np(x, np.uint16)
+    wb = _np(w_router, np.uint16)
+    T, d = xb.shape
+    E = wb.shape[0]
+    out = np.zeros((T, E), np.float64)
+    rc = lib().orc_router_logits(_ptr(xb), _ptr(wb), T, d, E, _ptr(out))
+    if rc:
+        raise ValueError(f"orc_router_logits rc={rc}")
+    return out
 
 
 def union(idx, E: int) -> dict:

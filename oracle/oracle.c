@@ -170,6 +170,24 @@ int orc_route(const float *logits, int T, int E, int k, int score, int32_t *idx,
     return 0;
 }
 
+/* Router logits (Section 1: the router scores every expert for each token):
+ * logits[t][e] = sum_c x[t][c] * W_r[e][c], x [T][d] and W_r [E][d] bf16
+ * bits, summed in fp64 in index order. */
+int orc_router_logits(const uint16_t *x, const uint16_t *w, int T, int d, int E, double *logits)
+{
+    int t, e, c;
+    if (T < 0 || d < 1 || E < 1)
+        return 1;
+    for (t = 0; t < T; t++)
+        for (e = 0; e < E; e++) {
+            double acc = 0.0;
+            for (c = 0; c < d; c++)
+                acc += orc_bf16(x[(size_t)t * d + c]) * orc_bf16(w[(size_t)e * d + c]);
+            logits[(size_t)t * E + e] = acc;
+        }
+    return 0;
+}
+
 /* ------------------------------------------------------------------ union and grouping */
 
 /* Expert union of the verified tokens (Section 3, Eq. 1), with the grouping the

@@ -173,6 +173,12 @@ def weights_bf16(n_exp: int, N: int, K: int, seed: int = 0, tag="w", device="cpu
     return out
 
 
+def router_weight(E: int, d: int, seed: int = 0, device="cpu", tag="router", std: float = 0.02) -> torch.Tensor:
+    """bf16 router matrix W_r [E, d] ~ N(0, std), d contiguous."""
+    g = generator(seed, tag, device)
+    return (torch.randn(E, d, generator=g, device=device) * std).to(torch.bfloat16)
+
+
 def weights_fp8_b128(n_exp: int, N: int, K: int, seed: int = 0, tag="w", device="cpu",
                      std: float = 0.02) -> tuple[torch.Tensor, torch.Tensor]:
     """FP8 e4m3fn codes [n_exp, N, K] (uint8) and fp32 block scales [n_exp, N/128, K/128].

@@ -118,3 +118,44 @@ def test_exact_u_and_routes_to_logits_roundtrip():
 def test_invalid_expert_index_rejected():
     with pytest.raises(ValueError):
         oracle.union(np.array([[0, 16]], np.int32), 16)
+
+
+# --------------------------------------------------------------------------- router logits (Section 1)
+
+def _bf16_values(t):
+    return t.float().double().numpy()
+
+
+@pytest.mark.parametrize("T,d,E", [(1, 32, 1), (3, 96, 5), (7, 256, 16), (2, 544, 33)])
+def test_router_logits_match_numpy_fp64_product(T, d, E):
+    x = synth.activations(T, d, seed=11)
+    w = synth.router_weight(E, d, seed=11, std=0.5)
+    ref = _bf16_values(x) @ _bf16_values(w).T
+    got = oracle.router_logits(x, w)
+    assert got.shape == (T, E)
+    np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-13)
+
+
+def test_router_logits_one_hot_rows_pick_weight_columns():
+    T, d, E = 5, 64, 9
+    w = synth.router_weight(E, d, seed=12, std=1.0)
+    cols = [0, 17, 31, 32, 63]
+    x = torch.zeros(T, d, dtype=torch.bfloat16)
+    for t, c in enumerate(cols):
+        x[t, c] = 1.0
+    got = oracle.router_logits(x, w)
+    for t, c in enumerate(cols):
+        assert np.array_equal(got[t], _bf16_values(w)[:, c])
+
+
+def test_router_logits_orientation_rows_are_experts():
+    # W_r[e] = (e + 1) everywhere and x[t] = t-th small integer pattern:
+    # logit[t][e] = (e + 1) * sum_c x[t][c]; a transposed operand breaks this.
+    T, d, E = 3, 32, 6
+    w = torch.arange(1, E + 1, dtype=torch.float32)[:, None].expand(E, d).to(torch.bfloat16)
+    x = torch.stack([torch.full((d,), float(t + 1)) * ((torch.arange(d) % 3) - 1) for t in range(T)])
+    x[:, 0] = 5.0
+    x = x.to(torch.bfloat16)
+    got = oracle.router_logits(x, w)
+    rs = _bf16_values(x).sum(1)
+    assert np.array_equal(got, rs[:, None] * np.arange(1, E + 1)[None, :])
