@@ -236,6 +236,52 @@ class TSweep:
         return step_alg_bytes(sh, self.T, U)
 
 
+def router_timing(wl, reps=20, replays=10):
+    """Router from hidden states (x . W_r^T in split-K on the matrix cores, then the top-k that
+    sums the K slices) against top-k from given logits, at the workload's T.  Each is captured
+    `reps` times into one HIP graph and replayed, so host launch cost does not enter."""
+    import torch
+    import synth
+    moe, sh = wl.moe, wl.sh
+    T = wl.T
+    w_r = synth.router_weight(sh.E, sh.d, seed=3, device=wl.dev)
+    ws = torch.empty(moe.moe_router_workspace_size(T, sh.d, sh.E), dtype=torch.uint8, device=wl.dev)
+    idx = torch.empty(T, sh.k, dtype=torch.int32, device=wl.dev)
+    tw = torch.empty(T, sh.k, dtype=torch.float32, device=wl.dev)
+    lg = torch.empty(T, sh.E, dtype=torch.float32, device=wl.dev)
+    idx2, tw2 = torch.empty_like(idx), torch.empty_like(tw)
+    moe.moe_route_topk_hidden(wl.x, w_r, sh.k, sh.score, logits=lg, workspace=ws, topk_idx=idx, topk_w=tw)
+    moe.moe_route_topk(lg, sh.k, sh.score, topk_idx=idx2, topk_w=tw2)
+    torch.cuda.synchronize()
+    consistent = bool(torch.equal(idx, idx2) and torch.equal(tw, tw2))
+
+    def graph_us(fn):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            fn()
+        torch.cuda.current_stream().wait_stream(s)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(replays):
+            g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / (reps * replays)
+
+    hid = graph_us(lambda: moe.moe_route_topk_hidden(wl.x, w_r, sh.k, sh.score, workspace=ws, topk_idx=idx,
+                                                     topk_w=tw))
+    lgt = graph_us(lambda: moe.moe_route_topk(lg, sh.k, sh.score, topk_idx=idx2, topk_w=tw2))
+    return {"T": T, "d": sh.d, "E": sh.E, "router_from_hidden_us": hid, "route_from_logits_us": lgt,
+            "router_gemm_bytes": 2 * sh.E * sh.d + 2 * T * sh.d, "routing_matches_logits_entry": consistent}
+
+
 def pct(v, q):
     s = sorted(v)
     return s[min(len(s) - 1, max(0, int(round(q * (len(s) - 1)))))]
@@ -562,6 +608,10 @@ def main():
             log(f"  T={T:4d}: U~{uniq:5.0f} step {med:8.1f} us")
             del wt
 
+    router = router_timing(wl)
+    log(f"router from hidden states {router['router_from_hidden_us']:.1f} us, "
+        f"top-k from logits {router['route_from_logits_us']:.1f} us")
+
     cpu, err = (None, None)
     if not args.no_cpu:
         log("timing the oracle on the host ...")
@@ -597,6 +647,7 @@ def main():
         "linear_fit_us_vs_U": fit,
         "sweep_T_scattered": sweep_t,
         "stack_8_layers_T16": stack,
+        "router": router,
     }
     print(json.dumps(out))
     return 0

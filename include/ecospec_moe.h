@@ -3,7 +3,7 @@
  *
  * The library computes, for one MoE layer, what a speculative-decoding
  * verifier must do for T draft tokens (EcoSpec, arXiv 2607.12696):
- *   router top-k          -> moe_route_topk
+ *   router top-k          -> moe_route_topk (or moe_route_topk_hidden from x)
  *   expert union, Eq. 1   -> moe_expert_union
  *   grouped SwiGLU experts streaming every activated expert's weights from
  *   HBM once, gate-weighted combine -> moe_verify_layer
@@ -135,6 +135,29 @@ moe_status_t moe_pack_weights(int fmt, int E, int N, int K, const void *w, const
  */
 moe_status_t moe_route_topk(const float *logits, int T, int E, int k, int score, int32_t *topk_idx,
                             float *topk_w, void *stream);
+
+/*
+ * Router from hidden states (Section 1: the router scores every expert for
+ * each token, and the token goes to the top-k of them): logits = x . W_r^T,
+ * then the same top-k and gate weights as moe_route_topk.
+ *   x         [T][d] bf16, device, 16-byte aligned.
+ *   w_router  [E][d] bf16, device, 16-byte aligned.
+ *   topk_idx, topk_w: as for moe_route_topk, ranked on the logits below.
+ *   logits    [T][E] fp32 out, device, or NULL: the router logits the top-k
+ *             was taken on.  Each is the exact bf16 products summed in fp32;
+ *             the reduction order is fixed (within 512-wide slices of d on
+ *             the matrix cores, then over the slices in order), so results
+ *             are deterministic, but they are not the sequential fp32 sum.
+ *   workspace device scratch of moe_router_workspace_size bytes, 16-byte
+ *             aligned; its contents on entry do not matter.
+ * Limits: T >= 1, 1 <= E <= 1024, 1 <= k <= min(E, 64); d % 32 == 0 and x,
+ * W_r each below 2 GiB (else MOE_ERR_UNSUPPORTED).  Two kernels on `stream`,
+ * no allocation.
+ */
+moe_status_t moe_router_workspace_size(int T, int d, int E, size_t *bytes);
+moe_status_t moe_route_topk_hidden(const void *x, const void *w_router, int T, int d, int E, int k, int score,
+                                   int32_t *topk_idx, float *topk_w, float *logits, void *workspace,
+                                   size_t workspace_bytes, void *stream);
 
 /*
  * Expert union and grouping (Section 3, Eq. 1: the verifier must fetch the

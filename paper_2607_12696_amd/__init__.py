@@ -8,6 +8,7 @@ the library has not been built, importing the functions that need it raises
 ``ImportError``; there is no fallback.
 
     moe_route_topk(logits, k, score)            -> (topk_idx, topk_w)
+    moe_route_topk_hidden(x, w_router, k, score) -> (topk_idx, topk_w)
     moe_expert_union(topk_idx, E)               -> Routing
     moe_verify_workspace_size(weights, T, k)    -> bytes
     moe_pack_weights(fmt, w, s)                 -> (w_packed, s_packed)   once per model load
@@ -32,7 +33,7 @@ MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
 MOE_W_BF16, MOE_W_FP8_E4M3_B128, MOE_W_MXFP4 = 0, 1, 2
 MOE_SEL_COST_RATIO, MOE_SEL_CONFIDENCE, MOE_SEL_GLOBAL_COST, MOE_SEL_COST_DIFF = 0, 1, 2, 3
 
-EXPORTED = ("moe_route_topk", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
+EXPORTED = ("moe_route_topk", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
             "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree",
             "moe_status_string", "moe_last_error")
 
@@ -68,6 +69,8 @@ def lib() -> C.CDLL:
             L = C.CDLL(LIB_PATH)
             p, i = C.c_void_p, C.c_int
             L.moe_route_topk.argtypes = [p, i, i, i, i, p, p, p]
+            L.moe_router_workspace_size.argtypes = [i, i, i, C.POINTER(C.c_size_t)]
+            L.moe_route_topk_hidden.argtypes = [p, p, i, i, i, i, i, p, p, p, p, C.c_size_t, p]
             L.moe_expert_union.argtypes = [p, i, i, i, p, p, p, p, p, p]
             L.moe_verify_workspace_size.argtypes = [C.POINTER(moe_weights_t), i, i, C.POINTER(C.c_size_t)]
             L.moe_verify_layer.argtypes = [p, C.POINTER(moe_weights_t), C.POINTER(moe_routing_t), p, p, C.c_size_t, p]
@@ -79,7 +82,7 @@ def lib() -> C.CDLL:
             L.moe_status_string.argtypes = [i]
             L.moe_status_string.restype = C.c_char_p
             L.moe_last_error.restype = C.c_char_p
-            for f in ("moe_route_topk", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
+            for f in ("moe_route_topk", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
                       "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree"):
                 getattr(L, f).restype = i
             _lib = L
@@ -134,6 +137,37 @@ def moe_route_topk(logits, k: int, score: int, topk_idx=None, topk_w=None):
     _check("moe_route_topk", lib().moe_route_topk(_dev_ptr(logits, "logits"), T, E, k, score,
                                                     _dev_ptr(topk_idx, "topk_idx"), _dev_ptr(topk_w, "topk_w"),
                                                     _stream(logits)))
+    return topk_idx, topk_w
+
+
+def moe_router_workspace_size(T: int, d: int, E: int) -> int:
+    n = C.c_size_t(0)
+    _check("moe_router_workspace_size", lib().moe_router_workspace_size(T, d, E, C.byref(n)))
+    return n.value
+
+
+def moe_route_topk_hidden(x, w_router, k: int, score: int, logits=None, workspace=None, topk_idx=None, topk_w=None):
+    """Router logits x . W_r^T (bf16 x [T, d], bf16 W_r [E, d]) and their top-k on the device
+    -> (int32 [T, k], fp32 [T, k]); the fp32 logits land in `logits` [T, E] when it is given."""
+    torch = _torch()
+    T, d = x.shape
+    E, d2 = w_router.shape
+    if d2 != d:
+        raise ValueError("x and w_router disagree on d")
+    if x.dtype != torch.bfloat16 or w_router.dtype != torch.bfloat16:
+        raise ValueError("x and w_router must be bfloat16")
+    if logits is not None and (logits.dtype != torch.float32 or tuple(logits.shape) != (T, E)):
+        raise ValueError("logits must be float32 [T, E]")
+    if topk_idx is None:
+        topk_idx = torch.empty(T, k, dtype=torch.int32, device=x.device)
+    if topk_w is None:
+        topk_w = torch.empty(T, k, dtype=torch.float32, device=x.device)
+    if workspace is None:
+        workspace = torch.empty(moe_router_workspace_size(T, d, E), dtype=torch.uint8, device=x.device)
+    _check("moe_route_topk_hidden", lib().moe_route_topk_hidden(
+        _dev_ptr(x, "x"), _dev_ptr(w_router, "w_router"), T, d, E, k, score, _dev_ptr(topk_idx, "topk_idx"),
+        _dev_ptr(topk_w, "topk_w"), _dev_ptr(logits, "logits"), _dev_ptr(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(x)))
     return topk_idx, topk_w
 
 

@@ -78,7 +78,38 @@ moe_status_t moe_route_topk(const float *logits, int T, int E, int k, int score,
     if (T < 1 || E < 1 || E > kMaxE || k < 1 || k > E || k > kMaxK) return MOE_ERR_INVALID_ARG;
     if ((long)T * E > (1L << 31) - 1 || (long)T * k > kMaxSlots) return MOE_ERR_INVALID_ARG;
     if (score != MOE_SCORE_SOFTMAX && score != MOE_SCORE_SIGMOID) return MOE_ERR_INVALID_ARG;
-    return from_hip(ecospec::launch_route_topk(logits, T, E, k, score, topk_idx, topk_w, (hipStream_t)stream));
+    return from_hip(
+        ecospec::launch_route_topk(logits, 0, T, E, k, score, topk_idx, topk_w, nullptr, (hipStream_t)stream));
+}
+
+moe_status_t moe_router_workspace_size(int T, int d, int E, size_t *bytes)
+{
+    if (!bytes || T < 1 || d < 1 || E < 1 || E > kMaxE) return MOE_ERR_INVALID_ARG;
+    if (d % 32) return MOE_ERR_UNSUPPORTED;
+    *bytes = (size_t)ecospec::router_slices(d) * T * E * 4;
+    return MOE_OK;
+}
+
+moe_status_t moe_route_topk_hidden(const void *x, const void *w_router, int T, int d, int E, int k, int score,
+                                   int32_t *topk_idx, float *topk_w, float *logits, void *workspace,
+                                   size_t workspace_bytes, void *stream)
+{
+    if (!x || !w_router || !topk_idx || !topk_w || !workspace) return MOE_ERR_INVALID_ARG;
+    if (T < 1 || E < 1 || E > kMaxE || k < 1 || k > E || k > kMaxK || d < 1) return MOE_ERR_INVALID_ARG;
+    if ((long)T * k > kMaxSlots || (long)T * E > (1L << 31) - 1) return MOE_ERR_INVALID_ARG;
+    if (score != MOE_SCORE_SOFTMAX && score != MOE_SCORE_SIGMOID) return MOE_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(w_router, 16) || !aligned(workspace, 16)) return MOE_ERR_INVALID_ARG;
+    if (d % 32) return MOE_ERR_UNSUPPORTED;
+    if ((size_t)T * d * 2 >= (1u << 31) || (size_t)E * d * 2 >= (1u << 31)) return MOE_ERR_UNSUPPORTED;
+    const size_t need = (size_t)ecospec::router_slices(d) * T * E * 4;
+    if (workspace_bytes < need) return MOE_ERR_WORKSPACE;
+    float *partial = static_cast<float *>(workspace);
+    hipError_t err = ecospec::launch_router_gemm(static_cast<const uint16_t *>(x),
+                                                 static_cast<const uint16_t *>(w_router), T, d, E, partial,
+                                                 (hipStream_t)stream);
+    if (err != hipSuccess) return from_hip(err);
+    return from_hip(ecospec::launch_route_topk(partial, ecospec::router_slices(d), T, E, k, score, topk_idx, topk_w,
+                                               logits, (hipStream_t)stream));
 }
 
 moe_status_t moe_expert_union(const int32_t *topk_idx, int T, int k, int E, int32_t *counts, int32_t *union_ids,

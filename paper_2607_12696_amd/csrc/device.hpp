@@ -14,6 +14,31 @@ typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 
 constexpr int kWave = 64;
 
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+// Buffer offset beyond every range used here (all ranges are below 2 GiB):
+// a load at it returns zeros.
+constexpr uint32_t kOff = 0x80000000u;
+
+// Raw buffer descriptor over [p, p + bytes): loads at offsets >= bytes return 0.
+// The base goes through readfirstlane: descriptors must live in scalar
+// registers, and a descriptor the compiler cannot prove wave-uniform would
+// turn every load into a loop over the distinct values in the wave.
+__device__ __forceinline__ rsrc_t make_rsrc(const void *p, uint32_t bytes)
+{
+    const uint64_t v = reinterpret_cast<uintptr_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    void *u = reinterpret_cast<void *>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(u, 0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+
+template <int AUX>
+__device__ __forceinline__ u32x4 load16(rsrc_t r, uint32_t off)
+{
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, AUX));
+}
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
 // Butterfly reductions over the 64 lanes of a wavefront; every lane gets the result.

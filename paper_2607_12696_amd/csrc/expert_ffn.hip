@@ -74,32 +74,10 @@ constexpr int kWG = ECOSPEC_WG_WAVES;   // wavefronts per workgroup
 constexpr int kThreads = kWG * kWave;
 constexpr int kBRowsPerPass = kThreads / 16;         // activation rows staged per pass (16 threads per row)
 constexpr int kBPass = kTokGroup / kBRowsPerPass;    // passes per step
-constexpr uint32_t kOff = 0x80000000u;  // buffer offset beyond every range: the load returns zeros
 constexpr int kAuxNT = 2;               // nontemporal: streamed weights should not displace activations
 constexpr int kBRow = 256 + 16;         // LDS bytes per activation row of a step (256 + pad against bank conflicts)
 constexpr int kBBuf = kMB * 16 * kBRow; // LDS bytes of one step's activation tile
 constexpr int kPartialFloats = kWG * 2 * kMB * 4 * kWave;  // one workgroup's accumulators
-
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-
-// Raw buffer descriptor over [p, p + bytes): loads at offsets >= bytes return 0.
-// The base goes through readfirstlane: descriptors must live in scalar
-// registers, and a descriptor the compiler cannot prove wave-uniform would
-// turn every load into a loop over the distinct values in the wave.
-__device__ __forceinline__ rsrc_t make_rsrc(const void *p, uint32_t bytes)
-{
-    const uint64_t v = reinterpret_cast<uintptr_t>(p);
-    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-    void *u = reinterpret_cast<void *>(((uint64_t)hi << 32) | lo);
-    return __builtin_amdgcn_make_buffer_rsrc(u, 0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
-}
-
-template <int AUX>
-__device__ __forceinline__ u32x4 load16(rsrc_t r, uint32_t off)
-{
-    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, AUX));
-}
 
 // Wave-uniform loads through the constant address space (scalar memory).
 __device__ __forceinline__ int ld_s(const int32_t *p)

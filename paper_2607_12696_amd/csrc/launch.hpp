@@ -9,8 +9,15 @@
 
 namespace ecospec {
 
-hipError_t launch_route_topk(const float *logits, int T, int E, int k, int score, int32_t *idx, float *w,
-                             hipStream_t stream);
+// slices == 0: logits [T][E]; slices > 0: router partial sums [slices][T][E]
+// (summed in slice order, and stored to logits_out if it is not null).
+hipError_t launch_route_topk(const float *logits, int slices, int T, int E, int k, int score, int32_t *idx, float *w,
+                             float *logits_out, hipStream_t stream);
+
+// Router K-slice partial sums of x [T][d] . W_router [E][d]^T -> [router_slices(d)][T][E] fp32.
+int router_slices(int d);
+hipError_t launch_router_gemm(const uint16_t *x, const uint16_t *w, int T, int d, int E, float *partial,
+                              hipStream_t stream);
 
 hipError_t launch_expert_union(const int32_t *idx, int T, int k, int E, int32_t *counts, int32_t *union_ids,
                                int32_t *n_unique, int32_t *offsets, int32_t *perm, hipStream_t stream);

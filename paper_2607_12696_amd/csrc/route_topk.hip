@@ -22,21 +22,59 @@ __device__ __forceinline__ uint32_t order_key(float v)
     return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+// slices == 0: `logits` is [T][E].  slices > 0: `logits` holds the router's
+// K-slice partial sums [slices][T][E], added here in slice order; the sums
+// are also stored to logits_out when it is given.
 template <int EPL>  // experts per lane: ceil(E / 64)
-__global__ __launch_bounds__(256) void route_topk_kernel(const float *__restrict__ logits, int T, int E, int k,
-                                                         int score, int32_t *__restrict__ topk_idx,
-                                                         float *__restrict__ topk_w)
+__global__ __launch_bounds__(256) void route_topk_kernel(const float *__restrict__ logits, int slices, int T, int E,
+                                                         int k, int score, int32_t *__restrict__ topk_idx,
+                                                         float *__restrict__ topk_w, float *__restrict__ logits_out)
 {
     const int lane = lane_id();
     const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
     if (t >= T) return;  // uniform per wave
     const float *row = logits + (size_t)t * E;
 
+    float val[EPL];
+    if (slices == 0) {
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) {
+            const int e = lane + kWave * i;
+            val[i] = e < E ? row[e] : 0.f;
+        }
+    } else {
+        // Sum the slices in order, CH at a time with all their loads in flight.
+        constexpr int CH = EPL >= 8 ? 2 : 8;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) val[i] = 0.f;
+        for (int s0 = 0; s0 < slices; s0 += CH) {
+            float p[EPL][CH];
+#pragma unroll
+            for (int c = 0; c < CH; ++c)
+#pragma unroll
+                for (int i = 0; i < EPL; ++i) {
+                    const int e = lane + kWave * i;
+                    p[i][c] = (s0 + c < slices && e < E) ? logits[((size_t)(s0 + c) * T + t) * E + e] : 0.f;
+                }
+#pragma unroll
+            for (int c = 0; c < CH; ++c)
+                if (s0 + c < slices)
+#pragma unroll
+                    for (int i = 0; i < EPL; ++i) val[i] += p[i][c];
+        }
+        if (logits_out) {
+#pragma unroll
+            for (int i = 0; i < EPL; ++i) {
+                const int e = lane + kWave * i;
+                if (e < E) logits_out[(size_t)t * E + e] = val[i];
+            }
+        }
+    }
     uint64_t key[EPL];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
         const int e = lane + kWave * i;
-        key[i] = e < E ? ((uint64_t)order_key(row[e]) << 32) | (uint32_t)~(uint32_t)e : 0ull;
+        key[i] = e < E ? ((uint64_t)order_key(val[i]) << 32) | (uint32_t)~(uint32_t)e : 0ull;
     }
 
     int mine = -1;  // lane r keeps the expert of rank r
@@ -55,8 +93,16 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float *__restrict
         if (lane == r) mine = (int)~(uint32_t)win;
     }
 
+    // The selected logit of each rank, from the lane that holds that expert.
+    float v = 0.f;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        const int src = mine - kWave * i;  // lane holding `mine` in register i
+        const float c = __shfl(val[i], src & (kWave - 1), kWave);
+        if (mine >= kWave * i && mine < kWave * (i + 1)) v = c;
+    }
     const bool sel = lane < k;
-    const float v = sel ? row[mine] : 0.f;
+    if (!sel) v = 0.f;
     float g;
     if (score == 0) {
         const float m = __shfl(v, 0, kWave);  // rank 0 holds the largest logit
@@ -71,14 +117,15 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float *__restrict
     }
 }
 
-hipError_t launch_route_topk(const float *logits, int T, int E, int k, int score, int32_t *idx, float *w,
-                             hipStream_t stream)
+hipError_t launch_route_topk(const float *logits, int slices, int T, int E, int k, int score, int32_t *idx, float *w,
+                             float *logits_out, hipStream_t stream)
 {
     const dim3 block(256), grid((T + 3) / 4);
     const int epl = (E + kWave - 1) / kWave;
-#define ROUTE_CASE(N)                                                                                  \
-    case N:                                                                                            \
-        hipLaunchKernelGGL(route_topk_kernel<N>, grid, block, 0, stream, logits, T, E, k, score, idx, w); \
+#define ROUTE_CASE(N)                                                                                          \
+    case N:                                                                                                    \
+        hipLaunchKernelGGL(route_topk_kernel<N>, grid, block, 0, stream, logits, slices, T, E, k, score, idx, w, \
+                           logits_out);                                                                        \
         break;
     switch (epl) {
         ROUTE_CASE(1) ROUTE_CASE(2) ROUTE_CASE(3) ROUTE_CASE(4) ROUTE_CASE(5) ROUTE_CASE(6) ROUTE_CASE(7)

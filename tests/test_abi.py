@@ -45,6 +45,41 @@ def test_route_topk_rejects(T, E, k, score, null):
     assert L.moe_route_topk(p, T, E, k, score, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG
 
 
+def test_router_workspace_size():
+    L = moe.lib()
+    n = C.c_size_t()
+    assert L.moe_router_workspace_size(64, 7168, 256, C.byref(n)) == moe.MOE_OK
+    assert n.value == 14 * 64 * 256 * 4  # 14 slices of 512 along d
+    assert L.moe_router_workspace_size(3, 544, 33, C.byref(n)) == moe.MOE_OK and n.value == 2 * 3 * 33 * 4
+    assert L.moe_router_workspace_size(4, 80, 16, C.byref(n)) == moe.MOE_ERR_UNSUPPORTED
+    for T, d, E in [(0, 64, 16), (4, 0, 16), (4, 64, 0), (4, 64, 1025)]:
+        assert L.moe_router_workspace_size(T, d, E, C.byref(n)) == moe.MOE_ERR_INVALID_ARG
+    assert L.moe_router_workspace_size(4, 64, 16, None) == moe.MOE_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("T,d,E,k,score,status", [
+    (0, 64, 16, 2, 0, moe.MOE_ERR_INVALID_ARG), (4, 64, 0, 1, 0, moe.MOE_ERR_INVALID_ARG),
+    (4, 64, 16, 0, 0, moe.MOE_ERR_INVALID_ARG), (4, 64, 16, 17, 0, moe.MOE_ERR_INVALID_ARG),
+    (4, 64, 1025, 8, 0, moe.MOE_ERR_INVALID_ARG), (4, 64, 128, 65, 0, moe.MOE_ERR_INVALID_ARG),
+    (4, 64, 16, 2, 2, moe.MOE_ERR_INVALID_ARG), (4, 80, 16, 2, 0, moe.MOE_ERR_UNSUPPORTED),
+    (4, 64, 16, 2, 0, moe.MOE_ERR_WORKSPACE)])
+def test_route_topk_hidden_rejects(T, d, E, k, score, status):
+    L = moe.lib()
+    # workspace of 16 bytes: too small for any valid shape here
+    assert L.moe_route_topk_hidden(FAKE, FAKE, T, d, E, k, score, FAKE, FAKE, None, FAKE, 16, None) == status
+
+
+def test_route_topk_hidden_rejects_null_and_misaligned():
+    L = moe.lib()
+    big = 1 << 20
+    assert L.moe_route_topk_hidden(0, FAKE, 4, 64, 16, 2, 0, FAKE, FAKE, None, FAKE, big, None) == moe.MOE_ERR_INVALID_ARG
+    assert L.moe_route_topk_hidden(FAKE, FAKE, 4, 64, 16, 2, 0, FAKE, FAKE, None, 0, big, None) == moe.MOE_ERR_INVALID_ARG
+    assert L.moe_route_topk_hidden(FAKE + 8, FAKE, 4, 64, 16, 2, 0, FAKE, FAKE, None, FAKE, big,
+                                   None) == moe.MOE_ERR_INVALID_ARG
+    assert L.moe_route_topk_hidden(FAKE, FAKE + 2, 4, 64, 16, 2, 0, FAKE, FAKE, None, FAKE, big,
+                                   None) == moe.MOE_ERR_INVALID_ARG
+
+
 @pytest.mark.parametrize("T,k,E", [(0, 2, 16), (4, 0, 16), (4, 65, 128), (4, 2, 0), (4, 2, 1025), (1 << 20, 32, 64)])
 def test_expert_union_rejects(T, k, E):
     L = moe.lib()

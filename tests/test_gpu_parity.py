@@ -83,6 +83,54 @@ def test_route_nan_and_signed_zero_order():
     assert list(idx_o[0]) == [7, 2, 5, 6, 4, 1, 0, 3]
 
 
+# ----------------------------------------------------------------------------- router from hidden states
+
+def _abs_bits(t):
+    # |value| of bf16 data: clear the sign bit
+    return (t.view(torch.int16) & 0x7FFF).view(torch.bfloat16)
+
+
+# (T, d, E, k, score): DS 7168/256/8 sigmoid; Qwen 4096/128/8; GPT 2880/128/4 (ragged last d slice);
+# toy 256/16/2; E tails (1000 = 62 tiles + 8, 33); T tails across the 64-token wave loop.
+ROUTER_CASES = [(64, 7168, 256, 8, 1), (256, 7168, 256, 8, 1), (37, 4096, 128, 8, 0), (8, 2880, 128, 4, 0),
+                (8, 256, 16, 2, 0), (1, 32, 1, 1, 0), (130, 96, 1000, 64, 0), (3, 544, 33, 5, 1), (65, 2048, 64, 6, 0)]
+
+
+@pytest.mark.parametrize("T,d,E,k,score", ROUTER_CASES)
+def test_router_from_hidden_matches_oracle(T, d, E, k, score):
+    note(f"router T={T} d={d} E={E} k={k} score={score}")
+    x = synth.activations(T, d, seed=T + d)
+    w = synth.router_weight(E, d, seed=E, std=0.02)
+    lg_g = torch.full((T, E), float("nan"), dtype=torch.float32, device=DEV)
+    ws = torch.full((moe.moe_router_workspace_size(T, d, E),), 0x7F, dtype=torch.uint8, device=DEV)
+    idx_g, w_g = moe.moe_route_topk_hidden(x.to(DEV), w.to(DEV), k, score, logits=lg_g, workspace=ws)
+    torch.cuda.synchronize()
+    lg = lg_g.cpu().numpy()
+    ref = oracle.router_logits(x, w)
+    mag = oracle.router_logits(_abs_bits(x), _abs_bits(w))
+    # Exact bf16 products summed in fp32 in any order: |err| <= (d - 1) * 2^-24 * sum |x w|.
+    assert np.all(np.abs(lg.astype(np.float64) - ref) <= d * 2.0 ** -24 * mag + 1e-30)
+    # The top-k decision is taken on the fp32 logits the kernel produced: bit-exact against the oracle
+    # on those same logits, weights to the routing tolerance.
+    idx_o, w_o = oracle.route(lg, k, score)
+    assert np.array_equal(idx_g.cpu().numpy(), idx_o)
+    assert np.abs(w_g.cpu().numpy().astype(np.float64) - w_o).max() <= WTOL
+    # Without a logits buffer the routing is the same, and it is deterministic.
+    idx2, w2 = moe.moe_route_topk_hidden(x.to(DEV), w.to(DEV), k, score)
+    assert torch.equal(idx2, idx_g) and torch.equal(w2, w_g)
+
+
+def test_router_from_hidden_agrees_with_logits_entry():
+    T, d, E, k = 64, 7168, 256, 8
+    x = synth.activations(T, d, seed=5).to(DEV)
+    w = synth.router_weight(E, d, seed=5).to(DEV)
+    lg = torch.empty(T, E, dtype=torch.float32, device=DEV)
+    idx_h, w_h = moe.moe_route_topk_hidden(x, w, k, 1, logits=lg)
+    idx_l, w_l = moe.moe_route_topk(lg, k, 1)
+    torch.cuda.synchronize()
+    assert torch.equal(idx_h, idx_l) and torch.equal(w_h, w_l)
+
+
 @pytest.mark.parametrize("T,E,k,U", [(8, 256, 8, 8), (64, 256, 8, 256), (64, 256, 8, 32), (3, 16, 2, 5),
                                      (4096, 1024, 8, 1000), (1, 1024, 64, 64)])
 def test_union_on_given_routes(T, E, k, U):
