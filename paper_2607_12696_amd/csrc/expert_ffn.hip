@@ -147,6 +147,7 @@ struct FfnParams {
     int workers;          // workgroups of the main kernel's grid
     float *partials;      // [workers][2][kPartialFloats]
     long long *ranges;    // [workers][2]: unit range [x0, x1) of each workgroup, written by the expert kernel
+    long long *fix;       // gate/up only: [workers][4] fix-up record of each workgroup (see write_fix_record)
     long long *cut;       // down only: [groups * nbands] how combine reads each item (see record_cuts)
     const int32_t *plan;  // token groups when T > 64 (else null: one group per expert)
 };
@@ -526,15 +527,36 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
     }
 }
 
+// The contributors of a cut item (units [ib, ie)): the partial-sum slots
+// (workgroup * 2 + slot) of the workgroups whose ranges overlap it, in
+// workgroup order, 20 bits each, their count in bits 60..61 (bit 62 set); or,
+// past 3 contributors, bits 62 and 63 clear and (w0 << 16 | w1), the first
+// and last workgroup.
+__device__ __forceinline__ long long contributors(const FfnParams &P, const Plan &pl, const Split &sp, long ib,
+                                                  long ie)
+{
+    const long KU = (long)P.nbands * P.nsteps;
+    const int w0 = owner_of(sp, pl.n_groups, KU, P.workers, ib);
+    const int w1 = owner_of(sp, pl.n_groups, KU, P.workers, ie - 1);
+    long long packed = 0;
+    int cnt = 0;
+    for (int v = w0; v <= w1; ++v) {
+        long v0, v1;
+        worker_range(sp, v, v0, v1);
+        if (v0 >= v1) continue;
+        if (cnt < 3) packed |= (long long)(2 * v + ((ib <= v0 && v0 < ie) ? 0 : 1)) << (20 * cnt);
+        ++cnt;
+    }
+    return cnt <= 3 ? ((1ll << 62) | ((long long)cnt << 60) | packed) : (long long)((w0 << 16) | w1);
+}
+
 // Down launch: for the combine kernel, how each item this range touches is to
 // be read (every item is touched by some range, so the table is rewritten
-// whole on every launch): -1 if it is whole (its rows are in O); if it is cut,
-// the partial-sum slots (workgroup * 2 + slot) of its contributors in
-// workgroup order, 20 bits each, their count in bits 60..61 (bit 62 set); or,
-// past 3 contributors, bit 63 clear, bit 62 clear and (w0 << 16 | w1).
+// whole on every launch): -1 if it is whole (its rows are in O), else its
+// contributors().
 __device__ __forceinline__ void record_cuts(const FfnParams &P, const Plan &pl, Split &sp, long x0, long x1)
 {
-    const long ns = P.nsteps, KU = (long)P.nbands * ns;
+    const long ns = P.nsteps;
     const long i0 = x0 / ns, i1 = (x1 - 1) / ns;
     for (long item = i0 + threadIdx.x; item <= i1; item += kThreads)
         if (item * ns >= x0 && (item + 1) * ns <= x1) P.cut[item] = -1;
@@ -543,21 +565,35 @@ __device__ __forceinline__ void record_cuts(const FfnParams &P, const Plan &pl, 
     if (i0 * ns < x0 || (i0 + 1) * ns > x1) it[n++] = i0;
     if (i1 != i0 && (i1 + 1) * ns > x1) it[n++] = i1;
     for (int i = 0; i < n; ++i) {
-        const long ib = it[i] * ns, ie = ib + ns;
-        const int w0 = owner_of(sp, pl.n_groups, KU, P.workers, ib);
-        const int w1 = owner_of(sp, pl.n_groups, KU, P.workers, ie - 1);
-        long long packed = 0;
-        int cnt = 0;
-        for (int v = w0; v <= w1; ++v) {
-            long v0, v1;
-            worker_range(sp, v, v0, v1);
-            if (v0 >= v1) continue;
-            if (cnt < 3) packed |= (long long)(2 * v + ((ib <= v0 && v0 < ie) ? 0 : 1)) << (20 * cnt);
-            ++cnt;
-        }
-        if (threadIdx.x == 0)
-            P.cut[it[i]] = cnt <= 3 ? ((1ll << 62) | ((long long)cnt << 60) | packed) : (long long)((w0 << 16) | w1);
+        const long long c = contributors(P, pl, sp, it[i] * ns, (it[i] + 1) * ns);
+        if (threadIdx.x == 0) P.cut[it[i]] = c;
     }
+}
+
+// Gate/up launch, thread 0 of workgroup w: the record its fix-up reads.  If
+// the range starts inside an item that ends within it (w is the item's last
+// contributor), {item, contributors(), first grouped position, tokens} of that
+// item; else item = -1.  Every workgroup writes its record on every launch.
+__device__ __forceinline__ void write_fix_record(const FfnParams &P, const Plan &pl, const Split &sp, int w, long x0,
+                                                 long x1)
+{
+    long long r[4] = {-1, 0, 0, 0};
+    const long ns = P.nsteps;
+    if (x0 < x1) {
+        const long item = x0 / ns, ib = item * ns, ie = ib + ns;
+        if (ib < x0 && ie <= x1) {
+            const int gi = (int)(item / P.nbands);
+            r[0] = item;
+            r[1] = contributors(P, pl, sp, ib, ie);
+            r[2] = sp.gp0[gi];
+            r[3] = sp.gM[gi];
+        }
+    }
+    long long *dst = P.fix + 4 * (size_t)w;
+    dst[0] = r[0];
+    dst[1] = r[1];
+    dst[2] = r[2];
+    dst[3] = r[3];
 }
 
 // Where a wavefront's accumulator (tile t, token block mb) is parked in a
@@ -596,6 +632,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     if (threadIdx.x == 0) {  // for the fix-up (gate/up) and combine (down) kernels
         P.ranges[2 * w] = x0;
         P.ranges[2 * w + 1] = x1;
+        if (!DOWN) write_fix_record(P, pl, sp, w, x0, x1);
     }
     if (x0 >= x1) return;
     const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
@@ -701,72 +738,73 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     if (DOWN) record_cuts(P, pl, sp, x0, x1);
 }
 
-// Finishes the items cut between workgroups: the workgroup whose range holds
-// an item's last unit (but not its first) adds the parked partial sums of
-// every contributor, in workgroup order, and finishes the item.  The ranges
-// come from the expert kernel; the kernel boundary makes its partial sums
-// visible here.
+// Finishes the gate/up items cut between workgroups.  Block w < workers
+// handles the record of workgroup w (an item whose last unit, but not its
+// first, lies in w's range): it adds the parked partial sums of the item's
+// contributors, in workgroup order, and finishes the item.  The blocks past
+// the workers write, for the combine kernel, each routed slot's grouped
+// position and (token group, row in the group), one grouped position per
+// thread.  The kernel boundary makes the expert kernel's records and partial
+// sums visible here.
 template <bool DOWN>
 __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
 {
     const int lane = lane_id();
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int w = blockIdx.x;
-    if (!DOWN && w == (int)gridDim.x - 1) {
-        // For the combine kernel: each routed slot's grouped position and its
-        // (token group, row within the group), one grouped position per thread.
+    if (w >= P.workers) {
         __shared__ int off_s[1025];
         const VerifyArgs &a = P.a;
+        const int p = (w - P.workers) * kThreads + (int)threadIdx.x;
+        const int S = a.T * a.k;
+        const int slot = p < S ? a.perm[p] : 0;  // in flight with the offsets
         const int U = *a.n_unique;
         for (int u = threadIdx.x; u <= U; u += kThreads) off_s[u] = a.offsets[u];
         __syncthreads();
-        for (int p = threadIdx.x; p < a.T * a.k; p += kThreads) {
-            int lo = 0, hi = U - 1;  // the union member u with off_s[u] <= p < off_s[u + 1]
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (off_s[mid] <= p) lo = mid; else hi = mid - 1;
-            }
-            const int o0 = off_s[lo];
-            const int g0 = P.plan ? P.plan[8 + 2 * kMaxGroups + lo] : lo;  // first token group of u
-            const int slot = a.perm[p];
-            a.inv[slot] = p;
-            a.gidx[slot] = ((g0 + (p - o0) / kTokGroup) << 6) | ((p - o0) % kTokGroup);
+        if (p >= S) return;
+        int lo = 0, hi = U - 1;  // the union member u with off_s[u] <= p < off_s[u + 1]
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (off_s[mid] <= p) lo = mid; else hi = mid - 1;
         }
+        const int o0 = off_s[lo];
+        const int g0 = P.plan ? P.plan[8 + 2 * kMaxGroups + lo] : lo;  // first token group of u
+        a.inv[slot] = p;
+        a.gidx[slot] = ((g0 + (p - o0) / kTokGroup) << 6) | ((p - o0) % kTokGroup);
+        return;
     }
-    const long x0 = (long)ld_s64(P.ranges + 2 * w), x1 = (long)ld_s64(P.ranges + 2 * w + 1);
-    if (x0 >= x1) return;
-    const long ns = P.nsteps;
-    const int item = (int)(x0 / ns);
-    const long ib = (long)item * ns, ie = ib + ns;
-    if (ib >= x0 || ie > x1) return;  // not cut before this range, or its end lies beyond it
-    // First contributor: walk back over the ranges that reach into the item.
-    int wf = w;
-    for (int v = w - 1; v >= 0; --v) {
-        const long v0 = (long)ld_s64(P.ranges + 2 * v), v1 = (long)ld_s64(P.ranges + 2 * v + 1);
-        if (v0 >= v1) continue;  // empty range
-        if (v1 <= ib) break;
-        wf = v;
-    }
-    const Plan pl = load_plan(P);
-    const ItemDesc d = describe<DOWN>(P, pl, item);
+    const long long *rec = P.fix + 4 * (size_t)w;
+    const long long item = ld_s64(rec);
+    if (item < 0) return;
+    const long long cut = ld_s64(rec + 1);
+    ItemDesc d{};
+    d.p0 = (int)ld_s64(rec + 2);
+    d.M = (int)ld_s64(rec + 3);
+    d.n0 = (int)(item % P.nbands) * P.band_rows;
     const int nmb = (d.M + 15) / 16;  // only the live token blocks were parked
     f32x4 acc[2][kMB];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int v = wf; v <= w; ++v) {
-        const long v0 = (long)ld_s64(P.ranges + 2 * v), v1 = (long)ld_s64(P.ranges + 2 * v + 1);
-        if (v0 >= v1) continue;
-        const int slot = (ib <= v0 && v0 < ie) ? 0 : 1;  // the item holds v's first unit, or is v's last item
-        const float *src = P.partials + ((size_t)v * 2 + slot) * kPartialFloats;
+    auto add = [&](const float *src) {
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int mb = 0; mb < kMB; ++mb)
-                if (mb < nmb)
-                    acc[t][mb] +=
-                        *reinterpret_cast<const f32x4 *>(src + (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4);
+                if (mb < nmb) acc[t][mb] += *reinterpret_cast<const f32x4 *>(src + partial_offset<DOWN>(wave, t, mb, lane));
+    };
+    if (cut >> 62) {
+        const int cnt = (int)((cut >> 60) & 3);
+        for (int i = 0; i < cnt; ++i) add(P.partials + (size_t)((cut >> (20 * i)) & 0xfffff) * kPartialFloats);
+    } else {
+        // More than three contributors: each one's slot follows from its range.
+        const long ib = (long)item * P.nsteps, ie = ib + P.nsteps;
+        for (int v = (int)(cut >> 16) & 0xffff, w1 = (int)cut & 0xffff; v <= w1; ++v) {
+            const long v0 = (long)ld_s64(P.ranges + 2 * v), v1 = (long)ld_s64(P.ranges + 2 * v + 1);
+            if (v0 >= v1) continue;
+            add(P.partials + ((size_t)v * 2 + ((ib <= v0 && v0 < ie) ? 0 : 1)) * kPartialFloats);
+        }
     }
     finish_item<DOWN>(P, d, wave, acc);
 }
@@ -913,7 +951,8 @@ VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared)
     w.o_offset = align(w.h_bytes);
     w.o_bytes = rows * d * 4;
     w.p_offset = w.o_offset + align(w.o_bytes);
-    w.p_bytes = (size_t)kMaxWorkers * 2 * kPartialFloats * 4 + (size_t)kMaxWorkers * 2 * 8;  // + unit ranges
+    // partial sums, unit ranges, fix-up records
+    w.p_bytes = (size_t)kMaxWorkers * 2 * kPartialFloats * 4 + (size_t)kMaxWorkers * 2 * 8 + (size_t)kMaxWorkers * 4 * 8;
     w.plan_cap = plan_capacity(T, k, shared);
     w.plan_offset = w.p_offset + align(w.p_bytes);
     w.plan_bytes = (8 + 2 * (size_t)kMaxGroups + 1026) * 4;  // groups, then first group per expert
@@ -961,12 +1000,14 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     g.workers = G;
     g.partials = partials;
     g.ranges = reinterpret_cast<long long *>(partials + (size_t)kMaxWorkers * 2 * kPartialFloats);
+    g.fix = g.ranges + (size_t)kMaxWorkers * 2;
     g.cut = reinterpret_cast<long long *>(ws_base + ws.cut_offset);
     g.plan = grouped ? plan : nullptr;
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = mark(events, 1, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false>), dim3(G), dim3(kThreads), 0, stream, g);
+    const int map_blocks = (a.T * a.k + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false>), dim3(G + map_blocks), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     FfnParams dn = g;
