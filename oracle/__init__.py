@@ -10,6 +10,7 @@ Public functions
 ----------------
 route(logits, k, score)          -> idx int32 [T,k], w float64 [T,k]
 router_logits(x, w_router)       -> float64 [T,E] = x . W_r^T of bf16 inputs
+route_grouped(logits, bias, k, n_group, topk_group, scale) -> idx, w (group-limited sigmoid routing)
 union(idx, E)                    -> dict(counts, union_ids, n_unique, offsets, perm)
 verify_tokens(layer, x, idx, w, tokens, threads) -> y float64 [len(tokens), d]
 decode_table(kind)               -> float64 array of every code's value
@@ -59,6 +60,7 @@ def lib():
             L = C.CDLL(_LIB)
             p = C.c_void_p
             L.orc_route.argtypes = [p, C.c_int, C.c_int, C.c_int, C.c_int, p, p]
+            L.orc_route_grouped.argtypes = [p, p, C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, C.c_double, p, p]
             L.orc_router_logits.argtypes = [p, p, C.c_int, C.c_int, C.c_int, p]
             L.orc_union.argtypes = [p, C.c_int, C.c_int, C.c_int, p, p, p, p, p]
             L.orc_verify_tokens.argtypes = [C.POINTER(_Layer), p, C.c_int, C.c_int, p, p, C.c_int, p, p,
@@ -101,6 +103,19 @@ def route(logits, k: int, score: int):
     rc = lib().orc_route(_ptr(lg), T, E, k, score, _ptr(idx), _ptr(w))
     if rc:
         raise ValueError(f"orc_route rc={rc}")
+    return idx, w
+
+
+def route_grouped(logits, bias, k: int, n_group: int, topk_group: int, scale: float):
+    lg = _np(logits, np.float32)
+    T, E = lg.shape
+    b = None if bias is None else _np(bias, np.float32)
+    idx = np.zeros((T, k), np.int32)
+    w = np.zeros((T, k), np.float64)
+    rc = lib().orc_route_grouped(_ptr(lg), None if b is None else _ptr(b), T, E, k, n_group, topk_group,
+                                 float(scale), _ptr(idx), _ptr(w))
+    if rc:
+        raise ValueError(f"orc_route_grouped rc={rc}")
     return idx, w
 
 

@@ -170,6 +170,79 @@ int orc_route(const float *logits, int T, int E, int k, int score, int32_t *idx,
     return 0;
 }
 
+/* Routing order on fp64 scores: larger first, NaN after every number, equal
+ * values by lower index. */
+static int before_d(double a, int ia, double b, int ib)
+{
+    int na = isnan(a), nb = isnan(b);
+    if (na || nb)
+        return (na && nb) ? ia < ib : nb;
+    if (a != b)
+        return a > b;
+    return ia < ib;
+}
+
+static const double *g_sort_d;
+static int cmp_d(const void *pa, const void *pb)
+{
+    int a = *(const int *)pa, b = *(const int *)pb;
+    if (a == b) return 0;
+    return before_d(g_sort_d[a], a, g_sort_d[b], b) ? -1 : 1;
+}
+
+/* Group-limited top-k (DeepSeek-V3 routing; the paper routes each token to a
+ * top-k subset of experts, Section 1, and this is the rule of its DeepSeek
+ * model family).  Per token: s_e = sigmoid(l_e), c_e = s_e + bias_e; the E
+ * experts form G contiguous groups of E/G; a group's score is the sum of its
+ * two highest c (routing order); the TG groups of highest score (ties: lower
+ * group) are kept and the k experts of highest c among them (ties: lower
+ * index) are selected, slot j = rank j.  Weights: w_j = scale * s_j / sum_i
+ * s_i over the selected.  fp64.  bias may be NULL (zero). */
+int orc_route_grouped(const float *logits, const float *bias, int T, int E, int k, int G, int TG, double scale,
+                      int32_t *idx, double *w)
+{
+    int t, e, g, j, gs;
+    double *sv, *cv, *gsc;
+    int *order, *gorder, *cand;
+    if (T < 0 || E < 1 || G < 1 || E % G || E / G < 2 || TG < 1 || TG > G || k < 1 || k > TG * (E / G))
+        return 1;
+    gs = E / G;
+    sv = (double *)malloc(sizeof(double) * (size_t)E);
+    cv = (double *)malloc(sizeof(double) * (size_t)E);
+    gsc = (double *)malloc(sizeof(double) * (size_t)G);
+    order = (int *)malloc(sizeof(int) * (size_t)E);
+    gorder = (int *)malloc(sizeof(int) * (size_t)G);
+    cand = (int *)malloc(sizeof(int) * (size_t)E);
+    for (t = 0; t < T; t++) {
+        int nc = 0;
+        double sum = 0.0;
+        for (e = 0; e < E; e++) {
+            sv[e] = 1.0 / (1.0 + exp(-(double)logits[(size_t)t * E + e]));
+            cv[e] = sv[e] + (bias ? (double)bias[e] : 0.0);
+        }
+        g_sort_d = cv;
+        for (g = 0; g < G; g++) {
+            for (j = 0; j < gs; j++) order[j] = g * gs + j;
+            qsort(order, (size_t)gs, sizeof(int), cmp_d);
+            gsc[g] = cv[order[0]] + cv[order[1]];
+        }
+        for (g = 0; g < G; g++) gorder[g] = g;
+        g_sort_d = gsc;
+        qsort(gorder, (size_t)G, sizeof(int), cmp_d);
+        for (g = 0; g < TG; g++)
+            for (j = 0; j < gs; j++) cand[nc++] = gorder[g] * gs + j;
+        g_sort_d = cv;
+        qsort(cand, (size_t)nc, sizeof(int), cmp_d);
+        for (j = 0; j < k; j++) {
+            idx[(size_t)t * k + j] = cand[j];
+            sum += sv[cand[j]];
+        }
+        for (j = 0; j < k; j++) w[(size_t)t * k + j] = scale * sv[cand[j]] / sum;
+    }
+    free(sv); free(cv); free(gsc); free(order); free(gorder); free(cand);
+    return 0;
+}
+
 /* Router logits (Section 1: the router scores every expert for each token):
  * logits[t][e] = sum_c x[t][c] * W_r[e][c], x [T][d] and W_r [E][d] bf16
  * bits, summed in fp64 in index order. */

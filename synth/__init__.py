@@ -99,6 +99,12 @@ def logits_scattered(T: int, E: int, seed: int = 0, device="cpu", tag="logits") 
     return torch.randn(T, E, generator=g, device=device, dtype=torch.float32)
 
 
+def router_bias(E: int, seed: int = 0, device="cpu", tag="rbias", amp: float = 0.1) -> torch.Tensor:
+    """fp32 per-expert routing correction bias [E] ~ U(-amp, amp)."""
+    g = generator(seed, tag, device)
+    return (torch.rand(E, generator=g, device=device) * 2 - 1) * amp
+
+
 def logits_tie_grid(T: int, E: int, seed: int = 0, device="cpu", tag="ties") -> torch.Tensor:
     """Logits on a 0.5 grid in [-2, 2], so that many entries tie exactly (incl. -0.0)."""
     g = generator(seed, tag, device)

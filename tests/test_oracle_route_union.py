@@ -159,3 +159,72 @@ def test_router_logits_orientation_rows_are_experts():
     got = oracle.router_logits(x, w)
     rs = _bf16_values(x).sum(1)
     assert np.array_equal(got, rs[:, None] * np.arange(1, E + 1)[None, :])
+
+
+# --------------------------------------------------------------------------- group-limited routing
+
+def test_grouped_route_hand_example():
+    # E=8 in G=4 pairs, keep 2 groups, k=4.  All logits 0 -> s = 0.5 and c = 0.5 + bias.
+    # Group scores (top-2 sums): g0 0.95+0.5=1.45, g1 0.8+0.75=1.55, g2 0.55+0.5=1.05, g3 0.7+0.7=1.4.
+    # Kept: g1, g0 -> candidates 0..3, ranked by c: 0 (0.95), 2 (0.8), 3 (0.75), 1 (0.5).  Plain top-4
+    # of c would take expert 6 (0.7) instead of 1.  Weights: equal s, so 2.5 / 4 each.
+    lg = np.zeros((1, 8), np.float32)
+    b = np.array([0.45, 0, 0.3, 0.25, 0, 0.05, 0.2, 0.2], np.float32)
+    idx, w = oracle.route_grouped(lg, b, 4, 4, 2, 2.5)
+    assert list(idx[0]) == [0, 2, 3, 1]
+    np.testing.assert_allclose(w[0], [0.625] * 4, rtol=0, atol=1e-15)
+    # The bias steers the choice but not the weights: raise s of expert 2 (logit ln 3 -> s = 3/4).
+    lg[0, 2] = np.float32(np.log(3.0))
+    idx, w = oracle.route_grouped(lg, b, 4, 4, 2, 1.0)
+    assert list(idx[0]) == [2, 0, 3, 1]  # c: 1.05, 0.95, 0.75, 0.5
+    s2 = 1.0 / (1.0 + np.exp(-np.float64(lg[0, 2])))
+    np.testing.assert_allclose(w[0], np.array([s2, 0.5, 0.5, 0.5]) / (s2 + 1.5), rtol=1e-15)
+
+
+def test_grouped_route_one_group_is_plain_sigmoid_topk():
+    T, E, k = 16, 64, 6
+    lg = synth.logits_scattered(T, E, seed=21).numpy()
+    idx, w = oracle.route_grouped(lg, None, k, 1, 1, 1.0)
+    idx_p, w_p = oracle.route(lg, k, 1)
+    assert np.array_equal(idx, idx_p)
+    np.testing.assert_allclose(w, w_p, rtol=1e-13)
+
+
+def _grouped_brute(lg, b, k, G, TG, scale):
+    """Best TG-subset of groups by enumeration, then a full sort of the candidates."""
+    import itertools
+    T, E = lg.shape
+    gs = E // G
+    out_i, out_w = [], []
+    for t in range(T):
+        s = 1.0 / (1.0 + np.exp(-lg[t].astype(np.float64)))
+        c = s + (0.0 if b is None else b.astype(np.float64))
+        gsc = np.sort(c.reshape(G, gs), axis=1)[:, ::-1][:, :2].sum(1)
+        best = max(itertools.combinations(range(G), TG), key=lambda sub: gsc[list(sub)].sum())
+        cand = np.concatenate([np.arange(g * gs, (g + 1) * gs) for g in sorted(best)])
+        sel = cand[np.argsort(-c[cand], kind="stable")[:k]]
+        out_i.append(sel)
+        out_w.append(scale * s[sel] / s[sel].sum())
+    return np.array(out_i), np.array(out_w)
+
+
+@pytest.mark.parametrize("E,G,TG,k,bias", [(256, 8, 4, 8, True), (32, 4, 2, 4, False), (64, 16, 3, 5, True),
+                                           (24, 3, 3, 7, True), (256, 8, 1, 8, True)])
+def test_grouped_route_matches_subset_enumeration(E, G, TG, k, bias):
+    T = 12
+    lg = synth.logits_scattered(T, E, seed=E + G).numpy()
+    b = synth.router_bias(E, seed=E).numpy() if bias else None
+    idx, w = oracle.route_grouped(lg, b, k, G, TG, 2.5)
+    ri, rw = _grouped_brute(lg, b, k, G, TG, 2.5)
+    assert np.array_equal(idx, ri)
+    np.testing.assert_allclose(w, rw, rtol=1e-13)
+    # invariants: at most TG groups touched, weights sum to the scale
+    assert all(len(set(int(e) // (E // G) for e in row)) <= TG for row in idx)
+    np.testing.assert_allclose(w.sum(1), 2.5, rtol=1e-13)
+
+
+def test_grouped_route_rejects_bad_shapes():
+    lg = np.zeros((1, 12), np.float32)
+    for args in [(4, 5, 2), (4, 12, 2), (4, 4, 5), (7, 4, 2), (4, 4, 0)]:  # E%G, E/G<2, TG>G, k>TG*E/G, TG<1
+        with pytest.raises(ValueError):
+            oracle.route_grouped(lg, None, args[0], args[1], args[2], 1.0)
