@@ -3,7 +3,8 @@
  *
  * The library computes, for one MoE layer, what a speculative-decoding
  * verifier must do for T draft tokens (EcoSpec, arXiv 2607.12696):
- *   router top-k          -> moe_route_topk (or moe_route_topk_hidden from x)
+ *   router top-k          -> moe_route_topk (or moe_route_topk_hidden from x,
+ *                            moe_route_topk_grouped for group-limited routing)
  *   expert union, Eq. 1   -> moe_expert_union
  *   grouped SwiGLU experts streaming every activated expert's weights from
  *   HBM once, gate-weighted combine -> moe_verify_layer
@@ -135,6 +136,26 @@ moe_status_t moe_pack_weights(int fmt, int E, int N, int K, const void *w, const
  */
 moe_status_t moe_route_topk(const float *logits, int T, int E, int k, int score, int32_t *topk_idx,
                             float *topk_w, void *stream);
+
+/*
+ * Group-limited router top-k: the routing rule of the DeepSeek-V3 family (the
+ * DeepSeek-V3.1 rows of Tables 1-13; Section 1 only fixes that each token goes
+ * to a top-k subset of experts).  Per token, from the fp32 logits l:
+ *   s_e = sigmoid(l_e), c_e = s_e + bias_e (bias NULL: zero);
+ *   the E experts form n_group contiguous groups of E / n_group; a group's
+ *   score is the sum of its two highest c (in routing order: NaN below every
+ *   number, so it only counts in a group with fewer than two numbers);
+ *   the topk_group groups of highest score stay eligible (ties: lower group);
+ *   the k eligible experts of highest c are selected, in order (ties: lower
+ *   index), slot j holding rank j;
+ *   topk_w[j] = scale * s_j / sum_i s_i over the selected, in fp32.
+ *   logits [T][E], bias [E], topk_idx / topk_w [T][k]: fp32 / int32 device.
+ * Limits: T >= 1, 1 <= E <= 1024, 1 <= n_group <= 64, E % n_group == 0,
+ * E / n_group >= 2, 1 <= topk_group <= n_group, 1 <= k <= min(64,
+ * topk_group * E / n_group), scale finite; else MOE_ERR_INVALID_ARG.
+ */
+moe_status_t moe_route_topk_grouped(const float *logits, const float *bias, int T, int E, int k, int n_group,
+                                    int topk_group, float scale, int32_t *topk_idx, float *topk_w, void *stream);
 
 /*
  * Router from hidden states (Section 1: the router scores every expert for

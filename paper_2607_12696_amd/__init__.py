@@ -9,6 +9,7 @@ the library has not been built, importing the functions that need it raises
 
     moe_route_topk(logits, k, score)            -> (topk_idx, topk_w)
     moe_route_topk_hidden(x, w_router, k, score) -> (topk_idx, topk_w)
+    moe_route_topk_grouped(logits, bias, k, n_group, topk_group, scale) -> (topk_idx, topk_w)
     moe_expert_union(topk_idx, E)               -> Routing
     moe_verify_workspace_size(weights, T, k)    -> bytes
     moe_pack_weights(fmt, w, s)                 -> (w_packed, s_packed)   once per model load
@@ -33,7 +34,7 @@ MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
 MOE_W_BF16, MOE_W_FP8_E4M3_B128, MOE_W_MXFP4 = 0, 1, 2
 MOE_SEL_COST_RATIO, MOE_SEL_CONFIDENCE, MOE_SEL_GLOBAL_COST, MOE_SEL_COST_DIFF = 0, 1, 2, 3
 
-EXPORTED = ("moe_route_topk", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
+EXPORTED = ("moe_route_topk", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
             "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree",
             "moe_status_string", "moe_last_error")
 
@@ -69,6 +70,7 @@ def lib() -> C.CDLL:
             L = C.CDLL(LIB_PATH)
             p, i = C.c_void_p, C.c_int
             L.moe_route_topk.argtypes = [p, i, i, i, i, p, p, p]
+            L.moe_route_topk_grouped.argtypes = [p, p, i, i, i, i, i, C.c_float, p, p, p]
             L.moe_router_workspace_size.argtypes = [i, i, i, C.POINTER(C.c_size_t)]
             L.moe_route_topk_hidden.argtypes = [p, p, i, i, i, i, i, p, p, p, p, C.c_size_t, p]
             L.moe_expert_union.argtypes = [p, i, i, i, p, p, p, p, p, p]
@@ -82,7 +84,7 @@ def lib() -> C.CDLL:
             L.moe_status_string.argtypes = [i]
             L.moe_status_string.restype = C.c_char_p
             L.moe_last_error.restype = C.c_char_p
-            for f in ("moe_route_topk", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
+            for f in ("moe_route_topk", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
                       "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree"):
                 getattr(L, f).restype = i
             _lib = L
@@ -137,6 +139,24 @@ def moe_route_topk(logits, k: int, score: int, topk_idx=None, topk_w=None):
     _check("moe_route_topk", lib().moe_route_topk(_dev_ptr(logits, "logits"), T, E, k, score,
                                                     _dev_ptr(topk_idx, "topk_idx"), _dev_ptr(topk_w, "topk_w"),
                                                     _stream(logits)))
+    return topk_idx, topk_w
+
+
+def moe_route_topk_grouped(logits, bias, k: int, n_group: int, topk_group: int, scale: float, topk_idx=None,
+                           topk_w=None):
+    """Group-limited sigmoid routing (correction bias [E] or None, routed scaling `scale`) of fp32
+    logits [T, E] on the device -> (int32 [T, k], fp32 [T, k])."""
+    torch = _torch()
+    T, E = logits.shape
+    if logits.dtype != torch.float32 or (bias is not None and (bias.dtype != torch.float32 or bias.numel() != E)):
+        raise ValueError("logits [T, E] and bias [E] must be float32")
+    if topk_idx is None:
+        topk_idx = torch.empty(T, k, dtype=torch.int32, device=logits.device)
+    if topk_w is None:
+        topk_w = torch.empty(T, k, dtype=torch.float32, device=logits.device)
+    _check("moe_route_topk_grouped", lib().moe_route_topk_grouped(
+        _dev_ptr(logits, "logits"), _dev_ptr(bias, "bias"), T, E, k, n_group, topk_group, scale,
+        _dev_ptr(topk_idx, "topk_idx"), _dev_ptr(topk_w, "topk_w"), _stream(logits)))
     return topk_idx, topk_w
 
 

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include "launch.hpp"
+#include <math.h>
 
 namespace {
 
@@ -80,6 +81,19 @@ moe_status_t moe_route_topk(const float *logits, int T, int E, int k, int score,
     if (score != MOE_SCORE_SOFTMAX && score != MOE_SCORE_SIGMOID) return MOE_ERR_INVALID_ARG;
     return from_hip(
         ecospec::launch_route_topk(logits, 0, T, E, k, score, topk_idx, topk_w, nullptr, (hipStream_t)stream));
+}
+
+moe_status_t moe_route_topk_grouped(const float *logits, const float *bias, int T, int E, int k, int n_group,
+                                    int topk_group, float scale, int32_t *topk_idx, float *topk_w, void *stream)
+{
+    if (!logits || !topk_idx || !topk_w) return MOE_ERR_INVALID_ARG;
+    if (T < 1 || E < 1 || E > kMaxE || k < 1 || k > kMaxK) return MOE_ERR_INVALID_ARG;
+    if ((long)T * E > (1L << 31) - 1 || (long)T * k > kMaxSlots) return MOE_ERR_INVALID_ARG;
+    if (n_group < 1 || n_group > 64 || E % n_group || E / n_group < 2) return MOE_ERR_INVALID_ARG;
+    if (topk_group < 1 || topk_group > n_group || k > topk_group * (E / n_group)) return MOE_ERR_INVALID_ARG;
+    if (!(scale == scale) || scale == INFINITY || scale == -INFINITY) return MOE_ERR_INVALID_ARG;
+    return from_hip(ecospec::launch_route_grouped(logits, bias, T, E, k, n_group, topk_group, scale, topk_idx,
+                                                  topk_w, (hipStream_t)stream));
 }
 
 moe_status_t moe_router_workspace_size(int T, int d, int E, size_t *bytes)

@@ -14,6 +14,10 @@ namespace ecospec {
 hipError_t launch_route_topk(const float *logits, int slices, int T, int E, int k, int score, int32_t *idx, float *w,
                              float *logits_out, hipStream_t stream);
 
+// Group-limited sigmoid routing with correction bias (may be null) and scaling.
+hipError_t launch_route_grouped(const float *logits, const float *bias, int T, int E, int k, int G, int TG,
+                                float scale, int32_t *idx, float *w, hipStream_t stream);
+
 // Router K-slice partial sums of x [T][d] . W_router [E][d]^T -> [router_slices(d)][T][E] fp32.
 int router_slices(int d);
 hipError_t launch_router_gemm(const uint16_t *x, const uint16_t *w, int T, int d, int E, float *partial,

@@ -22,6 +22,44 @@ __device__ __forceinline__ uint32_t order_key(float v)
     return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+// k rounds of a wave-wide max over the experts' keys (expert e = lane + 64 i
+// in register i; key 0 = not eligible): lane r returns the expert of rank r.
+template <int EPL>
+__device__ __forceinline__ int select_ranks(uint64_t (&key)[EPL], int k)
+{
+    const int lane = lane_id();
+    int mine = -1;
+    for (int r = 0; r < k; ++r) {
+        uint64_t best = 0ull;
+        int bi = -1;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i)
+            if (key[i] > best) { best = key[i]; bi = i; }
+        const uint64_t win = wave_max_u64(best);
+        if (bi >= 0 && best == win) {
+#pragma unroll
+            for (int i = 0; i < EPL; ++i)
+                if (i == bi) key[i] = 0ull;
+        }
+        if (lane == r) mine = (int)~(uint32_t)win;
+    }
+    return mine;
+}
+
+// val of expert `mine` (held by lane mine % 64 in register mine / 64).  Call
+// it from every lane: a lane-permute reads nothing from inactive lanes.
+template <int EPL>
+__device__ __forceinline__ float value_of(const float (&val)[EPL], int mine)
+{
+    float v = 0.f;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        const float c = __shfl(val[i], (mine - kWave * i) & (kWave - 1), kWave);
+        if (mine >= kWave * i && mine < kWave * (i + 1)) v = c;
+    }
+    return v;
+}
+
 // slices == 0: `logits` is [T][E].  slices > 0: `logits` holds the router's
 // K-slice partial sums [slices][T][E], added here in slice order; the sums
 // are also stored to logits_out when it is given.
@@ -77,32 +115,10 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float *__restrict
         key[i] = e < E ? ((uint64_t)order_key(val[i]) << 32) | (uint32_t)~(uint32_t)e : 0ull;
     }
 
-    int mine = -1;  // lane r keeps the expert of rank r
-    for (int r = 0; r < k; ++r) {
-        uint64_t best = 0ull;
-        int bi = -1;
-#pragma unroll
-        for (int i = 0; i < EPL; ++i)
-            if (key[i] > best) { best = key[i]; bi = i; }
-        const uint64_t win = wave_max_u64(best);
-        if (bi >= 0 && best == win) {
-#pragma unroll
-            for (int i = 0; i < EPL; ++i)
-                if (i == bi) key[i] = 0ull;
-        }
-        if (lane == r) mine = (int)~(uint32_t)win;
-    }
-
-    // The selected logit of each rank, from the lane that holds that expert.
-    float v = 0.f;
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-        const int src = mine - kWave * i;  // lane holding `mine` in register i
-        const float c = __shfl(val[i], src & (kWave - 1), kWave);
-        if (mine >= kWave * i && mine < kWave * (i + 1)) v = c;
-    }
+    const int mine = select_ranks(key, k);
     const bool sel = lane < k;
-    if (!sel) v = 0.f;
+    const float vm = value_of(val, mine);  // every lane takes part in the shuffles
+    const float v = sel ? vm : 0.f;
     float g;
     if (score == 0) {
         const float m = __shfl(v, 0, kWave);  // rank 0 holds the largest logit
@@ -115,6 +131,100 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float *__restrict
         topk_idx[(size_t)t * k + lane] = mine;
         topk_w[(size_t)t * k + lane] = g / s;
     }
+}
+
+// Group-limited routing (the DeepSeek-V3 rule): sigmoid scores s, choice
+// scores c = s + bias; the E experts form G contiguous groups of gs = E / G
+// (gs >= 2); a group's score is the sum of its two highest choice scores (in
+// the routing order of order_key, so NaN only counts when a group has fewer
+// than two numbers); the TG groups of highest score (ties: lower group) stay
+// eligible and the k highest choice scores among their experts are selected,
+// in order.  Gate weights: scale * s / sum(s) over the selected.  One
+// wavefront per token; the choice scores go through LDS so that lane g can
+// score group g.
+template <int EPL>
+__global__ __launch_bounds__(256) void route_grouped_kernel(const float *__restrict__ logits,
+                                                            const float *__restrict__ bias, int T, int E, int k,
+                                                            int G, int TG, float scale, int32_t *__restrict__ topk_idx,
+                                                            float *__restrict__ topk_w)
+{
+    __shared__ float cs[4][1024];
+    const int lane = lane_id(), wv = threadIdx.x / kWave;
+    const int t = blockIdx.x * 4 + wv;
+    const bool active = t < T;
+    const int gs = E / G;
+    float sv[EPL], cv[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        const int e = lane + kWave * i;
+        const float l = (active && e < E) ? logits[(size_t)t * E + e] : 0.f;
+        sv[i] = 1.f / (1.f + expf(-l));
+        cv[i] = sv[i] + ((bias && e < E) ? bias[e] : 0.f);
+        if (e < E) cs[wv][e] = cv[i];
+    }
+    __syncthreads();
+    if (!active) return;  // uniform per wave, after the block's only barrier
+
+    uint64_t gkey = 0ull;
+    if (lane < G) {
+        uint32_t k1 = 0u, k2 = 0u;
+        float v1 = 0.f, v2 = 0.f;
+        bool h1 = false, h2 = false;
+        for (int j = 0; j < gs; ++j) {
+            const float v = cs[wv][lane * gs + j];
+            const uint32_t kv = order_key(v);
+            if (!h1 || kv > k1) {
+                k2 = k1; v2 = v1; h2 = h1;
+                k1 = kv; v1 = v; h1 = true;
+            } else if (!h2 || kv > k2) {
+                k2 = kv; v2 = v; h2 = true;
+            }
+        }
+        gkey = ((uint64_t)order_key(v1 + v2) << 32) | (uint32_t)~(uint32_t)lane;
+    }
+    uint64_t gmask = 0ull;  // bit g: group g stays eligible
+    for (int r = 0; r < TG; ++r) {
+        const uint64_t m = wave_max_u64(gkey);
+        const int g = (int)~(uint32_t)m;
+        gmask |= 1ull << g;
+        if (lane == g) gkey = 0ull;
+    }
+    uint64_t key[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        const int e = lane + kWave * i;
+        key[i] = (e < E && ((gmask >> (e / gs)) & 1ull)) ? ((uint64_t)order_key(cv[i]) << 32) | (uint32_t)~(uint32_t)e
+                                                          : 0ull;
+    }
+    const int mine = select_ranks(key, k);
+    const bool sel = lane < k;
+    const float sm = value_of(sv, mine);  // every lane takes part in the shuffles
+    const float g = sel ? sm : 0.f;
+    const float sum = wave_sum(g);
+    if (sel) {
+        topk_idx[(size_t)t * k + lane] = mine;
+        topk_w[(size_t)t * k + lane] = scale * (g / sum);
+    }
+}
+
+hipError_t launch_route_grouped(const float *logits, const float *bias, int T, int E, int k, int G, int TG,
+                                float scale, int32_t *idx, float *w, hipStream_t stream)
+{
+    const dim3 block(256), grid((T + 3) / 4);
+    const int epl = (E + kWave - 1) / kWave;
+#define GROUPED_CASE(N)                                                                                         \
+    case N:                                                                                                     \
+        hipLaunchKernelGGL(route_grouped_kernel<N>, grid, block, 0, stream, logits, bias, T, E, k, G, TG, scale, \
+                           idx, w);                                                                             \
+        break;
+    switch (epl) {
+        GROUPED_CASE(1) GROUPED_CASE(2) GROUPED_CASE(3) GROUPED_CASE(4) GROUPED_CASE(5) GROUPED_CASE(6)
+        GROUPED_CASE(7) GROUPED_CASE(8) GROUPED_CASE(9) GROUPED_CASE(10) GROUPED_CASE(11) GROUPED_CASE(12)
+        GROUPED_CASE(13) GROUPED_CASE(14) GROUPED_CASE(15) GROUPED_CASE(16)
+    default: return hipErrorInvalidValue;
+    }
+#undef GROUPED_CASE
+    return hipGetLastError();
 }
 
 hipError_t launch_route_topk(const float *logits, int slices, int T, int E, int k, int score, int32_t *idx, float *w,

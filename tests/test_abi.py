@@ -45,6 +45,18 @@ def test_route_topk_rejects(T, E, k, score, null):
     assert L.moe_route_topk(p, T, E, k, score, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("T,E,k,G,TG,scale,null", [
+    (0, 256, 8, 8, 4, 2.5, False), (4, 256, 0, 8, 4, 2.5, False), (4, 256, 65, 8, 4, 2.5, False),
+    (4, 1025, 8, 8, 4, 2.5, False), (4, 256, 8, 0, 4, 2.5, False), (4, 256, 8, 128, 4, 2.5, False),
+    (4, 250, 8, 8, 4, 2.5, False), (4, 16, 2, 16, 4, 2.5, False), (4, 256, 8, 8, 0, 2.5, False),
+    (4, 256, 8, 8, 9, 2.5, False), (4, 256, 33, 8, 1, 2.5, False), (4, 256, 8, 8, 4, float("nan"), False),
+    (4, 256, 8, 8, 4, float("inf"), False), (4, 256, 8, 8, 4, 2.5, True)])
+def test_route_topk_grouped_rejects(T, E, k, G, TG, scale, null):
+    L = moe.lib()
+    p = 0 if null else FAKE
+    assert L.moe_route_topk_grouped(p, None, T, E, k, G, TG, scale, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG
+
+
 def test_router_workspace_size():
     L = moe.lib()
     n = C.c_size_t()
