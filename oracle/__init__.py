@@ -49,7 +49,10 @@ class _Layer(C.Structure):
                 ("down", C.POINTER(C.c_void_p)), ("s_gate", C.POINTER(C.c_void_p)),
                 ("s_up", C.POINTER(C.c_void_p)), ("s_down", C.POINTER(C.c_void_p)),
                 ("sh_gate", C.c_void_p), ("sh_up", C.c_void_p), ("sh_down", C.c_void_p),
-                ("sh_s_gate", C.c_void_p), ("sh_s_up", C.c_void_p), ("sh_s_down", C.c_void_p)]
+                ("sh_s_gate", C.c_void_p), ("sh_s_up", C.c_void_p), ("sh_s_down", C.c_void_p),
+                ("act", C.c_int), ("alpha", C.c_double), ("limit", C.c_double),
+                ("b_gate", C.POINTER(C.c_void_p)), ("b_up", C.POINTER(C.c_void_p)),
+                ("b_down", C.POINTER(C.c_void_p))]
 
 
 def lib():
@@ -162,7 +165,10 @@ def verify_tokens(layer: dict, x, idx, w, tokens=None, threads: int = 1):
 
     ``layer`` holds fmt, d, d_ff and either stacked arrays gate/up/down
     [E, N, K(/2)] (+ s_gate/s_up/s_down) or dicts {expert id: array} for just
-    the experts that are needed, plus optional sh_* arrays of the shared expert.
+    the experts that are needed, plus optional sh_* arrays of the shared expert,
+    optional fp32 biases b_gate/b_up [E, d_ff] and b_down [E, d] (same forms) and
+    the activation: act 0 (SwiGLU, default) or 1 (GPT-OSS clamped SwiGLU with
+    alpha and limit).
     """
     fmt, d, d_ff = int(layer["fmt"]), int(layer["d"]), int(layer["d_ff"])
     wdt = {0: np.uint16, 1: np.uint8, 2: np.uint8}[fmt]
@@ -189,6 +195,15 @@ def verify_tokens(layer: dict, x, idx, w, tokens=None, threads: int = 1):
 
     lay = _Layer()
     lay.fmt, lay.d, lay.d_ff, lay.n_experts = fmt, d, d_ff, n_exp
+    lay.act = int(layer.get("act", 0))
+    lay.alpha = float(layer.get("alpha", 1.702))
+    lay.limit = float(layer.get("limit", 7.0))
+    for name in ("b_gate", "b_up", "b_down"):
+        g = getter(name, np.float32)
+        if g is not None:
+            arr, kp = _expert_ptrs(g, n_exp)
+            keep += [arr, kp]
+            setattr(lay, name, C.cast(arr, C.POINTER(C.c_void_p)))
     for name in ("gate", "up", "down"):
         arr, kp = _expert_ptrs(getter(name, wdt), n_exp)
         keep += [arr, kp]

@@ -307,11 +307,20 @@ typedef struct {
     const void *const *s_down;
     const void *sh_gate, *sh_up, *sh_down;       /* shared expert, or NULL */
     const void *sh_s_gate, *sh_s_up, *sh_s_down;
+    int act;                   /* 0: SwiGLU; 1: clamped SwiGLU of GPT-OSS (alpha, limit, up + 1) */
+    double alpha, limit;
+    const void *const *b_gate; /* fp32 biases per routed expert ([d_ff], [d_ff], [d]); NULL array = none */
+    const void *const *b_up;
+    const void *const *b_down;
 } orc_layer;
 
-/* o[m] = sum_n h_n W_down[m][n], h_n = silu(sum_c x_c W_gate[n][c]) * sum_c x_c W_up[n][c]. */
+/* One expert FFN.  g_n = sum_c x_c W_gate[n][c] + bg_n, v_n = sum_c x_c W_up[n][c] + bu_n
+ * (biases NULL: zero).  act 0: h_n = silu(g_n) * v_n.  act 1 (GPT-OSS): g clamped
+ * from above at `limit`, v clamped to [-limit, limit], h_n = g sigmoid(alpha g) (v + 1).
+ * o[m] = sum_n h_n W_down[m][n] + bd_m. */
 static void swiglu_expert(int fmt, int d, int d_ff, const void *wg, const void *wu, const void *wd,
-                          const void *sg, const void *su, const void *sd, const double *x,
+                          const void *sg, const void *su, const void *sd, int act, double alpha,
+                          double limit, const float *bg, const float *bu, const float *bd, const double *x,
                           double *h, double *o)
 {
     int n, c, m;
@@ -321,12 +330,21 @@ static void swiglu_expert(int fmt, int d, int d_ff, const void *wg, const void *
             g += x[c] * weight_at(fmt, wg, sg, d_ff, d, n, c);
             v += x[c] * weight_at(fmt, wu, su, d_ff, d, n, c);
         }
-        h[n] = g / (1.0 + exp(-g)) * v;
+        if (bg) g += (double)bg[n];
+        if (bu) v += (double)bu[n];
+        if (act == 0) {
+            h[n] = g / (1.0 + exp(-g)) * v;
+        } else {
+            if (g > limit) g = limit;
+            if (v > limit) v = limit;
+            if (v < -limit) v = -limit;
+            h[n] = g / (1.0 + exp(-alpha * g)) * (v + 1.0);
+        }
     }
     for (m = 0; m < d; m++) {
         double acc = 0.0;
         for (n = 0; n < d_ff; n++) acc += h[n] * weight_at(fmt, wd, sd, d, d_ff, m, n);
-        o[m] = acc;
+        o[m] = acc + (bd ? (double)bd[m] : 0.0);
     }
 }
 
@@ -367,10 +385,14 @@ int orc_verify_tokens(const orc_layer *L, const uint16_t *x, int T, int k, const
             int e = idx[(size_t)t * k + j];
             swiglu_expert(L->fmt, d, d_ff, L->gate[e], L->up[e], L->down[e],
                           L->s_gate ? L->s_gate[e] : NULL, L->s_up ? L->s_up[e] : NULL,
-                          L->s_down ? L->s_down[e] : NULL, xt, h, o + (size_t)q * d);
+                          L->s_down ? L->s_down[e] : NULL, L->act, L->alpha, L->limit,
+                          L->b_gate ? (const float *)L->b_gate[e] : NULL,
+                          L->b_up ? (const float *)L->b_up[e] : NULL,
+                          L->b_down ? (const float *)L->b_down[e] : NULL, xt, h, o + (size_t)q * d);
         } else {
             swiglu_expert(L->fmt, d, d_ff, L->sh_gate, L->sh_up, L->sh_down, L->sh_s_gate,
-                          L->sh_s_up, L->sh_s_down, xt, h, o + (size_t)q * d);
+                          L->sh_s_up, L->sh_s_down, L->act, L->alpha, L->limit, NULL, NULL, NULL, xt, h,
+                          o + (size_t)q * d);
         }
         free(xt);
         free(h);

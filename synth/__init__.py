@@ -185,6 +185,12 @@ def router_weight(E: int, d: int, seed: int = 0, device="cpu", tag="router", std
     return (torch.randn(E, d, generator=g, device=device) * std).to(torch.bfloat16)
 
 
+def expert_biases(n_exp: int, N: int, seed: int = 0, tag="b", device="cpu", std: float = 0.5) -> torch.Tensor:
+    """fp32 per-expert biases [n_exp, N] ~ N(0, std)."""
+    g = generator(seed, tag, device)
+    return torch.randn(n_exp, N, generator=g, device=device) * std
+
+
 def weights_fp8_b128(n_exp: int, N: int, K: int, seed: int = 0, tag="w", device="cpu",
                      std: float = 0.02) -> tuple[torch.Tensor, torch.Tensor]:
     """FP8 e4m3fn codes [n_exp, N, K] (uint8) and fp32 block scales [n_exp, N/128, K/128].

@@ -148,3 +148,69 @@ def test_expert_dict_input_equals_stacked_input():
     for n in ("gate", "up", "down", "s_gate", "s_up", "s_down"):
         compact[n] = {e: layer[n][e].clone() for e in used}
     assert np.array_equal(oracle.verify_tokens(compact, x, idx, w), oracle.verify_tokens(layer, x, idx, w))
+
+
+# --------------------------------------------------------------------------- GPT-OSS expert variant
+
+def _ffn_oai(x, Wg, Wu, Wd, bg, bu, bd, alpha, limit):
+    g = np.minimum(x @ Wg.T + bg, limit)
+    v = np.clip(x @ Wu.T + bu, -limit, limit)
+    return (g * sp.expit(alpha * g) * (v + 1.0)) @ Wd.T + bd
+
+
+def _with_biases(layer, sh, seed):
+    out = dict(layer)
+    out["b_gate"] = synth.expert_biases(sh.E, sh.d_ff, seed, "bg")
+    out["b_up"] = synth.expert_biases(sh.E, sh.d_ff, seed, "bu")
+    out["b_down"] = synth.expert_biases(sh.E, sh.d, seed, "bd")
+    out["act"], out["alpha"], out["limit"] = 1, 1.702, 7.0
+    return out
+
+
+def test_oai_single_expert_is_dense_clamped_swiglu():
+    sh = synth.Shape("one", 128, 64, 1, 1, 0, 0, False)
+    layer = synth.layer_weights(sh, seed=31)
+    for n in ("gate", "up", "down"):  # large weights so that both clamps bind on some rows
+        layer[n] = (layer[n].float() * 40).to(torch.bfloat16)
+    layer = _with_biases(layer, sh, 31)
+    x = synth.activations(1, 128, seed=31)
+    y = oracle.verify_tokens(layer, x, np.zeros((1, 1), np.int32), np.ones((1, 1)))
+    Wg, Wu, Wd = (layer[n][0].to(torch.float64).numpy() for n in ("gate", "up", "down"))
+    bg, bu, bd = (layer[n][0].double().numpy() for n in ("b_gate", "b_up", "b_down"))
+    xd = x.to(torch.float64).numpy()[0]
+    g, v = Wg @ xd + bg, Wu @ xd + bu
+    assert (g > 7.0).any() and (v > 7.0).any() and (v < -7.0).any()
+    ref = _ffn_oai(xd, Wg, Wu, Wd, bg, bu, bd, 1.702, 7.0)
+    np.testing.assert_allclose(y[0], ref, rtol=1e-12, atol=1e-12 * np.abs(ref).max())
+
+
+def test_oai_clamp_free_limit_differs_from_swiglu_by_silu_term():
+    # limit = inf, alpha = 1, no biases: g sigma(g) (v + 1) = silu(g) v + silu(g), so the two
+    # activations differ by W_down silu(W_gate x) exactly.
+    sh = synth.Shape("one", 64, 32, 1, 1, 0, 0, False)
+    layer = synth.layer_weights(sh, seed=32)
+    x = synth.activations(1, 64, seed=32)
+    one = (np.zeros((1, 1), np.int32), np.ones((1, 1)))
+    y0 = oracle.verify_tokens(layer, x, *one)
+    y1 = oracle.verify_tokens(dict(layer, act=1, alpha=1.0, limit=float("inf")), x, *one)
+    Wg, Wd = (layer[n][0].to(torch.float64).numpy() for n in ("gate", "down"))
+    g = Wg @ x.to(torch.float64).numpy()[0]
+    np.testing.assert_allclose(y1[0] - y0[0], Wd @ (g * sp.expit(g)), rtol=1e-9, atol=1e-14)
+
+
+def test_oai_mxfp4_layer_matches_dense_numpy():
+    sh = synth.Shape("gpt", 192, 96, 8, 4, 2, 0, False)
+    layer = _with_biases(synth.layer_weights(sh, seed=33), sh, 33)
+    T = 4
+    x = synth.activations(T, sh.d, seed=33)
+    idx, w = oracle.route(synth.logits_scattered(T, sh.E, seed=33).numpy(), sh.k, 0)
+    y = oracle.verify_tokens(layer, x, idx, w)
+    xd = x.to(torch.float64).numpy()
+    ref = np.zeros_like(y)
+    for t in range(T):
+        for j in range(sh.k):
+            e = int(idx[t, j])
+            mats = [_dense(2, layer[n][e], layer["s_" + n][e]) for n in ("gate", "up", "down")]
+            bias = [layer[n][e].double().numpy() for n in ("b_gate", "b_up", "b_down")]
+            ref[t] += w[t, j] * _ffn_oai(xd[t], *mats, *bias, 1.702, 7.0)
+    np.testing.assert_allclose(y, ref, rtol=1e-10, atol=1e-12 * np.abs(ref).max())
