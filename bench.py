@@ -282,6 +282,88 @@ def router_timing(wl, reps=20, replays=10):
             "router_gemm_bytes": 2 * sh.E * sh.d + 2 * T * sh.d, "routing_matches_logits_entry": consistent}
 
 
+def variant_timing(T=64, steps=30, warmup=3, n_pool=8):
+    """The real-model variants: a GPT-OSS-120B-shaped MXFP4 layer (d 2880, d_ff 2880, 128 experts,
+    top-4 softmax) with clustered routing (children keep a parent expert with p = 0.8), plain
+    SwiGLU against the GPT-OSS expert (biases, clamped SwiGLU); and DeepSeek-V3's group-limited
+    routing (8 groups of 32, 4 kept, correction bias, scale 2.5) against plain sigmoid top-8 on
+    the same logits, each captured 20 times in a HIP graph and replayed."""
+    import torch
+    import synth
+    import paper_2607_12696_amd as moe
+    dev = torch.device("cuda:0")
+    sh = synth.SHAPES["gpt"]
+    raw = synth.layer_weights(sh, seed=0, device=dev)
+    plain = moe.pack_layer(raw)
+    del raw
+    oai = dict(plain, act=moe.MOE_ACT_SWIGLU_OAI, alpha=1.702, limit=7.0,
+               b_gate=synth.expert_biases(sh.E, sh.d_ff, 0, "bg", dev), b_up=synth.expert_biases(sh.E, sh.d_ff, 0, "bu", dev),
+               b_down=synth.expert_biases(sh.E, sh.d, 0, "bd", dev))
+    x = synth.activations(T, sh.d, seed=1, device=dev)
+    pool = [synth.routes_to_logits(synth.routes_clustered(T, sh.E, sh.k, 0.8, seed=50 + i), sh.E, seed=i,
+                                   device=dev) for i in range(n_pool)]
+    ws = torch.empty(moe.moe_verify_workspace_size(plain, T, sh.k), dtype=torch.uint8, device=dev)
+    y = torch.empty_like(x)
+    uniq = []
+    for lg in pool:
+        _, r = moe.moe_verify_step(x, lg, plain, sh.k, sh.score, workspace=ws, y=y)
+        uniq.append(int(r.n_unique.item()))
+    U = float(np.median(uniq))
+
+    def steps_us(wd):
+        for i in range(warmup):
+            moe.moe_verify_step(x, pool[i % n_pool], wd, sh.k, sh.score, workspace=ws, y=y)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(steps):
+            moe.moe_verify_step(x, pool[i % n_pool], wd, sh.k, sh.score, workspace=ws, y=y)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / steps
+
+    t_plain, t_oai = steps_us(plain), steps_us(oai)
+    per_expert = sum(synth.expert_bytes(sh.d, sh.d_ff, sh.fmt))  # weights + e8m0 scales, unpadded
+    B = U * per_expert + 4 * T * sh.d + 4 * T * sh.E
+    out = {"gpt_oss_T64_clustered": {"unique_experts_median": U, "plain_swiglu_us": t_plain,
+                                     "gpt_oss_expert_us": t_oai, "GB_s_gpt_oss_expert": B / (t_oai * 1e-6) / 1e9,
+                                     "alg_bytes": B}}
+    del plain, oai, ws
+    torch.cuda.empty_cache()
+
+    E, k = 256, 8
+    lg = synth.logits_scattered(T, E, seed=3, device=dev)
+    bias = synth.router_bias(E, seed=3, device=dev)
+    idx = torch.empty(T, k, dtype=torch.int32, device=dev)
+    tw = torch.empty(T, k, dtype=torch.float32, device=dev)
+
+    def graph_us(fn, reps=20, replays=10):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            fn()
+        torch.cuda.current_stream().wait_stream(s)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(replays):
+            g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / (reps * replays)
+
+    out["ds_routing_T64"] = {
+        "grouped_us": graph_us(lambda: moe.moe_route_topk_grouped(lg, bias, k, 8, 4, 2.5, topk_idx=idx, topk_w=tw)),
+        "plain_sigmoid_us": graph_us(lambda: moe.moe_route_topk(lg, k, moe.MOE_SCORE_SIGMOID, topk_idx=idx,
+                                                                topk_w=tw))}
+    return out
+
+
 def pct(v, q):
     s = sorted(v)
     return s[min(len(s) - 1, max(0, int(round(q * (len(s) - 1)))))]
@@ -617,9 +699,19 @@ def main():
         log("timing the oracle on the host ...")
         cpu, err = cpu_baseline(wl, args.U, args.cpu_tokens)
 
+    variants = None
+    if not args.no_sweep:
+        del wl
+        torch.cuda.empty_cache()
+        variants = variant_timing()
+        log(f"GPT-OSS layer T=64: plain {variants['gpt_oss_T64_clustered']['plain_swiglu_us']:.1f} us, "
+            f"GPT-OSS expert {variants['gpt_oss_T64_clustered']['gpt_oss_expert_us']:.1f} us; "
+            f"grouped routing {variants['ds_routing_T64']['grouped_us']:.1f} us")
+
     stack = None
     if not args.no_stack:
-        del wl
+        if "wl" in locals():
+            del wl
         torch.cuda.empty_cache()
         st = Stack()
         stack = st.measure(max(10, args.steps // 2), 3)
@@ -648,6 +740,7 @@ def main():
         "sweep_T_scattered": sweep_t,
         "stack_8_layers_T16": stack,
         "router": router,
+        "variants": variants,
     }
     print(json.dumps(out))
     return 0

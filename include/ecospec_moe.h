@@ -71,11 +71,27 @@ typedef enum {
     MOE_SEL_COST_DIFF = 3    /* P - lambda * DeltaCost                                      */
 } moe_sel_mode_t;
 
+/* Expert activation.  MOE_ACT_SWIGLU: h = silu(g) * u.  MOE_ACT_SWIGLU_OAI:
+ * the clamped form of the GPT-OSS family (the GPT-OSS-120B rows of the
+ * paper's tables): g = min(g, limit), u = clamp(u, -limit, limit),
+ * h = g * sigmoid(alpha * g) * (u + 1). */
+typedef enum {
+    MOE_ACT_SWIGLU = 0,
+    MOE_ACT_SWIGLU_OAI = 1
+} moe_act_t;
+
 /* Weights of one MoE layer, in the streaming layout written by
  * moe_pack_weights; all pointers are device pointers.  The scale pointers
  * are NULL for MOE_W_BF16.  The sh_* fields describe one always-on shared
  * expert (packed the same way, E = 1) with gate weight 1 that every token
  * uses; all sh_* weight pointers NULL means no shared expert.
+ * act / alpha / limit select the activation (moe_act_t; alpha and limit are
+ * read for MOE_ACT_SWIGLU_OAI only, finite, limit > 0).  b_gate, b_up
+ * [E][d_ff] and b_down [E][d] are optional fp32 biases of the routed experts
+ * (NULL: none; 16-byte aligned): g and u get b_gate, b_up before the
+ * activation and each expert output gets b_down before the gate weight.
+ * The shared expert takes the activation but no biases.  A zero-initialised
+ * struct tail (act 0, NULL biases) is the plain SwiGLU layer.
  * Requirements: d % 32 == 0, d_ff % 32 == 0, and for FP8 d % 128 == 0 and
  * d_ff % 128 == 0; each packed matrix below 2 GiB; 16-byte aligned pointers.
  * Other shapes return MOE_ERR_UNSUPPORTED. */
@@ -86,6 +102,9 @@ typedef struct {
     const void *s_gate, *s_up, *s_down;
     const void *sh_gate, *sh_up, *sh_down;
     const void *sh_s_gate, *sh_s_up, *sh_s_down;
+    int act; /* moe_act_t */
+    float alpha, limit;
+    const float *b_gate, *b_up, *b_down;
 } moe_weights_t;
 
 /* Routing of T tokens as produced by moe_route_topk + moe_expert_union

@@ -33,6 +33,7 @@ MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP
 MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
 MOE_W_BF16, MOE_W_FP8_E4M3_B128, MOE_W_MXFP4 = 0, 1, 2
 MOE_SEL_COST_RATIO, MOE_SEL_CONFIDENCE, MOE_SEL_GLOBAL_COST, MOE_SEL_COST_DIFF = 0, 1, 2, 3
+MOE_ACT_SWIGLU, MOE_ACT_SWIGLU_OAI = 0, 1
 
 EXPORTED = ("moe_route_topk", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
             "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree",
@@ -48,7 +49,9 @@ class MoeError(RuntimeError):
 class moe_weights_t(C.Structure):
     _fields_ = [("fmt", C.c_int), ("d", C.c_int), ("d_ff", C.c_int), ("E", C.c_int)] + [
         (n, C.c_void_p) for n in ("w_gate", "w_up", "w_down", "s_gate", "s_up", "s_down", "sh_gate", "sh_up",
-                                  "sh_down", "sh_s_gate", "sh_s_up", "sh_s_down")]
+                                  "sh_down", "sh_s_gate", "sh_s_up", "sh_s_down")] + [
+        ("act", C.c_int), ("alpha", C.c_float), ("limit", C.c_float),
+        ("b_gate", C.c_void_p), ("b_up", C.c_void_p), ("b_down", C.c_void_p)]
 
 
 class moe_routing_t(C.Structure):
@@ -256,7 +259,8 @@ def moe_pack_weights(fmt: int, w, s=None):
 
 def pack_layer(layer: dict) -> dict:
     """A layer dict (interchange layout, device tensors) with every matrix packed."""
-    out = {k: layer[k] for k in ("fmt", "d", "d_ff") if k in layer}
+    out = {k: layer[k] for k in ("fmt", "d", "d_ff", "act", "alpha", "limit", "b_gate", "b_up", "b_down")
+           if k in layer}
     out["E"] = int(layer.get("E", layer["gate"].shape[0]))
     fmt = int(layer["fmt"])
     for prefix in ("", "sh_"):
@@ -273,8 +277,17 @@ def pack_layer(layer: dict) -> dict:
 # --------------------------------------------------------------------------- verify layer
 
 def weights_struct(w: dict) -> moe_weights_t:
-    """moe_weights_t for a layer dict (keys fmt, d, d_ff, E, gate, up, down, optional s_* and sh_*)."""
+    """moe_weights_t for a layer dict (keys fmt, d, d_ff, E, gate, up, down, optional s_*, sh_*,
+    fp32 biases b_gate / b_up [E, d_ff] and b_down [E, d], and act / alpha / limit)."""
     s = moe_weights_t()
+    torch = _torch()
+    s.act = int(w.get("act", MOE_ACT_SWIGLU))
+    s.alpha, s.limit = float(w.get("alpha", 1.702)), float(w.get("limit", 7.0))
+    for name in ("b_gate", "b_up", "b_down"):
+        b = w.get(name)
+        if b is not None and b.dtype != torch.float32:
+            raise ValueError(f"{name} must be float32")
+        setattr(s, name, _dev_ptr(b, name))
     s.fmt, s.d, s.d_ff = int(w["fmt"]), int(w["d"]), int(w["d_ff"])
     s.E = int(w["E"]) if "E" in w else int(w["gate"].shape[0])
     for name in ("gate", "up", "down"):

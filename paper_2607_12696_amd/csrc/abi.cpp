@@ -51,6 +51,12 @@ moe_status_t check_weights(const moe_weights_t *w)
         for (const void *p : sc)
             if (p && !aligned(p, 4)) return MOE_ERR_INVALID_ARG;
     }
+    if (w->act != MOE_ACT_SWIGLU && w->act != MOE_ACT_SWIGLU_OAI) return MOE_ERR_INVALID_ARG;
+    if (w->act == MOE_ACT_SWIGLU_OAI && (!isfinite(w->alpha) || !isfinite(w->limit) || !(w->limit > 0.f)))
+        return MOE_ERR_INVALID_ARG;
+    const void *bs[] = {w->b_gate, w->b_up, w->b_down};
+    for (const void *p : bs)
+        if (p && !aligned(p, 16)) return MOE_ERR_INVALID_ARG;
     return MOE_OK;
 }
 
@@ -157,6 +163,7 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     if (r->T < 1 || r->k < 1 || r->k > kMaxK || r->k > w->E || r->E != w->E || (long)r->T * r->k > kMaxSlots)
         return MOE_ERR_INVALID_ARG;
     if (!r->topk_w || !r->union_ids || !r->n_unique || !r->offsets || !r->perm) return MOE_ERR_INVALID_ARG;
+    if (w->b_down && !r->topk_idx) return MOE_ERR_INVALID_ARG;  // the down bias follows each slot's expert
     const bool shared = w->sh_gate != nullptr;
     const ecospec::VerifyWorkspace ws = ecospec::verify_workspace(w->d, w->d_ff, r->T, r->k, shared);
     if (ws.plan_cap > ecospec::kMaxGroups) return MOE_ERR_UNSUPPORTED;
@@ -184,6 +191,13 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     a.sh_s_up = w->sh_s_up;
     a.sh_s_down = w->sh_s_down;
     a.topk_w = r->topk_w;
+    a.topk_idx = r->topk_idx;
+    a.act = w->act;
+    a.alpha = w->alpha;
+    a.limit = w->limit;
+    a.b_gate = w->b_gate;
+    a.b_up = w->b_up;
+    a.b_down = w->b_down;
     a.union_ids = r->union_ids;
     a.n_unique = r->n_unique;
     a.offsets = r->offsets;

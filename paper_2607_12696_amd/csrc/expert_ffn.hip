@@ -95,10 +95,13 @@ template <> struct Fmt<FMT_BF16>  { static constexpr int kVecs = 4; };
 template <> struct Fmt<FMT_FP8>   { static constexpr int kVecs = 2; };
 template <> struct Fmt<FMT_MXFP4> { static constexpr int kVecs = 1; };
 
-// One lane's 32 weights of one macro step of one tile (+ their scale).
+// One lane's 32 weights of one macro step of one tile (+ their scale).  The
+// MXFP4 scale stays the raw e8m0 code until the step is decoded: converting it
+// where it is loaded would wait for that load and drain the prefetch.
 template <int FMT> struct WFrag {
     u32x4 v[Fmt<FMT>::kVecs];
-    float scale;  // FP8: the 128x128 block scale; MXFP4: 2^(e8m0 - 127)
+    float scale;    // FP8: the 128x128 block scale
+    uint32_t code;  // MXFP4: e8m0 code of the lane's 32-element group
 };
 
 __device__ __forceinline__ float e8m0_to_f32(uint32_t code)
@@ -127,11 +130,12 @@ __device__ __forceinline__ bf16x8 decode_a(const WFrag<FMT> &f, int s)
         return __builtin_bit_cast(bf16x8, o);
     } else {
         const uint32_t w = f.v[0][s];
+        const float sc = e8m0_to_f32(f.code);
         u32x4 o;
-        o[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, f.scale, 0));
-        o[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, f.scale, 1));
-        o[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, f.scale, 2));
-        o[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, f.scale, 3));
+        o[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 0));
+        o[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 1));
+        o[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 2));
+        o[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 3));
         return __builtin_bit_cast(bf16x8, o);
     }
 }
@@ -294,6 +298,7 @@ struct ItemDesc {
     int n0;                  // first row of the band
     int p0;                  // grouped position of the group's first token
     int M;                   // tokens in the group (<= 64)
+    int e;                   // expert id (-1: the shared expert)
     bool shared;
 };
 
@@ -313,6 +318,7 @@ __device__ __forceinline__ ItemDesc describe(const FfnParams &P, const Plan &pl,
     const size_t sc = fmt == FMT_FP8 ? (size_t)(P.N / 128) * (P.K / 128) * 4 : fmt == FMT_MXFP4 ? (size_t)P.N * kp / 32 : 0;
     ItemDesc d;
     d.shared = u >= pl.U;
+    d.e = d.shared ? -1 : ld_s(a.union_ids + u);
     const int M = expert_tokens(a, u, pl.U);
     d.p0 = (d.shared ? a.T * a.k : ld_s(a.offsets + u)) + tg * kTokGroup;
     d.M = min(kTokGroup, M - tg * kTokGroup);
@@ -346,6 +352,7 @@ __device__ __forceinline__ ItemDesc describe_lds(const FfnParams &P, const Split
     ItemDesc d;
     const int e0 = __builtin_amdgcn_readfirstlane(sp.ge[gi]);
     d.shared = e0 < 0;
+    d.e = e0;
     d.p0 = __builtin_amdgcn_readfirstlane(sp.gp0[gi]);
     d.M = __builtin_amdgcn_readfirstlane(sp.gM[gi]);
     d.n0 = band * P.band_rows;
@@ -375,6 +382,18 @@ __device__ __forceinline__ int tile_row(const ItemDesc &d, int wave, int t)
 
 // ----------------------------------------------------------------------------- epilogue
 
+// h from the gate and up values of one row (biases already added):
+// act 0 silu(g) * u; act 1 (GPT-OSS) with g capped at limit and u clamped to
+// [-limit, limit], g * sigmoid(alpha * g) * (u + 1).  The comparisons keep NaN.
+__device__ __forceinline__ float activate(const VerifyArgs &a, float g, float u)
+{
+    if (a.act == 0) return g / (1.f + expf(-g)) * u;
+    if (g > a.limit) g = a.limit;
+    if (u > a.limit) u = a.limit;
+    if (u < -a.limit) u = -a.limit;
+    return g / (1.f + expf(-a.alpha * g)) * (u + 1.f);
+}
+
 // Finishes a wavefront's (tile 0, tile 1) accumulators of an item: gate/up ->
 // bf16 SwiGLU rows of H, down -> fp32 rows of O, both at grouped positions.  Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for
 // token column col of each 16-token block.
@@ -391,12 +410,25 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
         if (r >= d.M) continue;
         const int p = d.p0 + r;
         if (!DOWN) {
-            const f32x4 g = acc[0][mb], v = acc[1][mb];
+            f32x4 g = acc[0][mb], v = acc[1][mb];
             uint32_t h2[2];
+            if (a.act == 0 && !a.b_gate && !a.b_up) {
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const float g0 = g[2 * i], g1 = g[2 * i + 1];
-                h2[i] = pack_bf16x2(g0 / (1.f + expf(-g0)) * v[2 * i], g1 / (1.f + expf(-g1)) * v[2 * i + 1]);
+                for (int i = 0; i < 2; ++i) {
+                    const float g0 = g[2 * i], g1 = g[2 * i + 1];
+                    h2[i] = pack_bf16x2(g0 / (1.f + expf(-g0)) * v[2 * i], g1 / (1.f + expf(-g1)) * v[2 * i + 1]);
+                }
+            } else {
+                const int row = tile_row<DOWN>(d, wave, 0) + 4 * grp;  // rows row .. row + 3 of this lane
+                if (!d.shared) {
+                    if (a.b_gate) g += *reinterpret_cast<const f32x4 *>(a.b_gate + (size_t)d.e * a.d_ff + row);
+                    if (a.b_up) v += *reinterpret_cast<const f32x4 *>(a.b_up + (size_t)d.e * a.d_ff + row);
+                }
+                float h[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) h[i] = activate(a, g[i], v[i]);
+                h2[0] = pack_bf16x2(h[0], h[1]);
+                h2[1] = pack_bf16x2(h[2], h[3]);
             }
             *reinterpret_cast<u32x2 *>(a.h + (size_t)p * a.d_ff + tile_row<DOWN>(d, wave, 0) + 4 * grp) =
                 u32x2{h2[0], h2[1]};
@@ -572,8 +604,8 @@ __device__ __forceinline__ void record_cuts(const FfnParams &P, const Plan &pl, 
 
 // Gate/up launch, thread 0 of workgroup w: the record its fix-up reads.  If
 // the range starts inside an item that ends within it (w is the item's last
-// contributor), {item, contributors(), first grouped position, tokens} of that
-// item; else item = -1.  Every workgroup writes its record on every launch.
+// contributor), {item, contributors(), first grouped position | (expert + 1)
+// << 32, tokens} of that item; else item = -1.  Every workgroup writes its record on every launch.
 __device__ __forceinline__ void write_fix_record(const FfnParams &P, const Plan &pl, const Split &sp, int w, long x0,
                                                  long x1)
 {
@@ -585,7 +617,7 @@ __device__ __forceinline__ void write_fix_record(const FfnParams &P, const Plan 
             const int gi = (int)(item / P.nbands);
             r[0] = item;
             r[1] = contributors(P, pl, sp, ib, ie);
-            r[2] = sp.gp0[gi];
+            r[2] = (long long)(uint32_t)sp.gp0[gi] | ((long long)(sp.ge[gi] + 1) << 32);
             r[3] = sp.gM[gi];
         }
     }
@@ -665,10 +697,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                 float, __builtin_amdgcn_raw_buffer_load_b32(src.rs1, (int)(ok ? src.q1 + sso : kOff), 0, 0));
         } else if constexpr (FMT == FMT_MXFP4) {
             const uint32_t sso = step * 64u;
-            wf[slot][0].scale =
-                e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(src.rs0, (int)(ok ? src.q0 + sso : kOff), 0, 0));
-            wf[slot][1].scale =
-                e8m0_to_f32(__builtin_amdgcn_raw_buffer_load_b8(src.rs1, (int)(ok ? src.q1 + sso : kOff), 0, 0));
+            wf[slot][0].code = __builtin_amdgcn_raw_buffer_load_b8(src.rs0, (int)(ok ? src.q0 + sso : kOff), 0, 0);
+            wf[slot][1].code = __builtin_amdgcn_raw_buffer_load_b8(src.rs1, (int)(ok ? src.q1 + sso : kOff), 0, 0);
         }
         const bool kok = ok && (int)step * kMacroK + bc * 8 < K;
 #pragma unroll
@@ -778,7 +808,10 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
     if (item < 0) return;
     const long long cut = ld_s64(rec + 1);
     ItemDesc d{};
-    d.p0 = (int)ld_s64(rec + 2);
+    const long long pe = ld_s64(rec + 2);
+    d.p0 = (int)(uint32_t)pe;
+    d.e = (int)(pe >> 32) - 1;
+    d.shared = d.e < 0;
     d.M = (int)ld_s64(rec + 3);
     d.n0 = (int)(item % P.nbands) * P.band_rows;
     const int nmb = (d.M + 15) / 16;  // only the live token blocks were parked
@@ -866,7 +899,7 @@ __device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, l
     return s;
 }
 
-// y[t] = sum_j w[t][j] * O[slot t*k + j] (+ shared) -> bf16, summed in the
+// y[t] = sum_j w[t][j] * (O[slot t*k + j] + b_down[expert of the slot]) (+ shared) -> bf16, summed in the
 // order j = 0..k-1, then the shared expert; 4 columns per thread.  D is the
 // down launch's geometry.  The k slots are handled 8 at a time, each stage's
 // loads issued together.
@@ -884,13 +917,15 @@ __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
         int pj[CH], gj[CH];
         float wj[CH];
         long long cj[CH];
-        f32x4 vj[CH];
+        f32x4 vj[CH], bj[CH];
 #pragma unroll
         for (int q = 0; q < CH; ++q) {
             const int slot = t * a.k + min(j0 + q, a.k - 1);
             pj[q] = a.inv[slot];
             gj[q] = a.gidx[slot];
             wj[q] = a.topk_w[slot];
+            bj[q] = a.b_down ? *reinterpret_cast<const f32x4 *>(a.b_down + (size_t)a.topk_idx[slot] * a.d + c)
+                             : f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
         for (int q = 0; q < CH; ++q) cj[q] = D.cut[(long)(gj[q] >> 6) * D.nbands + band];
@@ -898,7 +933,7 @@ __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
         for (int q = 0; q < CH; ++q) vj[q] = expert_out(D, cj[q], (long)(gj[q] >> 6) * D.nbands + band, pj[q], gj[q] & 63, c);
 #pragma unroll
         for (int q = 0; q < CH; ++q)
-            if (j0 + q < a.k) s += wj[q] * vj[q];
+            if (j0 + q < a.k) s += wj[q] * (a.b_down ? vj[q] + bj[q] : vj[q]);
     }
     if (a.sh_gate) {
         // The shared expert's token groups are the last ceil(T / 64).

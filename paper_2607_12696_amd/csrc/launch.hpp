@@ -33,6 +33,10 @@ struct VerifyArgs {
     const uint8_t *sh_gate, *sh_up, *sh_down;  // shared expert or null
     const void *sh_s_gate, *sh_s_up, *sh_s_down;
     const float *topk_w;
+    const int32_t *topk_idx;
+    int act;             // 0: SwiGLU, 1: GPT-OSS clamped SwiGLU
+    float alpha, limit;
+    const float *b_gate, *b_up, *b_down;  // routed experts' biases or null
     const int32_t *union_ids, *n_unique, *offsets, *perm;
     const uint16_t *x;  // [T][d] bf16
     uint16_t *y;        // [T][d] bf16

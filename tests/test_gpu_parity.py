@@ -320,6 +320,47 @@ def test_verify_small_matches_oracle(name, T):
     assert err <= YTOL
 
 
+def with_oai(layer, sh, seed, bias_std=4.0):
+    # GPT-OSS expert variant: biases large enough that both clamps bind on some rows.
+    out = dict(layer)
+    out["b_gate"] = synth.expert_biases(sh.E, sh.d_ff, seed, "bg", std=bias_std)
+    out["b_up"] = synth.expert_biases(sh.E, sh.d_ff, seed, "bu", std=bias_std)
+    out["b_down"] = synth.expert_biases(sh.E, sh.d, seed, "bd")
+    out["act"], out["alpha"], out["limit"] = moe.MOE_ACT_SWIGLU_OAI, 1.702, 7.0
+    return out
+
+
+@pytest.mark.parametrize("name", ["mxfp4", "bf16_tail", "fp8", "toy"])
+@pytest.mark.parametrize("T", [1, 8, 37, 64, 130])
+def test_verify_oai_variant_matches_oracle(name, T):
+    sh = SMALL[name]
+    note(f"verify GPT-OSS variant shape={name} T={T}")
+    layer = with_oai(small_layer(name), sh, seed=T)
+    x = synth.activations(T, sh.d, seed=T + 2)
+    lg = synth.logits_scattered(T, sh.E, seed=T + 3)
+    y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), to_dev(layer), sh.k, sh.score)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), sh.k, sh.score)
+    y_ref = oracle.verify_tokens(layer, x, idx_o, w_o, threads=8)
+    err = y_err(y.float().cpu().numpy(), y_ref)
+    note(f"  rel err {err:.3e}")
+    assert err <= YTOL
+
+
+def test_verify_biases_only_change_the_biased_terms():
+    # Zero biases with act 0 give the plain layer bit for bit (the bias path adds exact zeros).
+    sh = SMALL["mxfp4"]
+    layer = small_layer("mxfp4")
+    zero = dict(layer, b_gate=torch.zeros(sh.E, sh.d_ff), b_up=torch.zeros(sh.E, sh.d_ff),
+                b_down=torch.zeros(sh.E, sh.d))
+    x = synth.activations(40, sh.d, seed=4).to(DEV)
+    lg = synth.logits_scattered(40, sh.E, seed=4).to(DEV)
+    y0, _ = moe.moe_verify_step(x, lg, to_dev(layer), sh.k, sh.score)
+    y1, _ = moe.moe_verify_step(x, lg, to_dev(zero), sh.k, sh.score)
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1)
+
+
 @pytest.mark.parametrize("name", ["toy", "fp8", "mxfp4"])
 def test_verify_is_deterministic(name):
     sh = SMALL[name]
@@ -398,9 +439,12 @@ def full_layer(name):
 def host_experts(dl, experts):
     """Copy only the listed experts (and the shared one) to the host for the oracle."""
     out = {"fmt": dl["fmt"], "d": dl["d"], "d_ff": dl["d_ff"]}
-    for n in ("gate", "up", "down", "s_gate", "s_up", "s_down"):
+    for n in ("gate", "up", "down", "s_gate", "s_up", "s_down", "b_gate", "b_up", "b_down"):
         if n in dl:
             out[n] = {e: dl[n][e].cpu() for e in experts}
+    for n in ("act", "alpha", "limit"):
+        if n in dl:
+            out[n] = dl[n]
     for n in ("sh_gate", "sh_up", "sh_down", "sh_s_gate", "sh_s_up", "sh_s_down"):
         if n in dl:
             out[n] = dl[n].cpu()
@@ -416,6 +460,26 @@ FULL_CASES = [
     ("gpt", 64, "clustered", None, [0, 50]),
     ("gpt", 8, "scattered", None, [2, 7]),
 ]
+
+
+def test_full_gpt_oss_variant_sampled_rows():
+    sh = synth.SHAPES["gpt"]
+    T, rows = 64, [0, 21, 63]
+    note(f"full GPT-OSS variant T={T} rows={rows}")
+    raw, dl = full_layer("gpt")
+    ext = {n: v.to(DEV) if hasattr(v, "to") else v for n, v in with_oai({}, sh, seed=5).items()}
+    raw2, dl2 = dict(raw, **ext), dict(dl, **ext)
+    x = synth.activations(T, sh.d, seed=41)
+    lg = routed_logits("clustered", T, sh, seed=41)
+    y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), dl2, sh.k, sh.score)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), sh.k, sh.score)
+    used = sorted(set(idx_o[rows].reshape(-1).tolist()))
+    y_ref = oracle.verify_tokens(host_experts(raw2, used), x, idx_o, w_o, tokens=rows, threads=16)
+    err = y_err(y.float().cpu().numpy()[rows], y_ref)
+    note(f"  U={int(r.n_unique.item())} rel err {err:.3e}")
+    assert err <= YTOL
+    assert torch.isfinite(y.float()).all()
 
 
 @pytest.mark.parametrize("name,T,kind,U,rows", FULL_CASES)
