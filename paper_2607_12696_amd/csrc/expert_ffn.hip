@@ -650,7 +650,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     constexpr int NV = Fmt<FMT>::kVecs;
     constexpr uint32_t BLK = 1024u * NV;
     const VerifyArgs &a = P.a;
-    const int w = blockIdx.x;
+    // Workgroups are dispatched round-robin over the 8 XCDs; taking the ranges
+    // XCD-major gives each XCD one contiguous eighth of the units, so the
+    // workgroups sharing an L2 work on neighbouring items (the same experts'
+    // token rows) instead of the same band slice of every expert.
+    const int w = P.workers % 8 == 0 ? (int)(blockIdx.x % 8) * (P.workers / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
     const int tid = threadIdx.x, br = tid >> 4, bc = tid & 15;
