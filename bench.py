@@ -155,8 +155,7 @@ class Workload:
         wd = self.wdicts[i % len(self.wdicts)]
         if events is not None:
             events[0].record()
-        moe.moe_route_topk(lg, sh.k, sh.score, self.idx, self.w)
-        moe.moe_expert_union(self.idx, sh.E, topk_w=self.w, out=self.routing)
+        moe.moe_route_union(lg, sh.k, sh.score, out=self.routing)
         if events is None:
             moe.moe_verify_layer(self.x, wd, self.routing, y=self.y, workspace=self.ws)
         else:
@@ -210,8 +209,7 @@ class TSweep:
 
     def step(self, i):
         wl, sh = self.wl, self.wl.sh
-        wl.moe.moe_route_topk(self.logits[i % len(self.logits)], sh.k, sh.score, self.r.topk_idx, self.r.topk_w)
-        wl.moe.moe_expert_union(self.r.topk_idx, sh.E, topk_w=self.r.topk_w, out=self.r)
+        wl.moe.moe_route_union(self.logits[i % len(self.logits)], sh.k, sh.score, out=self.r)
         wl.moe.moe_verify_layer(self.x, wl.wdicts[i % len(wl.wdicts)], self.r, y=self.y, workspace=self.ws)
 
     def time(self, steps, warmup):
@@ -479,8 +477,7 @@ class Stack:
         moe, sh = self.moe, self.sh
         logits, routs = self.plans[name]
         for l in range(self.L):
-            moe.moe_route_topk(logits[l], sh.k, sh.score, routs[l].topk_idx, routs[l].topk_w)
-            moe.moe_expert_union(routs[l].topk_idx, sh.E, topk_w=routs[l].topk_w, out=routs[l])
+            moe.moe_route_union(logits[l], sh.k, sh.score, out=routs[l])
             moe.moe_verify_layer(self.xs[l], self.layers[l], routs[l], y=self.ys[l], workspace=self.ws)
         return self.ys
 

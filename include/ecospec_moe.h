@@ -5,7 +5,7 @@
  * verifier must do for T draft tokens (EcoSpec, arXiv 2607.12696):
  *   router top-k          -> moe_route_topk (or moe_route_topk_hidden from x,
  *                            moe_route_topk_grouped for group-limited routing)
- *   expert union, Eq. 1   -> moe_expert_union
+ *   expert union, Eq. 1   -> moe_expert_union (moe_route_union: route + union in one call)
  *   grouped SwiGLU experts streaming every activated expert's weights from
  *   HBM once, gate-weighted combine -> moe_verify_layer
  * and, on the host, the cost-aware draft-tree selection of Section 4.2
@@ -119,6 +119,16 @@ typedef struct {
     const int32_t *offsets;  /* [E+1]  */
     const int32_t *perm;     /* [T*k]  */
 } moe_routing_t;
+
+/*
+ * moe_route_topk followed by moe_expert_union in one call (the two kernels,
+ * enqueued back to back).  Same arguments, limits and results as the two
+ * calls: logits [T][E] fp32 in; topk_idx, topk_w [T][k] and counts,
+ * union_ids, n_unique, offsets, perm out.
+ */
+moe_status_t moe_route_union(const float *logits, int T, int E, int k, int score, int32_t *topk_idx, float *topk_w,
+                             int32_t *counts, int32_t *union_ids, int32_t *n_unique, int32_t *offsets, int32_t *perm,
+                             void *stream);
 
 /*
  * Weight packing (done once, when a model is loaded).  Converts E stacked

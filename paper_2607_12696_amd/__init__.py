@@ -15,7 +15,8 @@ the library has not been built, importing the functions that need it raises
     moe_pack_weights(fmt, w, s)                 -> (w_packed, s_packed)   once per model load
     moe_verify_layer(x, weights, routing)       -> y   (weights packed)
     moe_select_tree(parent, P, pred, E, budget) -> (selected, marginal_cost)
-    moe_verify_step(x, logits, weights, k, score) = the three device calls in order
+    moe_route_union(logits, k, score)           -> Routing   (route + union in one call)
+    moe_verify_step(x, logits, weights, k, score) = moe_route_union + moe_verify_layer
 """
 from __future__ import annotations
 
@@ -35,7 +36,7 @@ MOE_W_BF16, MOE_W_FP8_E4M3_B128, MOE_W_MXFP4 = 0, 1, 2
 MOE_SEL_COST_RATIO, MOE_SEL_CONFIDENCE, MOE_SEL_GLOBAL_COST, MOE_SEL_COST_DIFF = 0, 1, 2, 3
 MOE_ACT_SWIGLU, MOE_ACT_SWIGLU_OAI = 0, 1
 
-EXPORTED = ("moe_route_topk", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
+EXPORTED = ("moe_route_topk", "moe_route_union", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
             "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree",
             "moe_status_string", "moe_last_error")
 
@@ -73,6 +74,7 @@ def lib() -> C.CDLL:
             L = C.CDLL(LIB_PATH)
             p, i = C.c_void_p, C.c_int
             L.moe_route_topk.argtypes = [p, i, i, i, i, p, p, p]
+            L.moe_route_union.argtypes = [p, i, i, i, i, p, p, p, p, p, p, p, p]
             L.moe_route_topk_grouped.argtypes = [p, p, i, i, i, i, i, C.c_float, p, p, p]
             L.moe_router_workspace_size.argtypes = [i, i, i, C.POINTER(C.c_size_t)]
             L.moe_route_topk_hidden.argtypes = [p, p, i, i, i, i, i, p, p, p, p, C.c_size_t, p]
@@ -87,7 +89,7 @@ def lib() -> C.CDLL:
             L.moe_status_string.argtypes = [i]
             L.moe_status_string.restype = C.c_char_p
             L.moe_last_error.restype = C.c_char_p
-            for f in ("moe_route_topk", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
+            for f in ("moe_route_topk", "moe_route_union", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
                       "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree"):
                 getattr(L, f).restype = i
             _lib = L
@@ -232,6 +234,25 @@ def moe_expert_union(topk_idx, E: int, topk_w=None, out: Routing | None = None) 
     return out
 
 
+def moe_route_union(logits, k: int, score: int, out: Routing | None = None) -> Routing:
+    """moe_route_topk + moe_expert_union of fp32 logits [T, E] in one call."""
+    torch = _torch()
+    T, E = logits.shape
+    if logits.dtype != torch.float32:
+        raise ValueError("logits must be float32")
+    dev = logits.device
+    if out is None:
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = Routing(T, k, E, torch.empty(T, k, **i32), torch.empty(T, k, dtype=torch.float32, device=dev),
+                      torch.empty(E, **i32), torch.empty(E, **i32), torch.empty(1, **i32), torch.empty(E + 1, **i32),
+                      torch.empty(T * k, **i32))
+    _check("moe_route_union", lib().moe_route_union(
+        _dev_ptr(logits, "logits"), T, E, k, score, _dev_ptr(out.topk_idx, "topk_idx"), _dev_ptr(out.topk_w, "topk_w"),
+        _dev_ptr(out.counts, "counts"), _dev_ptr(out.union_ids, "union_ids"), _dev_ptr(out.n_unique, "n_unique"),
+        _dev_ptr(out.offsets, "offsets"), _dev_ptr(out.perm, "perm"), _stream(logits)))
+    return out
+
+
 # --------------------------------------------------------------------------- weight packing
 
 def moe_packed_size(fmt: int, E: int, N: int, K: int) -> tuple[int, int]:
@@ -340,8 +361,7 @@ def moe_verify_layer_timed(x, weights: dict, routing: Routing, y, workspace, eve
 
 def moe_verify_step(x, logits, weights: dict, k: int, score: int, workspace=None, y=None):
     """Route, union and verify one layer: the whole hot path on the device."""
-    idx, w = moe_route_topk(logits, k, score)
-    r = moe_expert_union(idx, logits.shape[1], topk_w=w)
+    r = moe_route_union(logits, k, score)
     return moe_verify_layer(x, weights, r, y=y, workspace=workspace), r
 
 

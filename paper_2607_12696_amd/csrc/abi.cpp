@@ -141,6 +141,21 @@ moe_status_t moe_expert_union(const int32_t *topk_idx, int T, int k, int E, int3
                                                  (hipStream_t)stream));
 }
 
+moe_status_t moe_route_union(const float *logits, int T, int E, int k, int score, int32_t *topk_idx, float *topk_w,
+                             int32_t *counts, int32_t *union_ids, int32_t *n_unique, int32_t *offsets, int32_t *perm,
+                             void *stream)
+{
+    if (!logits || !topk_idx || !topk_w || !counts || !union_ids || !n_unique || !offsets || !perm)
+        return MOE_ERR_INVALID_ARG;
+    if (T < 1 || E < 1 || E > kMaxE || k < 1 || k > E || k > kMaxK) return MOE_ERR_INVALID_ARG;
+    if ((long)T * E > (1L << 31) - 1 || (long)T * k > kMaxSlots) return MOE_ERR_INVALID_ARG;
+    if (score != MOE_SCORE_SOFTMAX && score != MOE_SCORE_SIGMOID) return MOE_ERR_INVALID_ARG;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t err = ecospec::launch_route_topk(logits, 0, T, E, k, score, topk_idx, topk_w, nullptr, st);
+    if (err != hipSuccess) return from_hip(err);
+    return from_hip(ecospec::launch_expert_union(topk_idx, T, k, E, counts, union_ids, n_unique, offsets, perm, st));
+}
+
 moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, size_t *bytes)
 {
     if (!bytes) return MOE_ERR_INVALID_ARG;

@@ -40,9 +40,11 @@ __device__ __forceinline__ void wave_match(int e, bool ok, int nbits, int &rank,
     top = ok && lane == 63 - __clzll(peers);
 }
 
-__global__ __launch_bounds__(kUnionThreads) void expert_union_kernel(
-    const int32_t *__restrict__ idx, int S, int E, int32_t *__restrict__ counts, int32_t *__restrict__ union_ids,
-    int32_t *__restrict__ n_unique, int32_t *__restrict__ offsets, int32_t *__restrict__ perm)
+// The union, scans and grouping of S routed slots idx[0 .. S) (global or LDS),
+// by the whole 1024-thread workgroup.
+__device__ __forceinline__ void union_block(const int32_t *idx, int S, int E, int32_t *__restrict__ counts,
+                                            int32_t *__restrict__ union_ids, int32_t *__restrict__ n_unique,
+                                            int32_t *__restrict__ offsets, int32_t *__restrict__ perm)
 {
     __shared__ int wcnt[kUnionWaves][kUnionThreads];  // per-wavefront counts of the current pass
     __shared__ int member_id[kUnionThreads];
@@ -115,6 +117,13 @@ __global__ __launch_bounds__(kUnionThreads) void expert_union_kernel(
         if (ok) perm[wcnt[wave][e] + rank] = s;
         __syncthreads();
     }
+}
+
+__global__ __launch_bounds__(kUnionThreads) void expert_union_kernel(
+    const int32_t *__restrict__ idx, int S, int E, int32_t *__restrict__ counts, int32_t *__restrict__ union_ids,
+    int32_t *__restrict__ n_unique, int32_t *__restrict__ offsets, int32_t *__restrict__ perm)
+{
+    union_block(idx, S, E, counts, union_ids, n_unique, offsets, perm);
 }
 
 hipError_t launch_expert_union(const int32_t *idx, int T, int k, int E, int32_t *counts, int32_t *union_ids,

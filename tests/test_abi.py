@@ -98,6 +98,15 @@ def test_expert_union_rejects(T, k, E):
     assert L.moe_expert_union(FAKE, T, k, E, FAKE, FAKE, FAKE, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("T,E,k,score,null", [
+    (0, 16, 2, 0, False), (4, 0, 1, 0, False), (4, 16, 0, 0, False), (4, 16, 17, 0, False),
+    (4, 1025, 8, 0, False), (4, 128, 65, 0, False), (4, 16, 2, 2, False), (4, 16, 2, 0, True)])
+def test_route_union_rejects(T, E, k, score, null):
+    L = moe.lib()
+    p = 0 if null else FAKE
+    assert L.moe_route_union(FAKE, T, E, k, score, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, p, None) == moe.MOE_ERR_INVALID_ARG
+
+
 def test_expert_union_rejects_null_output():
     L = moe.lib()
     assert L.moe_expert_union(FAKE, 4, 2, 16, FAKE, 0, FAKE, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG

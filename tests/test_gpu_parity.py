@@ -74,6 +74,26 @@ def test_route_and_union_bit_exact(E, k, score, kind, T):
         assert np.array_equal(getattr(r, name).cpu().numpy(), u[name]), name
 
 
+@pytest.mark.parametrize("E,k,score", ROUTE_CASES)
+@pytest.mark.parametrize("kind", ["scattered", "ties"])
+@pytest.mark.parametrize("T", [1, 37, 64, 130, 600])
+def test_route_union_call_matches_oracle(E, k, score, kind, T):
+    note(f"route_union E={E} k={k} score={score} kind={kind} T={T}")
+    lg = synth.logits_scattered(T, E, seed=T + 5) if kind == "scattered" else synth.logits_tie_grid(T, E, seed=T + 5)
+    r = moe.moe_route_union(lg.to(DEV), k, score)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), k, score)
+    assert np.array_equal(r.topk_idx.cpu().numpy(), idx_o)
+    assert np.abs(r.topk_w.cpu().numpy().astype(np.float64) - w_o).max() <= WTOL
+    u = oracle.union(idx_o, E)
+    assert int(r.n_unique.item()) == u["n_unique"]
+    for name in ("counts", "union_ids", "offsets", "perm"):
+        assert np.array_equal(getattr(r, name).cpu().numpy(), u[name]), name
+    # identical to the two separate calls, weights included
+    idx2, w2 = moe.moe_route_topk(lg.to(DEV), k, score)
+    assert torch.equal(idx2, r.topk_idx) and torch.equal(w2, r.topk_w)
+
+
 def test_route_nan_and_signed_zero_order():
     lg = torch.tensor([[float("nan"), -float("inf"), 1.0, float("nan"), -3.0, 0.0, -0.0, 2.0]], dtype=torch.float32)
     lg[0, 6] = -0.0
