@@ -143,8 +143,9 @@ moe_status_t moe_route_union(const float *logits, int T, int E, int k, int score
  *   the weights of row rb*16 + c from element kb*128 + 32*g + i*32*1024/B on,
  *   i.e. exactly the matrix-core operand fragment of lane l.
  *   FP8 scales keep their [N/128][K/128] layout (copied).  MXFP4 scales
- *   become [N/16][Kp/128][64] bytes, byte l of a block = the code of row
- *   rb*16 + c, 32-element chunk kb*4 + g (127 in the padding).
+ *   become [N/16][ceil(Kp/512)][64][4] bytes: in quad q of row tile rb,
+ *   the 4 bytes of lane l = c + 16*g are the codes of row rb*16 + c for the
+ *   32-element chunks (4q + j)*4 + g, j = 0..3 (127 in the padding).
  * w, s: device pointers in the interchange layout; w_packed, s_packed:
  * device buffers of the sizes moe_packed_size returns (s may be NULL for
  * bf16).  Requirements: N % 16 == 0, K % 32 == 0 (FP8: N, K % 128 == 0).

@@ -75,8 +75,6 @@ constexpr int kThreads = kWG * kWave;
 constexpr int kBRowsPerPass = kThreads / 16;         // activation rows staged per pass (16 threads per row)
 constexpr int kBPass = kTokGroup / kBRowsPerPass;    // passes per step
 constexpr int kAuxNT = 2;               // nontemporal: streamed weights should not displace activations
-constexpr int kBRow = 256 + 16;         // LDS bytes per activation row of a step (256 + pad against bank conflicts)
-constexpr int kBBuf = kMB * 16 * kBRow; // LDS bytes of one step's activation tile
 constexpr int kPartialFloats = kWG * 2 * kMB * 4 * kWave;  // one workgroup's accumulators
 
 // Wave-uniform loads through the constant address space (scalar memory).
@@ -90,28 +88,46 @@ __device__ __forceinline__ long long ld_s64(const long long *p)
     return *reinterpret_cast<const __attribute__((address_space(4))) long long *>(reinterpret_cast<uintptr_t>(p));
 }
 
+// kVecs: 16-byte vectors per lane in one 16 x 128 block of a tile; kBlocks:
+// 128-wide K blocks per macro step.  MXFP4 takes two blocks a step, so that a
+// step streams 2 KiB per tile like FP8 and pays its fixed per-step work (the
+// activation staging, the barrier, the item bookkeeping) over as many bytes.
 template <int FMT> struct Fmt;
-template <> struct Fmt<FMT_BF16>  { static constexpr int kVecs = 4; };
-template <> struct Fmt<FMT_FP8>   { static constexpr int kVecs = 2; };
-template <> struct Fmt<FMT_MXFP4> { static constexpr int kVecs = 1; };
+template <> struct Fmt<FMT_BF16>  { static constexpr int kVecs = 4, kBlocks = 1; };
+template <> struct Fmt<FMT_FP8>   { static constexpr int kVecs = 2, kBlocks = 1; };
+template <> struct Fmt<FMT_MXFP4> { static constexpr int kVecs = 1, kBlocks = 2; };
 
-// One lane's 32 weights of one macro step of one tile (+ their scale).  The
-// MXFP4 scale stays the raw e8m0 code until the step is decoded: converting it
+// LDS geometry of one step's activation tile (64 tokens x 128 * SB elements,
+// rows padded by 16 bytes against bank conflicts).
+template <int SB> struct BTile {
+    static constexpr int kRow = 256 * SB + 16;  // LDS bytes per activation row
+    static constexpr int kBuf = kMB * 16 * kRow;
+};
+
+// One lane's weights of one macro step of one tile (+ their scales).  The
+// MXFP4 scales stay raw e8m0 codes until the step is decoded: converting one
 // where it is loaded would wait for that load and drain the prefetch.
 template <int FMT> struct WFrag {
-    u32x4 v[Fmt<FMT>::kVecs];
-    float scale;    // FP8: the 128x128 block scale
-    uint32_t code;  // MXFP4: e8m0 code of the lane's 32-element group
+    u32x4 v[Fmt<FMT>::kVecs * Fmt<FMT>::kBlocks];  // block b's vectors at [b * kVecs ...]
+    float scale;                                   // FP8: the 128x128 block scale
+    uint32_t code;                                 // MXFP4: the lane's e8m0 codes of a quad of blocks
+    int shift;                                     // MXFP4: bit offset of the step's first block in `code`
 };
 
 __device__ __forceinline__ float e8m0_to_f32(uint32_t code)
 {
-    // 2^(code-127); code 0 is the subnormal 2^-127, code 255 is NaN.
-    return code == 0u ? __uint_as_float(0x00400000u) : code == 255u ? __uint_as_float(0x7fc00000u)
-                                                                      : __uint_as_float(code << 23);
+    // 2^(code-127); code 0 is the subnormal 2^-127, code 255 is NaN.  Written
+    // as two selects on the bits: as nested conditional expressions the
+    // compiler branched around them, splitting the contraction into many
+    // small blocks at every sub-step.
+    uint32_t b = code << 23;
+    b = code == 0u ? 0x00400000u : b;
+    b = code == 255u ? 0x7fc00000u : b;
+    return __uint_as_float(b);
 }
 
-// bf16 A operand of sub-step s (the lane's weights 8s .. 8s+7 of the step).
+// bf16 A operand of sub-step s (the lane's weights 8s .. 8s+7 of a block;
+// MXFP4: sub-step s of block s / 4).
 // Exact: FP8 codes as they are (the converter's scale operand only takes a
 // power of two, so the 128x128 block scale multiplies the fp32 partial sum of
 // the step instead); MXFP4 codes times their 2^e8m0 group scale.
@@ -129,8 +145,8 @@ __device__ __forceinline__ bf16x8 decode_a(const WFrag<FMT> &f, int s)
         o[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w1, 1.0f, true));
         return __builtin_bit_cast(bf16x8, o);
     } else {
-        const uint32_t w = f.v[0][s];
-        const float sc = e8m0_to_f32(f.code);
+        const uint32_t w = f.v[s >> 2][s & 3];
+        const float sc = e8m0_to_f32((f.code >> (f.shift + 8 * (s >> 2))) & 0xffu);
         u32x4 o;
         o[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 0));
         o[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 1));
@@ -145,7 +161,8 @@ __device__ __forceinline__ bf16x8 decode_a(const WFrag<FMT> &f, int s)
 struct FfnParams {
     VerifyArgs a;
     int N, K;             // rows and reduction length of one streamed matrix
-    int nsteps;           // macro steps per item: ceil(K / 128)
+    int nblocks;          // 128-wide K blocks of a matrix row tile: ceil(K / 128)
+    int nsteps;           // macro steps per item: ceil(nblocks / kBlocks of the format)
     int band_rows;        // rows per item: 16 * kWG (gate/up) or 32 * kWG (down)
     int nbands;           // bands per expert: ceil(N / band_rows)
     int workers;          // workgroups of the main kernel's grid
@@ -313,9 +330,10 @@ __device__ __forceinline__ ItemDesc describe(const FfnParams &P, const Plan &pl,
         tg = ld_s(P.plan + 8 + 2 * gi + 1);
     }
     const int fmt = a.fmt;
-    const size_t kp = (size_t)P.nsteps * kMacroK;
+    const size_t kp = (size_t)P.nblocks * kMacroK;
     const size_t mat = (size_t)P.N * kp * (fmt == FMT_BF16 ? 2 : 1) / (fmt == FMT_MXFP4 ? 2 : 1);
-    const size_t sc = fmt == FMT_FP8 ? (size_t)(P.N / 128) * (P.K / 128) * 4 : fmt == FMT_MXFP4 ? (size_t)P.N * kp / 32 : 0;
+    const size_t sc = fmt == FMT_FP8 ? (size_t)(P.N / 128) * (P.K / 128) * 4
+                      : fmt == FMT_MXFP4 ? (size_t)P.N * ((P.nblocks + 3) / 4) * 16 : 0;
     ItemDesc d;
     d.shared = u >= pl.U;
     d.e = d.shared ? -1 : ld_s(a.union_ids + u);
@@ -346,9 +364,10 @@ __device__ __forceinline__ ItemDesc describe_lds(const FfnParams &P, const Split
     const VerifyArgs &a = P.a;
     const int gi = item / P.nbands, band = item - gi * P.nbands;
     const int fmt = a.fmt;
-    const size_t kp = (size_t)P.nsteps * kMacroK;
+    const size_t kp = (size_t)P.nblocks * kMacroK;
     const size_t mat = (size_t)P.N * kp * (fmt == FMT_BF16 ? 2 : 1) / (fmt == FMT_MXFP4 ? 2 : 1);
-    const size_t sc = fmt == FMT_FP8 ? (size_t)(P.N / 128) * (P.K / 128) * 4 : fmt == FMT_MXFP4 ? (size_t)P.N * kp / 32 : 0;
+    const size_t sc = fmt == FMT_FP8 ? (size_t)(P.N / 128) * (P.K / 128) * 4
+                      : fmt == FMT_MXFP4 ? (size_t)P.N * ((P.nblocks + 3) / 4) * 16 : 0;
     ItemDesc d;
     const int e0 = __builtin_amdgcn_readfirstlane(sp.ge[gi]);
     d.shared = e0 < 0;
@@ -467,16 +486,17 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
     src.ib = (long)item * nsteps;
     src.ie = src.ib + nsteps;
 
+    const int nblocks = P.nblocks;
     const uint32_t mat_bytes =
-        (uint32_t)((size_t)P.N * nsteps * kMacroK * (FMT == FMT_BF16 ? 2 : 1) / (FMT == FMT_MXFP4 ? 2 : 1));
+        (uint32_t)((size_t)P.N * nblocks * kMacroK * (FMT == FMT_BF16 ? 2 : 1) / (FMT == FMT_MXFP4 ? 2 : 1));
     src.ra0 = make_rsrc(d.wa, mat_bytes);
     src.ra1 = make_rsrc(d.wb, mat_bytes);
     const int row0 = tile_row<DOWN>(d, wave, 0), row1 = tile_row<DOWN>(d, wave, 1);
     const bool arow_ok = row0 < P.N;
-    src.a0 = arow_ok ? (uint32_t)(row0 / 16) * nsteps * BLK + lane * 16u : kOff;
-    src.a1 = arow_ok ? (uint32_t)(row1 / 16) * nsteps * BLK + lane * 16u : kOff;
+    src.a0 = arow_ok ? (uint32_t)(row0 / 16) * nblocks * BLK + lane * 16u : kOff;
+    src.a1 = arow_ok ? (uint32_t)(row1 / 16) * nblocks * BLK + lane * 16u : kOff;
     const uint32_t sc_bytes = FMT == FMT_FP8 ? (uint32_t)((P.N / 128) * (K / 128) * 4)
-                                             : (uint32_t)((size_t)P.N * nsteps * 4);
+                                             : (uint32_t)((size_t)P.N * ((nblocks + 3) / 4) * 16);
     src.rs0 = make_rsrc(FMT == FMT_BF16 ? d.wa : d.sa, FMT == FMT_BF16 ? 0u : sc_bytes);
     src.rs1 = make_rsrc(FMT == FMT_BF16 ? d.wb : d.sb, FMT == FMT_BF16 ? 0u : sc_bytes);
     src.q0 = src.q1 = 0;
@@ -484,8 +504,8 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
         src.q0 = arow_ok ? (uint32_t)(row0 / 128) * (K / 128) * 4u : kOff;
         src.q1 = arow_ok ? (uint32_t)(row1 / 128) * (K / 128) * 4u : kOff;
     } else if constexpr (FMT == FMT_MXFP4) {
-        src.q0 = arow_ok ? (uint32_t)(row0 / 16) * nsteps * 64u + lane : kOff;
-        src.q1 = arow_ok ? (uint32_t)(row1 / 16) * nsteps * 64u + lane : kOff;
+        src.q0 = arow_ok ? (uint32_t)(row0 / 16) * ((nblocks + 3) / 4) * 256u + lane * 4u : kOff;
+        src.q1 = arow_ok ? (uint32_t)(row1 / 16) * ((nblocks + 3) / 4) * 256u + lane * 4u : kOff;
     }
 
     // Activation rows: in pass i this wavefront stages rows i*kBRowsPerPass +
@@ -520,12 +540,15 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
 template <int FMT, int NMB>
 __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_t *buf, f32x4 (&acc)[2][kMB])
 {
+    constexpr int SB = Fmt<FMT>::kBlocks, ROW = BTile<SB>::kRow, NS = 4 * SB;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
-    const uint8_t *bp = buf + col * kBRow + grp * 64;
+    const uint8_t *bp = buf + col * ROW + grp * 64;
+    // Sub-step s reads block s / 4 of the row (256 bytes each), 16 bytes per sub-step within it.
+    auto boff = [](int s) { return (s >> 2) * 256 + (s & 3) * 16; };
     bf16x8 b[2][NMB];
 #pragma unroll
     for (int mb = 0; mb < NMB; ++mb)
-        b[0][mb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kBRow));
+        b[0][mb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * ROW));
     // FP8 accumulates the step in `part` and adds scale * part at the end.
     f32x4 part[2][NMB];
 #pragma unroll
@@ -533,12 +556,12 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
 #pragma unroll
         for (int mb = 0; mb < NMB; ++mb) part[t][mb] = FMT == FMT_FP8 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[t][mb];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        if (s < 3) {
+    for (int s = 0; s < NS; ++s) {
+        if (s < NS - 1) {
 #pragma unroll
             for (int mb = 0; mb < NMB; ++mb)
                 b[(s + 1) & 1][mb] =
-                    __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kBRow + (s + 1) * 16));
+                    __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * ROW + boff(s + 1)));
         }
         const bf16x8 av0 = decode_a<FMT>(wv[0], s), av1 = decode_a<FMT>(wv[1], s);
 #pragma unroll
@@ -646,9 +669,10 @@ __device__ __forceinline__ int partial_offset(int wave, int t, int mb, int lane)
 template <int FMT, bool DOWN, int PD>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void expert_ffn_kernel(FfnParams P)
 {
-    __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kBBuf];
-    constexpr int NV = Fmt<FMT>::kVecs;
-    constexpr uint32_t BLK = 1024u * NV;
+    constexpr int NV = Fmt<FMT>::kVecs, SB = Fmt<FMT>::kBlocks;
+    constexpr int BROW = BTile<SB>::kRow, BBUF = BTile<SB>::kBuf;
+    constexpr uint32_t BLK = 1024u * NV;  // bytes of one 16 x 128 block of a tile
+    __shared__ __attribute__((aligned(16))) uint8_t lds[2 * BBUF];
     const VerifyArgs &a = P.a;
     // Workgroups are dispatched round-robin over the 8 XCDs; taking the ranges
     // XCD-major gives each XCD one contiguous eighth of the units, so the
@@ -679,7 +703,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     set_source<FMT, DOWN>(src, P, sp, (int)(x0 / nsteps));
 
     WFrag<FMT> wf[PD][2];
-    u32x4 bst[PD][kBPass];
+    u32x4 bst[PD][kBPass][SB];
     // Loads of unit v into ring slot `slot`; a unit past the range loads zeros
     // (offsets beyond every buffer), so every path issues the same loads and
     // the compiler's wait counts stay exact.
@@ -687,27 +711,37 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         if (v >= src.ie && v < x1) set_source<FMT, DOWN>(src, P, sp, src.item + 1);
         const bool ok = v < x1;
         const uint32_t step = (uint32_t)(v - src.ib);
-        const uint32_t so = step * BLK;
 #pragma unroll
-        for (int i = 0; i < NV; ++i) {
-            wf[slot][0].v[i] = load16<kAuxNT>(src.ra0, ok ? src.a0 + so + 1024u * i : kOff);
-            wf[slot][1].v[i] = load16<kAuxNT>(src.ra1, ok ? src.a1 + so + 1024u * i : kOff);
-        }
-        if constexpr (FMT == FMT_FP8) {
-            const uint32_t sso = step * 4u;
-            wf[slot][0].scale = __builtin_bit_cast(
-                float, __builtin_amdgcn_raw_buffer_load_b32(src.rs0, (int)(ok ? src.q0 + sso : kOff), 0, 0));
-            wf[slot][1].scale = __builtin_bit_cast(
-                float, __builtin_amdgcn_raw_buffer_load_b32(src.rs1, (int)(ok ? src.q1 + sso : kOff), 0, 0));
-        } else if constexpr (FMT == FMT_MXFP4) {
-            const uint32_t sso = step * 64u;
-            wf[slot][0].code = __builtin_amdgcn_raw_buffer_load_b8(src.rs0, (int)(ok ? src.q0 + sso : kOff), 0, 0);
-            wf[slot][1].code = __builtin_amdgcn_raw_buffer_load_b8(src.rs1, (int)(ok ? src.q1 + sso : kOff), 0, 0);
-        }
-        const bool kok = ok && (int)step * kMacroK + bc * 8 < K;
+        for (int b = 0; b < SB; ++b) {
+            // Block kb of the tile; a step's second block can lie past the last one.
+            const uint32_t kb = step * SB + b;
+            const bool okb = ok && (SB == 1 || (int)kb < P.nblocks);
+            const uint32_t so = kb * BLK;
 #pragma unroll
-        for (int i = 0; i < kBPass; ++i)
-            bst[slot][i] = load16<0>(rb, (kok && src.boff[i] != kOff) ? src.boff[i] + step * 256u : kOff);
+            for (int i = 0; i < NV; ++i) {
+                wf[slot][0].v[b * NV + i] = load16<kAuxNT>(src.ra0, okb ? src.a0 + so + 1024u * i : kOff);
+                wf[slot][1].v[b * NV + i] = load16<kAuxNT>(src.ra1, okb ? src.a1 + so + 1024u * i : kOff);
+            }
+            if constexpr (FMT == FMT_FP8) {
+                const uint32_t sso = kb * 4u;
+                wf[slot][0].scale = __builtin_bit_cast(
+                    float, __builtin_amdgcn_raw_buffer_load_b32(src.rs0, (int)(okb ? src.q0 + sso : kOff), 0, 0));
+                wf[slot][1].scale = __builtin_bit_cast(
+                    float, __builtin_amdgcn_raw_buffer_load_b32(src.rs1, (int)(okb ? src.q1 + sso : kOff), 0, 0));
+            } else if constexpr (FMT == FMT_MXFP4) {
+                // The quad holding the step's blocks (kb0 = step * SB is even, so both lie in it).
+                if (b == 0) {
+                    const uint32_t sso = (kb >> 2) * 256u;
+                    wf[slot][0].code = __builtin_amdgcn_raw_buffer_load_b32(src.rs0, (int)(okb ? src.q0 + sso : kOff), 0, 0);
+                    wf[slot][1].code = __builtin_amdgcn_raw_buffer_load_b32(src.rs1, (int)(okb ? src.q1 + sso : kOff), 0, 0);
+                    wf[slot][0].shift = wf[slot][1].shift = (int)(kb & 3u) * 8;
+                }
+            }
+            const bool kok = ok && (int)kb * kMacroK + bc * 8 < K;
+#pragma unroll
+            for (int i = 0; i < kBPass; ++i)
+                bst[slot][i][b] = load16<0>(rb, (kok && src.boff[i] != kOff) ? src.boff[i] + kb * 256u : kOff);
+        }
     };
 
     // The item being contracted.
@@ -724,11 +758,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         issue((slot + PD - 1) % PD, u + PD - 1);
         if (u >= x1) return;  // the last round of the unrolled loop runs past the range
         const int nmb = (cd.M + 15) / 16;
-        uint8_t *buf = lds + par * kBBuf;
+        uint8_t *buf = lds + par * BBUF;
         // After the previous step's barrier no wavefront still reads this buffer.
 #pragma unroll
         for (int i = 0; i < kBPass; ++i)
-            *reinterpret_cast<u32x4 *>(buf + (i * kBRowsPerPass + br) * kBRow + bc * 16) = bst[slot][i];
+#pragma unroll
+            for (int b = 0; b < SB; ++b)
+                *reinterpret_cast<u32x4 *>(buf + (i * kBRowsPerPass + br) * BROW + b * 256 + bc * 16) = bst[slot][i][b];
         __syncthreads();
         switch (nmb) {
         case 1: contract<FMT, 1>(wf[slot], buf, acc); break;
@@ -1033,7 +1069,9 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     g.a = a;
     g.N = a.d_ff;
     g.K = a.d;
-    g.nsteps = (a.d + kMacroK - 1) / kMacroK;
+    constexpr int SB = Fmt<FMT>::kBlocks;
+    g.nblocks = (a.d + kMacroK - 1) / kMacroK;
+    g.nsteps = (g.nblocks + SB - 1) / SB;
     g.band_rows = 16 * kWG;
     g.nbands = (a.d_ff + g.band_rows - 1) / g.band_rows;
     g.workers = G;
@@ -1052,7 +1090,8 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     FfnParams dn = g;
     dn.N = a.d;
     dn.K = a.d_ff;
-    dn.nsteps = (a.d_ff + kMacroK - 1) / kMacroK;
+    dn.nblocks = (a.d_ff + kMacroK - 1) / kMacroK;
+    dn.nsteps = (dn.nblocks + SB - 1) / SB;
     dn.band_rows = 32 * kWG;
     dn.nbands = (a.d + dn.band_rows - 1) / dn.band_rows;
     if ((err = mark(events, 2, stream)) != hipSuccess) return err;

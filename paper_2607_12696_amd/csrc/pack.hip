@@ -11,9 +11,12 @@
 // with one 16-byte load gets exactly the A-operand fragment of the matrix-core
 // instruction, and a wavefront reads each vector as 1 KiB of contiguous memory.
 //
-// MXFP4 scales move to the same blocking: 64 bytes per block, byte l = the
-// e8m0 code of row rb*16 + c, 32-element chunk kb*4 + g (127, i.e. 1.0, in
-// the padding).  FP8 block scales keep their [N/128][K/128] layout.
+// MXFP4 scales move to the same blocking, four blocks to a 256-byte quad: in
+// quad q of row tile rb, the 4 bytes at offset 4*l (l = c + 16*g) are the
+// e8m0 codes of row rb*16 + c for the 32-element chunks (4q + j)*4 + g,
+// j = 0..3 (127, i.e. 1.0, in the padding), so one dword load per lane
+// brings a lane's codes for four blocks.  FP8 block scales keep their
+// [N/128][K/128] layout.
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -48,20 +51,21 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const uint8_t *__rest
     }
 }
 
-// MXFP4 scales: [E][N][K/32] -> [E][N/16][Kp/128][64].
+// MXFP4 scales: [E][N][K/32] -> [E][N/16][ceil(Kp/512)][64][4], one byte per thread.
 __global__ __launch_bounds__(256) void pack_mx_scales_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict__ dst,
                                                              int E, int N, int K)
 {
-    const int nkb = (K + 127) / 128;
-    const size_t total = (size_t)E * (N / 16) * nkb * 64;
+    const int nq = ((K + 127) / 128 + 3) / 4;
+    const size_t per_e = (size_t)(N / 16) * nq * 256;
+    const size_t total = (size_t)E * per_e;
     for (size_t q = blockIdx.x * (size_t)blockDim.x + threadIdx.x; q < total; q += (size_t)gridDim.x * blockDim.x) {
-        const size_t e = q / ((size_t)(N / 16) * nkb * 64);
-        size_t r = q - e * ((size_t)(N / 16) * nkb * 64);
-        const int rb = (int)(r / ((size_t)nkb * 64));
-        r -= (size_t)rb * nkb * 64;
-        const int kb = (int)(r / 64), l = (int)(r % 64);
+        const size_t e = q / per_e;
+        size_t r = q - e * per_e;
+        const int rb = (int)(r / ((size_t)nq * 256));
+        r -= (size_t)rb * nq * 256;
+        const int qd = (int)(r / 256), l = (int)(r % 256) / 4, j = (int)(r % 4);
         const int c = l & 15, g = l >> 4;
-        const int chunk = kb * 4 + g;
+        const int chunk = (qd * 4 + j) * 4 + g;
         dst[q] = chunk < K / 32 ? src[e * (size_t)N * (K / 32) + (size_t)(rb * 16 + c) * (K / 32) + chunk] : 127;
     }
 }
@@ -75,7 +79,7 @@ size_t packed_matrix_bytes(int fmt, int N, int K)
 size_t packed_scale_bytes(int fmt, int N, int K)
 {
     if (fmt == 1) return (size_t)(N / 128) * (K / 128) * 4;
-    if (fmt == 2) return (size_t)N * ((K + 127) / 128) * 4;
+    if (fmt == 2) return (size_t)N * (((K + 127) / 128 + 3) / 4) * 16;
     return 0;
 }
 
@@ -92,7 +96,7 @@ hipError_t launch_pack(int fmt, int E, int N, int K, const void *w, const void *
     if (fmt == 1)
         return hipMemcpyAsync(sp, s, (size_t)E * packed_scale_bytes(1, N, K), hipMemcpyDeviceToDevice, stream);
     if (fmt == 2) {
-        const size_t total = (size_t)E * (N / 16) * ((K + 127) / 128) * 64;
+        const size_t total = (size_t)E * packed_scale_bytes(2, N, K);
         const int g2 = (int)((total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536);
         hipLaunchKernelGGL(pack_mx_scales_kernel, dim3(g2), dim3(256), 0, stream, static_cast<const uint8_t *>(s),
                            static_cast<uint8_t *>(sp), E, N, K);

@@ -214,7 +214,8 @@ def test_pack_validation(fmt, E, N, K, status):
 def test_packed_sizes():
     assert moe.moe_packed_size(1, 2, 2048, 7168) == (2 * 2048 * 7168, 2 * 16 * 56 * 4)
     assert moe.moe_packed_size(0, 1, 32, 96) == (32 * 128 * 2, 0)
-    assert moe.moe_packed_size(2, 1, 2880, 2880) == (2880 * 2944 // 2, 2880 * 23 * 4)
+    # MXFP4 scales: 23 blocks of 128 -> 6 quads of 4 blocks, 16 bytes per row and quad
+    assert moe.moe_packed_size(2, 1, 2880, 2880) == (2880 * 2944 // 2, 2880 * 6 * 16)
 
 
 def test_binding_refuses_host_tensors():

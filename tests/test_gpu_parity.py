@@ -274,19 +274,21 @@ def _expected_packed(fmt, w, s):
     sp = None
     if fmt == 2:
         s = s.numpy()
-        sp = np.full((E, N // 16, nkb, 64), 127, np.uint8)
+        nq = (nkb + 3) // 4
+        sp = np.full((E, N // 16, nq, 64, 4), 127, np.uint8)
         for c in range(16):
             for g in range(4):
                 for kb in range(nkb):
                     ch = kb * 4 + g
                     if ch < K // 32:
-                        sp[:, :, kb, c + 16 * g] = s[:, c::16, ch]
+                        sp[:, :, kb // 4, c + 16 * g, kb % 4] = s[:, c::16, ch]
     elif fmt == 1:
         sp = s.numpy().view(np.uint8)
     return out.reshape(-1), None if sp is None else sp.reshape(-1)
 
 
-@pytest.mark.parametrize("fmt,N,K", [(0, 32, 96), (0, 48, 256), (1, 128, 384), (2, 32, 160), (2, 64, 128)])
+@pytest.mark.parametrize("fmt,N,K", [(0, 32, 96), (0, 48, 256), (1, 128, 384), (2, 32, 160), (2, 64, 128),
+                                     (2, 48, 640), (2, 32, 2880)])
 def test_pack_layout(fmt, N, K):
     note(f"pack fmt={fmt} N={N} K={K}")
     E = 3
