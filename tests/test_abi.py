@@ -201,6 +201,42 @@ def test_verify_layer_rejects_before_launch():
     assert L.moe_verify_layer(*args()) == moe.MOE_ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("field,value", [
+    ("act", 2), ("act", -1),
+    ("alpha", float("nan")), ("limit", float("inf")), ("limit", 0.0), ("limit", -1.0)])
+def test_activation_fields_validated(field, value):
+    w = _weights()
+    w.act, w.alpha, w.limit = moe.MOE_ACT_SWIGLU_OAI, 1.702, 7.0
+    assert _ws(w, 8, 2)[0] == moe.MOE_OK
+    setattr(w, field, value)
+    assert _ws(w, 8, 2)[0] == moe.MOE_ERR_INVALID_ARG
+
+
+def test_plain_activation_ignores_alpha_and_limit():
+    w = _weights()
+    w.act, w.alpha, w.limit = moe.MOE_ACT_SWIGLU, float("nan"), 0.0
+    assert _ws(w, 8, 2)[0] == moe.MOE_OK
+
+
+@pytest.mark.parametrize("name", ["b_gate", "b_up", "b_down"])
+def test_misaligned_bias_rejected(name):
+    w = _weights()
+    setattr(w, name, FAKE)
+    assert _ws(w, 8, 2)[0] == moe.MOE_OK
+    setattr(w, name, FAKE + 4)
+    assert _ws(w, 8, 2)[0] == moe.MOE_ERR_INVALID_ARG
+
+
+def test_down_bias_needs_topk_idx():
+    L = moe.lib()
+    w, r = _weights(), _routing()
+    w.b_down = FAKE
+    st, need = _ws(w, 8, 2)
+    assert st == moe.MOE_OK
+    r.topk_idx = None
+    assert L.moe_verify_layer(FAKE, C.byref(w), C.byref(r), 2 * FAKE, 4 * FAKE, need, None) == moe.MOE_ERR_INVALID_ARG
+
+
 @pytest.mark.parametrize("fmt,E,N,K,status", [
     (3, 1, 16, 32, moe.MOE_ERR_INVALID_ARG), (0, 0, 16, 32, moe.MOE_ERR_INVALID_ARG),
     (0, 1, 24, 32, moe.MOE_ERR_UNSUPPORTED), (0, 1, 16, 48, moe.MOE_ERR_UNSUPPORTED),
