@@ -401,6 +401,27 @@ __device__ __forceinline__ int tile_row(const ItemDesc &d, int wave, int t)
 
 // ----------------------------------------------------------------------------- epilogue
 
+// Gate and up biases of a wavefront's rows of an item (zeros without biases,
+// for the shared expert and for the down launch).  The expert kernel loads
+// them when it starts an item and uses them when it finishes it, so the loads
+// are long done by then.
+struct ItemBias {
+    f32x4 g, u;
+};
+
+template <bool DOWN>
+__device__ __forceinline__ ItemBias load_bias(const FfnParams &P, const ItemDesc &d, int wave)
+{
+    const VerifyArgs &a = P.a;
+    ItemBias b{f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    if (DOWN || d.shared || (!a.b_gate && !a.b_up)) return b;
+    const int row = d.n0 + 16 * wave + 4 * (lane_id() >> 4);  // gate/up rows row .. row + 3 of this lane
+    if (row >= P.N) return b;
+    if (a.b_gate) b.g = *reinterpret_cast<const f32x4 *>(a.b_gate + (size_t)d.e * a.d_ff + row);
+    if (a.b_up) b.u = *reinterpret_cast<const f32x4 *>(a.b_up + (size_t)d.e * a.d_ff + row);
+    return b;
+}
+
 // h from the gate and up values of one row (biases already added):
 // act 0 silu(g) * u; act 1 (GPT-OSS) with g capped at limit and u clamped to
 // [-limit, limit], g * sigmoid(alpha * g) * (u + 1).  The comparisons keep NaN.
@@ -418,7 +439,7 @@ __device__ __forceinline__ float activate(const VerifyArgs &a, float g, float u)
 // token column col of each 16-token block.
 template <bool DOWN>
 __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &d, int wave,
-                                            const f32x4 (&acc)[2][kMB])
+                                            const f32x4 (&acc)[2][kMB], const ItemBias &bias)
 {
     const VerifyArgs &a = P.a;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
@@ -438,11 +459,8 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
                     h2[i] = pack_bf16x2(g0 / (1.f + expf(-g0)) * v[2 * i], g1 / (1.f + expf(-g1)) * v[2 * i + 1]);
                 }
             } else {
-                const int row = tile_row<DOWN>(d, wave, 0) + 4 * grp;  // rows row .. row + 3 of this lane
-                if (!d.shared) {
-                    if (a.b_gate) g += *reinterpret_cast<const f32x4 *>(a.b_gate + (size_t)d.e * a.d_ff + row);
-                    if (a.b_up) v += *reinterpret_cast<const f32x4 *>(a.b_up + (size_t)d.e * a.d_ff + row);
-                }
+                g += bias.g;
+                v += bias.u;
                 float h[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) h[i] = activate(a, g[i], v[i]);
@@ -747,6 +765,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // The item being contracted.
     int citem = (int)(x0 / nsteps);
     ItemDesc cd = describe_lds<DOWN>(P, sp, citem);
+    ItemBias cbias = load_bias<DOWN>(P, cd, wave);
     long cib = (long)citem * nsteps;
     f32x4 acc[2][kMB];
 #pragma unroll
@@ -776,7 +795,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         // cut at either end of the range) and move on to the next one.
         if (u + 1 == cib + nsteps || u + 1 == x1) {
             if (cib >= x0 && cib + nsteps <= x1) {
-                finish_item<DOWN>(P, cd, wave, acc);
+                finish_item<DOWN>(P, cd, wave, acc, cbias);
             } else {
                 float *dst = P.partials + ((size_t)w * 2 + (cib <= x0 ? 0 : 1)) * kPartialFloats;
 #pragma unroll
@@ -794,6 +813,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                 ++citem;
                 cib += nsteps;
                 cd = describe_lds<DOWN>(P, sp, citem);
+                cbias = load_bias<DOWN>(P, cd, wave);
             }
         }
     };
@@ -879,7 +899,7 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
             add(P.partials + ((size_t)v * 2 + ((ib <= v0 && v0 < ie) ? 0 : 1)) * kPartialFloats);
         }
     }
-    finish_item<DOWN>(P, d, wave, acc);
+    finish_item<DOWN>(P, d, wave, acc, load_bias<DOWN>(P, d, wave));
 }
 
 // Token groups when some expert may have more than 64 tokens (T > 64):
