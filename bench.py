@@ -362,6 +362,43 @@ def variant_timing(T=64, steps=30, warmup=3, n_pool=8):
     return out
 
 
+def shape_sweep(name, Us, T=64, steps=20, warmup=3, n_pool=8):
+    """Step latency and algorithmic GB/s vs U for another model shape (exact-U routing, a different
+    expert set every step, so weights are read cold: the sets rotate over all experts of the layer)."""
+    import torch
+    import synth
+    import paper_2607_12696_amd as moe
+    dev = torch.device("cuda:0")
+    sh = synth.SHAPES[name]
+    raw = synth.layer_weights(sh, seed=0, device=dev)
+    wd = moe.pack_layer(raw)
+    del raw
+    x = synth.activations(T, sh.d, seed=1, device=dev)
+    y = torch.empty_like(x)
+    ws = torch.empty(moe.moe_verify_workspace_size(wd, T, sh.k), dtype=torch.uint8, device=dev)
+    per_expert = sum(synth.expert_bytes(sh.d, sh.d_ff, sh.fmt))
+    out = []
+    for U in Us:
+        pool = [synth.routes_to_logits(synth.routes_exact_u(T, sh.E, sh.k, U, seed=500 * U + i), sh.E, seed=i,
+                                       device=dev) for i in range(n_pool)]
+        for i in range(warmup):
+            moe.moe_verify_step(x, pool[i % n_pool], wd, sh.k, sh.score, workspace=ws, y=y)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(steps):
+            moe.moe_verify_step(x, pool[i % n_pool], wd, sh.k, sh.score, workspace=ws, y=y)
+        b.record()
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) * 1e3 / steps
+        B = (U + (1 if sh.shared else 0)) * per_expert + 4 * T * sh.d + 4 * T * sh.E
+        out.append({"U": U, "step_us": us, "GB_s": B / (us * 1e-6) / 1e9, "frac_of_8TBs": B / (us * 1e-6) / 8e12})
+        log(f"  {name} U={U:4d}: step {us:8.1f} us  {out[-1]['GB_s']:7.0f} GB/s")
+    del wd, ws
+    torch.cuda.empty_cache()
+    return {"shape": name, "d": sh.d, "d_ff": sh.d_ff, "E": sh.E, "k": sh.k, "fmt": sh.fmt, "T": T, "points": out}
+
+
 def pct(v, q):
     s = sorted(v)
     return s[min(len(s) - 1, max(0, int(round(q * (len(s) - 1)))))]
@@ -696,11 +733,12 @@ def main():
         log("timing the oracle on the host ...")
         cpu, err = cpu_baseline(wl, args.U, args.cpu_tokens)
 
-    variants = None
+    variants, others = None, None
     if not args.no_sweep:
         del wl
         torch.cuda.empty_cache()
         variants = variant_timing()
+        others = [shape_sweep("qwen", [8, 32, 64, 128]), shape_sweep("gpt", [8, 32, 64, 128])]
         log(f"GPT-OSS layer T=64: plain {variants['gpt_oss_T64_clustered']['plain_swiglu_us']:.1f} us, "
             f"GPT-OSS expert {variants['gpt_oss_T64_clustered']['gpt_oss_expert_us']:.1f} us; "
             f"grouped routing {variants['ds_routing_T64']['grouped_us']:.1f} us")
@@ -738,6 +776,7 @@ def main():
         "stack_8_layers_T16": stack,
         "router": router,
         "variants": variants,
+        "sweep_other_shapes_T64": others,
     }
     print(json.dumps(out))
     return 0
