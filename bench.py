@@ -633,7 +633,7 @@ def main():
     ap.add_argument("--sweep", default="8,16,24,32,48,64,96,128,192,256")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=8)
+    ap.add_argument("--cpu-tokens", type=int, default=48)
     ap.add_argument("--no-stack", action="store_true", help="skip the 8-layer draft-tree verification step")
     ap.add_argument("--stack-only", action="store_true", help="only the 8-layer draft-tree verification step")
     ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 plus a calibration copy")
@@ -665,11 +665,12 @@ def main():
     sh = wl.sh
 
     if args.profile:
-        for i in range(3):
+        # The headline's own steps: W warm-ups, then K steps (as the timed region runs them).
+        for i in range(args.warmup):
             wl.step(args.U, i)
         torch.cuda.synchronize()
-        for i in range(10):
-            wl.step(args.U, 3 + i)
+        for i in range(args.steps):
+            wl.step(args.U, args.warmup + i)
         # Calibration copy for the HBM counters: one elementwise kernel that reads and
         # writes COPY_BYTES each, with a name nothing else in the run uses.
         src = torch.ones(COPY_BYTES // 4, dtype=torch.int32, device=wl.dev)
