@@ -342,6 +342,33 @@ def test_verify_small_matches_oracle(name, T):
     assert err <= YTOL
 
 
+# Limits of the verify path: T * k above the 4096 routed slots whose token rows the expert kernels stage in
+# LDS (the rows then come through scalar loads), E = 1024 with k = 64, and one token with k = 64.
+LIMIT_CASES = [
+    (synth.Shape("lim_bf16", 64, 32, 128, 64, synth.FMT_BF16, 0, False), 130),
+    (synth.Shape("lim_fp4", 64, 64, 64, 64, synth.FMT_MXFP4, 0, False), 70),
+    (synth.Shape("lim_e1024", 64, 32, 1024, 64, synth.FMT_BF16, 1, False), 64),
+    (synth.Shape("lim_t1", 128, 64, 64, 64, synth.FMT_BF16, 0, False), 1),
+    (synth.Shape("lim_fp8_sh", 128, 128, 96, 48, synth.FMT_FP8, 1, True), 100),
+]
+
+
+@pytest.mark.parametrize("sh,T", LIMIT_CASES, ids=[c[0].name for c in LIMIT_CASES])
+def test_verify_at_limits_matches_oracle(sh, T):
+    note(f"verify limits shape={sh.name} T={T} k={sh.k} E={sh.E} slots={T * sh.k}")
+    layer = synth.layer_weights(sh, seed=61)
+    x = synth.activations(T, sh.d, seed=62)
+    lg = synth.logits_scattered(T, sh.E, seed=63)
+    y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), to_dev(layer), sh.k, sh.score)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), sh.k, sh.score)
+    assert np.array_equal(r.topk_idx.cpu().numpy(), idx_o)
+    y_ref = oracle.verify_tokens(layer, x, idx_o, w_o, threads=16)
+    err = y_err(y.float().cpu().numpy(), y_ref)
+    note(f"  U={int(r.n_unique.item())} rel err {err:.3e}")
+    assert err <= YTOL
+
+
 def with_oai(layer, sh, seed, bias_std=4.0):
     # GPT-OSS expert variant: biases large enough that both clamps bind on some rows.
     out = dict(layer)
