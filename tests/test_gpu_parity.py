@@ -556,3 +556,46 @@ def test_full_shape_sampled_rows(name, T, kind, U, rows):
     y2, _ = moe.moe_verify_step(x.to(DEV), lg.to(DEV), dl, sh.k, sh.score)
     assert torch.isfinite(y.float()).all()
     assert torch.equal(y, y2)
+
+
+# ----------------------------------------------------------------------------- HIP graph capture
+
+@pytest.mark.parametrize("name,T", [("fp8", 64), ("mxfp4", 130), ("bf16_tail", 37)])
+def test_graph_replay_matches_eager(name, T):
+    # The whole step (route, union, verify) captured once and replayed with new routing each time, with eager
+    # work and synchronisations between the replays; every replay equals the eager step bit for bit.
+    sh = SMALL[name]
+    note(f"graph replay shape={name} T={T}")
+    dl = to_dev(small_layer(name))
+    x = synth.activations(T, sh.d, seed=71).to(DEV)
+    lg = torch.empty(T, sh.E, dtype=torch.float32, device=DEV)
+    ws = torch.empty(moe.moe_verify_workspace_size(dl, T, sh.k), dtype=torch.uint8, device=DEV)
+    y = torch.empty_like(x)
+    r = moe.moe_route_union(synth.logits_scattered(T, sh.E, seed=70).to(DEV), sh.k, sh.score)
+    lg.copy_(synth.logits_scattered(T, sh.E, seed=70).to(DEV))
+
+    def step():
+        moe.moe_route_union(lg, sh.k, sh.score, out=r)
+        moe.moe_verify_layer(x, dl, r, y=y, workspace=ws)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for rep in range(4):
+        lg.copy_(synth.logits_scattered(T, sh.E, seed=80 + rep).to(DEV))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        y_graph = y.clone()
+        idx_graph = r.topk_idx.clone()
+        ws.fill_(0x5A)  # eager work in between that also scribbles over the workspace
+        step()
+        torch.cuda.synchronize()
+        assert torch.equal(idx_graph, r.topk_idx), rep
+        assert torch.equal(y_graph, y), rep
