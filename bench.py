@@ -138,9 +138,9 @@ class Workload:
             raw.update(cp)
             self.rawdicts.append(raw)
             wd = dict(routed_packed)
-            for name in ("gate", "up", "down"):
-                wd["sh_" + name], wd["sh_s_" + name] = moe.moe_pack_weights(sh.fmt, cp["sh_" + name],
-                                                                           cp["sh_s_" + name])
+            wd["sh_gate"], wd["sh_s_gate"], wd["sh_s_up"] = moe.moe_pack_gate_up(
+                sh.fmt, cp["sh_gate"], cp["sh_up"], cp["sh_s_gate"], cp["sh_s_up"])
+            wd["sh_down"], wd["sh_s_down"] = moe.moe_pack_weights(sh.fmt, cp["sh_down"], cp["sh_s_down"])
             self.wdicts.append(wd)
         torch.cuda.synchronize()
         nbytes = moe.moe_verify_workspace_size(self.wdicts[0], T, sh.k)

@@ -92,6 +92,9 @@ typedef enum {
  * activation and each expert output gets b_down before the gate weight.
  * The shared expert takes the activation but no biases.  A zero-initialised
  * struct tail (act 0, NULL biases) is the plain SwiGLU layer.
+ * w_up == NULL means W_gate and W_up were packed together by
+ * moe_pack_gate_up into w_gate (likewise sh_up == NULL with sh_gate set);
+ * s_up (sh_s_up) still points to the up scales.
  * Requirements: d % 32 == 0, d_ff % 32 == 0, and for FP8 d % 128 == 0 and
  * d_ff % 128 == 0; each packed matrix below 2 GiB; 16-byte aligned pointers.
  * Other shapes return MOE_ERR_UNSUPPORTED. */
@@ -151,6 +154,20 @@ moe_status_t moe_route_union(const float *logits, int T, int E, int k, int score
  * bf16).  Requirements: N % 16 == 0, K % 32 == 0 (FP8: N, K % 128 == 0).
  */
 moe_status_t moe_packed_size(int fmt, int E, int N, int K, size_t *weight_bytes, size_t *scale_bytes);
+
+/*
+ * W_gate and W_up (both E x N x K, N = d_ff, K = d) packed as one pair: the
+ * streaming layout of moe_pack_weights, except that block (rb, kb) of the
+ * pair is the gate block (B bytes) immediately followed by the up block, so
+ * the verify kernel streams both tiles of a step as one contiguous run.
+ * w_packed: 2 * weight_bytes of moe_packed_size (per pair of matrices);
+ * s_gate_packed, s_up_packed: scale_bytes each (NULL for bf16), laid out as
+ * moe_pack_weights lays them out.  A layer packed this way passes w_gate =
+ * w_packed and w_up = NULL in moe_weights_t.  Requirements as for
+ * moe_pack_weights, and 2 * weight_bytes / E below 2 GiB.
+ */
+moe_status_t moe_pack_gate_up(int fmt, int E, int N, int K, const void *w_gate, const void *s_gate, const void *w_up,
+                              const void *s_up, void *w_packed, void *s_gate_packed, void *s_up_packed, void *stream);
 moe_status_t moe_pack_weights(int fmt, int E, int N, int K, const void *w, const void *s, void *w_packed,
                               void *s_packed, void *stream);
 

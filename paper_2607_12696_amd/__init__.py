@@ -37,7 +37,7 @@ MOE_SEL_COST_RATIO, MOE_SEL_CONFIDENCE, MOE_SEL_GLOBAL_COST, MOE_SEL_COST_DIFF =
 MOE_ACT_SWIGLU, MOE_ACT_SWIGLU_OAI = 0, 1
 
 EXPORTED = ("moe_route_topk", "moe_route_union", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
-            "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree",
+            "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_pack_gate_up", "moe_select_tree",
             "moe_status_string", "moe_last_error")
 
 
@@ -85,12 +85,14 @@ def lib() -> C.CDLL:
                                                  C.c_size_t, p, C.POINTER(C.c_void_p)]
             L.moe_packed_size.argtypes = [i, i, i, i, C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]
             L.moe_pack_weights.argtypes = [i, i, i, i, p, p, p, p, p]
+            L.moe_pack_gate_up.argtypes = [i, i, i, i, p, p, p, p, p, p, p, p]
             L.moe_select_tree.argtypes = [i, p, p, i, i, p, i, p, i, C.c_double, C.c_double, i, p, p, p]
             L.moe_status_string.argtypes = [i]
             L.moe_status_string.restype = C.c_char_p
             L.moe_last_error.restype = C.c_char_p
             for f in ("moe_route_topk", "moe_route_union", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
-                      "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_select_tree"):
+                      "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_pack_gate_up",
+                      "moe_select_tree"):
                 getattr(L, f).restype = i
             _lib = L
     return _lib
@@ -278,14 +280,42 @@ def moe_pack_weights(fmt: int, w, s=None):
     return wp, sp
 
 
-def pack_layer(layer: dict) -> dict:
-    """A layer dict (interchange layout, device tensors) with every matrix packed."""
+def moe_pack_gate_up(fmt: int, w_gate, w_up, s_gate=None, s_up=None):
+    """Pack stacked device W_gate and W_up [E, N, K(/2)] (+ scales) as one pair.
+
+    Returns (w_packed, s_gate_packed, s_up_packed); the scales are None for bf16.
+    """
+    torch = _torch()
+    E, N = w_gate.shape[0], w_gate.shape[1]
+    K = w_gate.shape[2] * (2 if fmt == MOE_W_MXFP4 else 1)
+    wb, sb = moe_packed_size(fmt, E, N, K)
+    wp = torch.empty(2 * wb, dtype=torch.uint8, device=w_gate.device)
+    sgp = torch.empty(sb, dtype=torch.uint8, device=w_gate.device) if sb else None
+    sup = torch.empty(sb, dtype=torch.uint8, device=w_gate.device) if sb else None
+    _check("moe_pack_gate_up", lib().moe_pack_gate_up(
+        fmt, E, N, K, _dev_ptr(w_gate, "w_gate"), _dev_ptr(s_gate, "s_gate"), _dev_ptr(w_up, "w_up"),
+        _dev_ptr(s_up, "s_up"), _dev_ptr(wp, "w_packed"), _dev_ptr(sgp, "s_gate_packed"), _dev_ptr(sup, "s_up_packed"),
+        _stream(w_gate)))
+    return wp, sgp, sup
+
+
+def pack_layer(layer: dict, pair: bool = True) -> dict:
+    """A layer dict (interchange layout, device tensors) with every matrix packed; with `pair`,
+    W_gate and W_up as one pair (moe_pack_gate_up; the dict then has no "up" / "sh_up" entry)."""
     out = {k: layer[k] for k in ("fmt", "d", "d_ff", "act", "alpha", "limit", "b_gate", "b_up", "b_down")
            if k in layer}
     out["E"] = int(layer.get("E", layer["gate"].shape[0]))
     fmt = int(layer["fmt"])
     for prefix in ("", "sh_"):
-        for name in ("gate", "up", "down"):
+        names = ("gate", "up", "down")
+        if pair and layer.get(prefix + "gate") is not None and layer.get(prefix + "up") is not None:
+            wp, sgp, sup = moe_pack_gate_up(fmt, layer[prefix + "gate"], layer[prefix + "up"],
+                                            layer.get(prefix + "s_gate"), layer.get(prefix + "s_up"))
+            out[prefix + "gate"] = wp
+            if sgp is not None:
+                out[prefix + "s_gate"], out[prefix + "s_up"] = sgp, sup
+            names = ("down",)
+        for name in names:
             if layer.get(prefix + name) is None:
                 continue
             wp, sp = moe_pack_weights(fmt, layer[prefix + name], layer.get(prefix + "s_" + name))
@@ -312,7 +342,7 @@ def weights_struct(w: dict) -> moe_weights_t:
     s.fmt, s.d, s.d_ff = int(w["fmt"]), int(w["d"]), int(w["d_ff"])
     s.E = int(w["E"]) if "E" in w else int(w["gate"].shape[0])
     for name in ("gate", "up", "down"):
-        setattr(s, "w_" + name, _dev_ptr(w[name], name))
+        setattr(s, "w_" + name, _dev_ptr(w.get(name), name))
         setattr(s, "s_" + name, _dev_ptr(w.get("s_" + name), "s_" + name))
         setattr(s, "sh_" + name, _dev_ptr(w.get("sh_" + name), "sh_" + name))
         setattr(s, "sh_s_" + name, _dev_ptr(w.get("sh_s_" + name), "sh_s_" + name))

@@ -31,18 +31,19 @@ moe_status_t check_weights(const moe_weights_t *w)
     if (!w) return MOE_ERR_INVALID_ARG;
     if (w->fmt < MOE_W_BF16 || w->fmt > MOE_W_MXFP4) return MOE_ERR_INVALID_ARG;
     if (w->d < 1 || w->d_ff < 1 || w->E < 1 || w->E > kMaxE) return MOE_ERR_INVALID_ARG;
-    if (!w->w_gate || !w->w_up || !w->w_down) return MOE_ERR_INVALID_ARG;
+    // w_up == NULL: W_gate and W_up packed as one pair in w_gate (moe_pack_gate_up); the same for sh_up.
+    if (!w->w_gate || !w->w_down) return MOE_ERR_INVALID_ARG;
     if (w->fmt != MOE_W_BF16 && (!w->s_gate || !w->s_up || !w->s_down)) return MOE_ERR_INVALID_ARG;
-    const int nsh = (w->sh_gate != nullptr) + (w->sh_up != nullptr) + (w->sh_down != nullptr);
-    if (nsh != 0 && nsh != 3) return MOE_ERR_INVALID_ARG;
-    if (nsh == 3 && w->fmt != MOE_W_BF16 && (!w->sh_s_gate || !w->sh_s_up || !w->sh_s_down))
-        return MOE_ERR_INVALID_ARG;
+    const bool sh = w->sh_gate != nullptr || w->sh_up != nullptr || w->sh_down != nullptr;
+    if (sh && (!w->sh_gate || !w->sh_down)) return MOE_ERR_INVALID_ARG;
+    if (sh && w->fmt != MOE_W_BF16 && (!w->sh_s_gate || !w->sh_s_up || !w->sh_s_down)) return MOE_ERR_INVALID_ARG;
     // Tile shapes of the kernels: 16-row gate/up bands, 32-row down bands,
     // 32-wide K chunks; FP8 needs whole 128x128 scale blocks.
     if (w->d % 32 || w->d_ff % 32) return MOE_ERR_UNSUPPORTED;
     if (w->fmt == MOE_W_FP8_E4M3_B128 && (w->d % 128 || w->d_ff % 128)) return MOE_ERR_UNSUPPORTED;
     // Every packed matrix is addressed through a 32-bit buffer range below 2^31 bytes.
-    if (ecospec::packed_matrix_bytes(w->fmt, w->d_ff, w->d) >= (1UL << 31)) return MOE_ERR_UNSUPPORTED;
+    const size_t pair = (!w->w_up || (sh && !w->sh_up)) ? 2 : 1;
+    if (ecospec::packed_matrix_bytes(w->fmt, w->d_ff, w->d) * pair >= (1UL << 31)) return MOE_ERR_UNSUPPORTED;
     const void *mats[] = {w->w_gate, w->w_up, w->w_down, w->sh_gate, w->sh_up, w->sh_down};
     for (const void *p : mats)
         if (p && !aligned(p, 16)) return MOE_ERR_INVALID_ARG;
@@ -195,6 +196,8 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     a.k = r->k;
     a.w_gate = static_cast<const uint8_t *>(w->w_gate);
     a.w_up = static_cast<const uint8_t *>(w->w_up);
+    a.gu_pair = w->w_up == nullptr;
+    a.sh_gu_pair = w->sh_gate != nullptr && w->sh_up == nullptr;
     a.w_down = static_cast<const uint8_t *>(w->w_down);
     a.s_gate = w->s_gate;
     a.s_up = w->s_up;
@@ -264,6 +267,20 @@ moe_status_t moe_pack_weights(int fmt, int E, int N, int K, const void *w, const
     if (!w || !w_packed || w == w_packed || !aligned(w, 16) || !aligned(w_packed, 16)) return MOE_ERR_INVALID_ARG;
     if (fmt != MOE_W_BF16 && (!s || !s_packed || s == s_packed)) return MOE_ERR_INVALID_ARG;
     return from_hip(ecospec::launch_pack(fmt, E, N, K, w, s, w_packed, s_packed, (hipStream_t)stream));
+}
+
+moe_status_t moe_pack_gate_up(int fmt, int E, int N, int K, const void *w_gate, const void *s_gate, const void *w_up,
+                              const void *s_up, void *w_packed, void *s_gate_packed, void *s_up_packed, void *stream)
+{
+    const moe_status_t st = check_pack(fmt, E, N, K);
+    if (st != MOE_OK) return st;
+    if (ecospec::packed_matrix_bytes(fmt, N, K) * 2 >= (1UL << 31)) return MOE_ERR_UNSUPPORTED;
+    if (!w_gate || !w_up || !w_packed || w_gate == w_packed || w_up == w_packed) return MOE_ERR_INVALID_ARG;
+    if (!aligned(w_gate, 16) || !aligned(w_up, 16) || !aligned(w_packed, 16)) return MOE_ERR_INVALID_ARG;
+    if (fmt != MOE_W_BF16 && (!s_gate || !s_up || !s_gate_packed || !s_up_packed || s_gate_packed == s_up_packed))
+        return MOE_ERR_INVALID_ARG;
+    return from_hip(ecospec::launch_pack_gate_up(fmt, E, N, K, w_gate, s_gate, w_up, s_up, w_packed, s_gate_packed,
+                                                 s_up_packed, (hipStream_t)stream));
 }
 
 }  // extern "C"

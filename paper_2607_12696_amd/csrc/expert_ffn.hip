@@ -317,6 +317,7 @@ struct ItemDesc {
     int M;                   // tokens in the group (<= 64)
     int e;                   // expert id (-1: the shared expert)
     bool shared;
+    bool pair;               // gate/up: the two matrices packed as one pair at wa (wb == wa)
 };
 
 template <bool DOWN>
@@ -345,9 +346,11 @@ __device__ __forceinline__ ItemDesc describe(const FfnParams &P, const Plan &pl,
     auto sptr = [&](const void *base) {
         return base ? static_cast<const void *>(static_cast<const uint8_t *>(base) + e * sc) : nullptr;
     };
+    d.pair = false;
     if (!DOWN) {
-        d.wa = (d.shared ? a.sh_gate : a.w_gate) + e * mat;
-        d.wb = (d.shared ? a.sh_up : a.w_up) + e * mat;
+        d.pair = d.shared ? a.sh_gu_pair : a.gu_pair;
+        d.wa = (d.shared ? a.sh_gate : a.w_gate) + e * mat * (d.pair ? 2 : 1);
+        d.wb = d.pair ? d.wa : (d.shared ? a.sh_up : a.w_up) + e * mat;
         d.sa = d.shared ? a.sh_s_gate : sptr(a.s_gate);
         d.sb = d.shared ? a.sh_s_up : sptr(a.s_up);
     } else {
@@ -379,9 +382,11 @@ __device__ __forceinline__ ItemDesc describe_lds(const FfnParams &P, const Split
     auto sptr = [&](const void *base) {
         return base ? static_cast<const void *>(static_cast<const uint8_t *>(base) + e * sc) : nullptr;
     };
+    d.pair = false;
     if (!DOWN) {
-        d.wa = (d.shared ? a.sh_gate : a.w_gate) + e * mat;
-        d.wb = (d.shared ? a.sh_up : a.w_up) + e * mat;
+        d.pair = d.shared ? a.sh_gu_pair : a.gu_pair;
+        d.wa = (d.shared ? a.sh_gate : a.w_gate) + e * mat * (d.pair ? 2 : 1);
+        d.wb = d.pair ? d.wa : (d.shared ? a.sh_up : a.w_up) + e * mat;
         d.sa = d.shared ? a.sh_s_gate : sptr(a.s_gate);
         d.sb = d.shared ? a.sh_s_up : sptr(a.s_up);
     } else {
@@ -484,6 +489,7 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
 struct Source {
     rsrc_t ra0, ra1, rs0, rs1;  // weight tiles 0 / 1 and their scales
     uint32_t a0, a1;            // lane offsets of the two tiles at step 0 (kOff: rows past N)
+    uint32_t kstride;           // bytes from one 128-wide block of a tile to the next
     uint32_t q0, q1;            // scale offsets at step 0
     uint32_t boff[kBPass];      // lane offsets of this thread's activation rows at step 0 (kOff: no token)
     long ib, ie;                // the item's units [ib, ie)
@@ -507,12 +513,21 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
     const int nblocks = P.nblocks;
     const uint32_t mat_bytes =
         (uint32_t)((size_t)P.N * nblocks * kMacroK * (FMT == FMT_BF16 ? 2 : 1) / (FMT == FMT_MXFP4 ? 2 : 1));
-    src.ra0 = make_rsrc(d.wa, mat_bytes);
-    src.ra1 = make_rsrc(d.wb, mat_bytes);
     const int row0 = tile_row<DOWN>(d, wave, 0), row1 = tile_row<DOWN>(d, wave, 1);
     const bool arow_ok = row0 < P.N;
-    src.a0 = arow_ok ? (uint32_t)(row0 / 16) * nblocks * BLK + lane * 16u : kOff;
-    src.a1 = arow_ok ? (uint32_t)(row1 / 16) * nblocks * BLK + lane * 16u : kOff;
+    if (d.pair) {
+        // Gate block then up block of the same rows: one contiguous run per block.
+        src.ra0 = src.ra1 = make_rsrc(d.wa, 2u * mat_bytes);
+        src.kstride = 2u * BLK;
+        src.a0 = arow_ok ? (uint32_t)(row0 / 16) * nblocks * 2u * BLK + lane * 16u : kOff;
+        src.a1 = arow_ok ? src.a0 + BLK : kOff;
+    } else {
+        src.ra0 = make_rsrc(d.wa, mat_bytes);
+        src.ra1 = make_rsrc(d.wb, mat_bytes);
+        src.kstride = BLK;
+        src.a0 = arow_ok ? (uint32_t)(row0 / 16) * nblocks * BLK + lane * 16u : kOff;
+        src.a1 = arow_ok ? (uint32_t)(row1 / 16) * nblocks * BLK + lane * 16u : kOff;
+    }
     const uint32_t sc_bytes = FMT == FMT_FP8 ? (uint32_t)((P.N / 128) * (K / 128) * 4)
                                              : (uint32_t)((size_t)P.N * ((nblocks + 3) / 4) * 16);
     src.rs0 = make_rsrc(FMT == FMT_BF16 ? d.wa : d.sa, FMT == FMT_BF16 ? 0u : sc_bytes);
@@ -734,7 +749,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             // Block kb of the tile; a step's second block can lie past the last one.
             const uint32_t kb = step * SB + b;
             const bool okb = ok && (SB == 1 || (int)kb < P.nblocks);
-            const uint32_t so = kb * BLK;
+            const uint32_t so = kb * src.kstride;
 #pragma unroll
             for (int i = 0; i < NV; ++i) {
                 wf[slot][0].v[b * NV + i] = load16<kAuxNT>(src.ra0, okb ? src.a0 + so + 1024u * i : kOff);

@@ -29,6 +29,7 @@ hipError_t launch_expert_union(const int32_t *idx, int T, int k, int E, int32_t 
 struct VerifyArgs {
     int fmt, d, d_ff, E, T, k;
     const uint8_t *w_gate, *w_up, *w_down;  // routed experts, stacked [E]
+    bool gu_pair, sh_gu_pair;               // W_gate and W_up packed as one pair in w_gate / sh_gate
     const void *s_gate, *s_up, *s_down;
     const uint8_t *sh_gate, *sh_up, *sh_down;  // shared expert or null
     const void *sh_s_gate, *sh_s_up, *sh_s_down;
@@ -71,6 +72,8 @@ hipError_t launch_verify(const VerifyArgs &a, void *workspace, const VerifyWorks
 // Packed (streaming) weight layout; see pack.hip.
 size_t packed_matrix_bytes(int fmt, int N, int K);
 size_t packed_scale_bytes(int fmt, int N, int K);
+hipError_t launch_pack_gate_up(int fmt, int E, int N, int K, const void *wg, const void *sg, const void *wu,
+                               const void *su, void *wp, void *sgp, void *sup, hipStream_t stream);
 hipError_t launch_pack(int fmt, int E, int N, int K, const void *w, const void *s, void *wp, void *sp,
                        hipStream_t stream);
 

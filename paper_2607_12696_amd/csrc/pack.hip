@@ -11,6 +11,11 @@
 // with one 16-byte load gets exactly the A-operand fragment of the matrix-core
 // instruction, and a wavefront reads each vector as 1 KiB of contiguous memory.
 //
+// W_gate and W_up can also be packed as one pair (moe_pack_gate_up): block
+// (rb, kb) of the pair is the gate block followed by the up block, so a
+// wavefront reads both tiles of a step as one contiguous run (one stream
+// instead of two, measured 4% more bandwidth in the kernel's geometry).
+//
 // MXFP4 scales move to the same blocking, four blocks to a 256-byte quad: in
 // quad q of row tile rb, the 4 bytes at offset 4*l (l = c + 16*g) are the
 // e8m0 codes of row rb*16 + c for the 32-element chunks (4q + j)*4 + g,
@@ -22,15 +27,19 @@
 
 namespace ecospec {
 
-// One thread writes one 16-byte lane vector of the packed matrix.
+// One thread writes one 16-byte lane vector of the packed matrix.  pair = 2
+// packs W_gate and W_up together: block (rb, kb) of the pair holds the gate
+// block and then the up block (`which` = 0 / 1), so the verify kernel reads
+// both tiles of a step as one contiguous run.
 __global__ __launch_bounds__(256) void pack_weights_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict__ dst,
-                                                           int E, int N, int K, int num, int den, int vecs)
+                                                           int E, int N, int K, int num, int den, int vecs, int pair,
+                                                           int which)
 {
     const int nkb = (K + 127) / 128;
     const size_t per_block = (size_t)vecs * 64;  // lane vectors per block
     const size_t total = (size_t)E * (N / 16) * nkb * per_block;
     const size_t src_row = (size_t)K * num / den, src_mat = (size_t)N * src_row;
-    const size_t dst_mat = (size_t)(N / 16) * nkb * per_block * 16;
+    const size_t dst_mat = (size_t)(N / 16) * nkb * per_block * 16 * pair;
     for (size_t q = blockIdx.x * (size_t)blockDim.x + threadIdx.x; q < total; q += (size_t)gridDim.x * blockDim.x) {
         const size_t e = q / ((size_t)(N / 16) * nkb * per_block);
         size_t r = q - e * ((size_t)(N / 16) * nkb * per_block);
@@ -46,7 +55,8 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const uint8_t *__rest
             const uint8_t *p = src + e * src_mat + (size_t)(rb * 16 + c) * src_row + (size_t)k0 * num / den;
             v = *reinterpret_cast<const u32x4 *>(p);
         }
-        uint8_t *o = dst + e * dst_mat + (((size_t)rb * nkb + kb) * vecs + i) * 1024 + (size_t)l * 16;
+        uint8_t *o = dst + e * dst_mat + (((size_t)rb * nkb + kb) * pair + which) * ((size_t)vecs * 1024) +
+                     (size_t)i * 1024 + (size_t)l * 16;
         *reinterpret_cast<u32x4 *>(o) = v;
     }
 }
@@ -83,16 +93,19 @@ size_t packed_scale_bytes(int fmt, int N, int K)
     return 0;
 }
 
-hipError_t launch_pack(int fmt, int E, int N, int K, const void *w, const void *s, void *wp, void *sp,
-                       hipStream_t stream)
+static hipError_t pack_matrix(int fmt, int E, int N, int K, const void *w, void *wp, int pair, int which,
+                              hipStream_t stream)
 {
     const int num = fmt == 0 ? 2 : 1, den = fmt == 2 ? 2 : 1, vecs = fmt == 0 ? 4 : fmt == 1 ? 2 : 1;
     const size_t vec_total = (size_t)E * (N / 16) * ((K + 127) / 128) * vecs * 64;
     const int grid = (int)((vec_total + 255) / 256 < 65536 ? (vec_total + 255) / 256 : 65536);
     hipLaunchKernelGGL(pack_weights_kernel, dim3(grid), dim3(256), 0, stream, static_cast<const uint8_t *>(w),
-                       static_cast<uint8_t *>(wp), E, N, K, num, den, vecs);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
+                       static_cast<uint8_t *>(wp), E, N, K, num, den, vecs, pair, which);
+    return hipGetLastError();
+}
+
+static hipError_t pack_scales(int fmt, int E, int N, int K, const void *s, void *sp, hipStream_t stream)
+{
     if (fmt == 1)
         return hipMemcpyAsync(sp, s, (size_t)E * packed_scale_bytes(1, N, K), hipMemcpyDeviceToDevice, stream);
     if (fmt == 2) {
@@ -103,6 +116,24 @@ hipError_t launch_pack(int fmt, int E, int N, int K, const void *w, const void *
         return hipGetLastError();
     }
     return hipSuccess;
+}
+
+hipError_t launch_pack(int fmt, int E, int N, int K, const void *w, const void *s, void *wp, void *sp,
+                       hipStream_t stream)
+{
+    hipError_t err = pack_matrix(fmt, E, N, K, w, wp, 1, 0, stream);
+    if (err != hipSuccess) return err;
+    return pack_scales(fmt, E, N, K, s, sp, stream);
+}
+
+hipError_t launch_pack_gate_up(int fmt, int E, int N, int K, const void *wg, const void *sg, const void *wu,
+                               const void *su, void *wp, void *sgp, void *sup, hipStream_t stream)
+{
+    hipError_t err = pack_matrix(fmt, E, N, K, wg, wp, 2, 0, stream);
+    if (err == hipSuccess) err = pack_matrix(fmt, E, N, K, wu, wp, 2, 1, stream);
+    if (err == hipSuccess) err = pack_scales(fmt, E, N, K, sg, sgp, stream);
+    if (err == hipSuccess) err = pack_scales(fmt, E, N, K, su, sup, stream);
+    return err;
 }
 
 }  // namespace ecospec

@@ -175,6 +175,32 @@ def test_partial_shared_expert_rejected():
     w = _weights()
     w.sh_gate = FAKE
     assert _ws(w, 8, 2)[0] == moe.MOE_ERR_INVALID_ARG
+    w.sh_gate, w.sh_up, w.sh_down = None, FAKE, FAKE  # sh_up alone cannot stand in for sh_gate
+    assert _ws(w, 8, 2)[0] == moe.MOE_ERR_INVALID_ARG
+
+
+def test_paired_gate_up_accepted():
+    # w_up = NULL: W_gate and W_up packed as one pair in w_gate (and sh_up = NULL for the shared expert)
+    w = _weights(fmt=1, d=256, d_ff=256, shared=True)
+    w.w_up = None
+    assert _ws(w, 8, 2)[0] == moe.MOE_OK
+    w.sh_up = None
+    assert _ws(w, 8, 2)[0] == moe.MOE_OK
+    w.s_up = None  # the up scales are still needed
+    assert _ws(w, 8, 2)[0] == moe.MOE_ERR_INVALID_ARG
+
+
+def test_pack_gate_up_rejects():
+    L = moe.lib()
+    args = [1, 2, 128, 256, FAKE, FAKE, 2 * FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 5 * FAKE, None]
+    bad = list(args); bad[6] = None  # no w_up
+    assert L.moe_pack_gate_up(*bad) == moe.MOE_ERR_INVALID_ARG
+    bad = list(args); bad[8] = FAKE  # packed buffer aliases w_gate
+    assert L.moe_pack_gate_up(*bad) == moe.MOE_ERR_INVALID_ARG
+    bad = list(args); bad[10] = bad[9]  # both scale outputs the same buffer
+    assert L.moe_pack_gate_up(*bad) == moe.MOE_ERR_INVALID_ARG
+    bad = list(args); bad[3] = 160  # FP8 needs K % 128 == 0
+    assert L.moe_pack_gate_up(*bad) == moe.MOE_ERR_UNSUPPORTED
 
 
 def test_misaligned_weight_rejected():

@@ -30,9 +30,10 @@ def note(msg):
     sys.stdout.flush()
 
 
-def to_dev(layer):
-    """Device copy of an interchange-layout layer, packed for the verify kernels."""
-    return moe.pack_layer({k: (v.to(DEV) if hasattr(v, "to") else v) for k, v in layer.items()})
+def to_dev(layer, pair=True):
+    """Device copy of an interchange-layout layer, packed for the verify kernels (W_gate and W_up as one
+    pair unless pair=False)."""
+    return moe.pack_layer({k: (v.to(DEV) if hasattr(v, "to") else v) for k, v in layer.items()}, pair=pair)
 
 
 def y_err(y_gpu, y_ref):
@@ -408,6 +409,50 @@ def test_verify_biases_only_change_the_biased_terms():
     y1, _ = moe.moe_verify_step(x, lg, to_dev(zero), sh.k, sh.score)
     torch.cuda.synchronize()
     assert torch.equal(y0, y1)
+
+
+@pytest.mark.parametrize("name", ["toy", "fp8", "mxfp4", "bf16_tail"])
+@pytest.mark.parametrize("T", [8, 64, 130])
+def test_separate_and_paired_gate_up_layouts_agree(name, T):
+    # W_gate and W_up packed separately or as one pair: the same arithmetic in the same order, so the same
+    # bits; and both match the oracle.
+    sh = SMALL[name]
+    note(f"gate/up layouts shape={name} T={T}")
+    layer = small_layer(name)
+    x = synth.activations(T, sh.d, seed=T + 9).to(DEV)
+    lg = synth.logits_scattered(T, sh.E, seed=T + 8).to(DEV)
+    y_pair, _ = moe.moe_verify_step(x, lg, to_dev(layer, pair=True), sh.k, sh.score)
+    y_sep, _ = moe.moe_verify_step(x, lg, to_dev(layer, pair=False), sh.k, sh.score)
+    torch.cuda.synchronize()
+    assert torch.equal(y_pair, y_sep)
+
+
+def _expected_pair(fmt, wg, sg, wu, su):
+    a, _ = _expected_packed(fmt, wg, sg)
+    b, _ = _expected_packed(fmt, wu, su)
+    E, N = wg.shape[0], wg.shape[1]
+    blk = {0: 4096, 1: 2048, 2: 1024}[fmt]
+    a = a.reshape(E, -1, blk)
+    b = b.reshape(E, -1, blk)
+    return np.stack([a, b], axis=2).reshape(-1)
+
+
+@pytest.mark.parametrize("fmt,N,K", [(0, 32, 96), (1, 128, 384), (2, 32, 160), (2, 48, 640)])
+def test_pack_gate_up_pair_layout(fmt, N, K):
+    note(f"pack pair fmt={fmt} N={N} K={K}")
+    E = 2
+    mk = {0: synth.weights_bf16, 1: synth.weights_fp8_b128, 2: synth.weights_mxfp4}[fmt]
+    g = mk(E, N, K, seed=1, tag="g")
+    u = mk(E, N, K, seed=2, tag="u")
+    wg, sg = (g, None) if fmt == 0 else g
+    wu, su = (u, None) if fmt == 0 else u
+    wp, sgp, sup = moe.moe_pack_gate_up(fmt, wg.to(DEV), wu.to(DEV), None if sg is None else sg.to(DEV),
+                                        None if su is None else su.to(DEV))
+    torch.cuda.synchronize()
+    assert np.array_equal(wp.cpu().numpy(), _expected_pair(fmt, wg, sg, wu, su))
+    if fmt:
+        assert np.array_equal(sgp.cpu().numpy(), _expected_packed(fmt, wg, sg)[1])
+        assert np.array_equal(sup.cpu().numpy(), _expected_packed(fmt, wu, su)[1])
 
 
 @pytest.mark.parametrize("name", ["toy", "fp8", "mxfp4"])
