@@ -445,7 +445,14 @@ def cpu_baseline(wl, U, n_tokens):
     dt = time.time() - t0
     full = dt * wl.T / n_tokens   # the oracle's cost is proportional to the token count
     err = float(np.abs(y_gpu[rows] - y_ref).max() / np.abs(y_ref).max())
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     base = {"value": step_alg_bytes(sh, wl.T, U) / full / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "nproc": os.cpu_count(), "cpu_model": cpu_model, "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
             "sample": f"fp64 C oracle on {n_tokens} of the {wl.T} tokens of the same step (U={U}), "
                       f"{n_tokens * (sh.k + 1)} expert FFNs in {dt:.2f}s; scaled x{wl.T / n_tokens:g} to the "
                       f"whole step ({full:.1f}s)"}
@@ -767,7 +774,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": gu_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": gu_gbs / PEAK_HBM_GBS, "traffic": traffic,
                      "kernel": "expert_ffn_kernel (FP8 gate/up + SwiGLU)", "alg_bytes_per_launch": gu_bytes,
-                     "avg_launch_us": gu_ms * 1e3},
+                     "avg_launch_us": gu_ms * 1e3,
+                     "traffic_GB_s": None if traffic is None else traffic / (gu_ms * 1e-3) / 1e9},
         "cpu_baseline": cpu,
         "parity_sampled_rows_max_rel_err": err,
         "kernels_us": {k: 1e3 * sum(v) / len(v) for k, v in per.items()},
