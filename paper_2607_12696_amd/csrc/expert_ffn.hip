@@ -186,11 +186,6 @@ __device__ __forceinline__ Plan load_plan(const FfnParams &P)
     return pl;
 }
 
-__device__ __forceinline__ int expert_tokens(const VerifyArgs &a, int u, int U)
-{
-    return u < U ? ld_s(a.offsets + u + 1) - ld_s(a.offsets + u) : a.T;
-}
-
 // ----------------------------------------------------------------------------- cost-weighted split
 //
 // A unit is one macro step of one item.  Units of a token group with more
@@ -227,15 +222,6 @@ struct Split {
     int tok[kMaxTokLds];                // token of each grouped position (if T*k <= kMaxTokLds)
     int wave_tot[kWG];
 };
-
-__device__ __forceinline__ int group_tokens(const FfnParams &P, const Plan &pl, int g)
-{
-    const VerifyArgs &a = P.a;
-    if (!P.plan) return g < pl.U ? a.offsets[g + 1] - a.offsets[g] : a.T;
-    const int u = P.plan[8 + 2 * g], tg = P.plan[8 + 2 * g + 1];
-    const int M = u < pl.U ? a.offsets[u + 1] - a.offsets[u] : a.T;
-    return min(kTokGroup, M - tg * kTokGroup);
-}
 
 // Fills sp.cw and the groups' metadata for the launch (whole workgroup).
 template <int FMT>
@@ -320,47 +306,7 @@ struct ItemDesc {
     bool pair;               // gate/up: the two matrices packed as one pair at wa (wb == wa)
 };
 
-template <bool DOWN>
-__device__ __forceinline__ ItemDesc describe(const FfnParams &P, const Plan &pl, int item)
-{
-    const VerifyArgs &a = P.a;
-    const int gi = item / P.nbands, band = item - gi * P.nbands;
-    int u = gi, tg = 0;
-    if (P.plan) {
-        u = ld_s(P.plan + 8 + 2 * gi);
-        tg = ld_s(P.plan + 8 + 2 * gi + 1);
-    }
-    const int fmt = a.fmt;
-    const size_t kp = (size_t)P.nblocks * kMacroK;
-    const size_t mat = (size_t)P.N * kp * (fmt == FMT_BF16 ? 2 : 1) / (fmt == FMT_MXFP4 ? 2 : 1);
-    const size_t sc = fmt == FMT_FP8 ? (size_t)(P.N / 128) * (P.K / 128) * 4
-                      : fmt == FMT_MXFP4 ? (size_t)P.N * ((P.nblocks + 3) / 4) * 16 : 0;
-    ItemDesc d;
-    d.shared = u >= pl.U;
-    d.e = d.shared ? -1 : ld_s(a.union_ids + u);
-    const int M = expert_tokens(a, u, pl.U);
-    d.p0 = (d.shared ? a.T * a.k : ld_s(a.offsets + u)) + tg * kTokGroup;
-    d.M = min(kTokGroup, M - tg * kTokGroup);
-    d.n0 = band * P.band_rows;
-    const size_t e = d.shared ? 0 : (size_t)ld_s(a.union_ids + u);
-    auto sptr = [&](const void *base) {
-        return base ? static_cast<const void *>(static_cast<const uint8_t *>(base) + e * sc) : nullptr;
-    };
-    d.pair = false;
-    if (!DOWN) {
-        d.pair = d.shared ? a.sh_gu_pair : a.gu_pair;
-        d.wa = (d.shared ? a.sh_gate : a.w_gate) + e * mat * (d.pair ? 2 : 1);
-        d.wb = d.pair ? d.wa : (d.shared ? a.sh_up : a.w_up) + e * mat;
-        d.sa = d.shared ? a.sh_s_gate : sptr(a.s_gate);
-        d.sb = d.shared ? a.sh_s_up : sptr(a.s_up);
-    } else {
-        d.wa = d.wb = (d.shared ? a.sh_down : a.w_down) + e * mat;
-        d.sa = d.sb = d.shared ? a.sh_s_down : sptr(a.s_down);
-    }
-    return d;
-}
-
-// describe() from the schedule in LDS.
+// What a workgroup needs to know about an item, from the schedule in LDS.
 template <bool DOWN>
 __device__ __forceinline__ ItemDesc describe_lds(const FfnParams &P, const Split &sp, int item)
 {
