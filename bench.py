@@ -399,6 +399,67 @@ def shape_sweep(name, Us, T=64, steps=20, warmup=3, n_pool=8):
     return {"shape": name, "d": sh.d, "d_ff": sh.d_ff, "E": sh.E, "k": sh.k, "fmt": sh.fmt, "T": T, "points": out}
 
 
+def token_sweep(name, Ms=(1, 4, 16, 32, 64), U=32, steps=20, warmup=3, n_pool=8):
+    """Tokens per expert: exact-U routing with T = M * U / k gives every one of the U experts exactly
+    M tokens (and the shared expert T).  Per-kernel medians (HIP events around each expert launch)
+    show where the matrix-core work of a step starts to cost on top of the weight stream: the
+    contraction grows with the 16-token blocks of an item, the weight bytes do not."""
+    import torch
+    import synth
+    import paper_2607_12696_amd as moe
+    dev = torch.device("cuda:0")
+    sh = synth.SHAPES[name]
+    raw = synth.layer_weights(sh, seed=0, device=dev)
+    wd = moe.pack_layer(raw)
+    del raw
+    w_b, s_b = synth.expert_bytes(sh.d, sh.d_ff, sh.fmt)
+    n_exp = U + (1 if sh.shared else 0)
+    spans = {"step": (0, 5), "gateup": (1, 2), "fixup": (2, 3), "down": (3, 4), "combine": (4, 5)}
+    out = []
+    for M in Ms:
+        T = M * U // sh.k
+        if T < 1 or T * sh.k != M * U:
+            continue
+        x = synth.activations(T, sh.d, seed=1, device=dev)
+        y = torch.empty_like(x)
+        ws = torch.empty(moe.moe_verify_workspace_size(wd, T, sh.k), dtype=torch.uint8, device=dev)
+        pool = [synth.routes_to_logits(synth.routes_exact_u(T, sh.E, sh.k, U, seed=700 * M + i), sh.E, seed=i,
+                                       device=dev) for i in range(n_pool)]
+        i32 = dict(dtype=torch.int32, device=dev)
+        r = moe.Routing(T, sh.k, sh.E, torch.empty(T, sh.k, **i32), torch.empty(T, sh.k, dtype=torch.float32,
+                                                                                    device=dev),
+                        torch.empty(sh.E, **i32), torch.empty(sh.E, **i32), torch.empty(1, **i32),
+                        torch.empty(sh.E + 1, **i32), torch.empty(T * sh.k, **i32))
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+        for row in evs:
+            for e in row:
+                e.record()
+        for i in range(warmup):
+            moe.moe_route_union(pool[i % n_pool], sh.k, sh.score, out=r)
+            moe.moe_verify_layer(x, wd, r, y=y, workspace=ws)
+        torch.cuda.synchronize()
+        for i in range(steps):
+            evs[i][0].record()
+            moe.moe_route_union(pool[i % n_pool], sh.k, sh.score, out=r)
+            moe.moe_verify_layer_timed(x, wd, r, y, ws, evs[i][1:])
+        torch.cuda.synchronize()
+        med = {k: 1e3 * pct([e[a].elapsed_time(e[b]) for e in evs], 0.5) for k, (a, b) in spans.items()}
+        gu_bytes = n_exp * (2 * w_b + 2 * s_b) / 3
+        dn_bytes = n_exp * (w_b + s_b) / 3
+        pt = {"M": M, "T": T, "step_us": med["step"], "gateup_us": med["gateup"], "fixup_us": med["fixup"],
+              "down_us": med["down"], "combine_us": med["combine"],
+              "gateup_GB_s": gu_bytes / (med["gateup"] * 1e-6) / 1e9,
+              "down_GB_s": dn_bytes / (med["down"] * 1e-6) / 1e9,
+              "step_GB_s": n_exp * (w_b + s_b) / (med["step"] * 1e-6) / 1e9}
+        out.append(pt)
+        log(f"  {name} M={M:3d} (T={T:4d}): step {pt['step_us']:7.1f} us, gate/up {pt['gateup_us']:6.1f} us "
+            f"({pt['gateup_GB_s']:5.0f} GB/s), down {pt['down_us']:6.1f} us ({pt['down_GB_s']:5.0f} GB/s)")
+        del x, y, ws, pool, r
+    del wd
+    torch.cuda.empty_cache()
+    return {"shape": name, "fmt": sh.fmt, "U": U, "points": out}
+
+
 def pct(v, q):
     s = sorted(v)
     return s[min(len(s) - 1, max(0, int(round(q * (len(s) - 1)))))]
@@ -643,11 +704,15 @@ def main():
     ap.add_argument("--cpu-tokens", type=int, default=48)
     ap.add_argument("--no-stack", action="store_true", help="skip the 8-layer draft-tree verification step")
     ap.add_argument("--stack-only", action="store_true", help="only the 8-layer draft-tree verification step")
+    ap.add_argument("--tokens-only", action="store_true", help="only the tokens-per-expert sweep of the three shapes")
     ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 plus a calibration copy")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--pmc-out", default=PMC_SUMMARY, help="where --summarize-pmc writes its summary")
     args = ap.parse_args()
 
+    if args.tokens_only:
+        print(json.dumps([token_sweep(n) for n in ("ds", "qwen", "gpt")]))
+        return 0
     if args.stack_only:
         import torch
         st = Stack()
@@ -741,12 +806,13 @@ def main():
         log("timing the oracle on the host ...")
         cpu, err = cpu_baseline(wl, args.U, args.cpu_tokens)
 
-    variants, others = None, None
+    variants, others, tokens = None, None, None
     if not args.no_sweep:
         del wl
         torch.cuda.empty_cache()
         variants = variant_timing()
         others = [shape_sweep("qwen", [8, 32, 64, 128]), shape_sweep("gpt", [8, 32, 64, 128])]
+        tokens = [token_sweep(n) for n in ("ds", "qwen", "gpt")]
         log(f"GPT-OSS layer T=64: plain {variants['gpt_oss_T64_clustered']['plain_swiglu_us']:.1f} us, "
             f"GPT-OSS expert {variants['gpt_oss_T64_clustered']['gpt_oss_expert_us']:.1f} us; "
             f"grouped routing {variants['ds_routing_T64']['grouped_us']:.1f} us")
@@ -786,6 +852,7 @@ def main():
         "router": router,
         "variants": variants,
         "sweep_other_shapes_T64": others,
+        "sweep_tokens_per_expert_U32": tokens,
     }
     print(json.dumps(out))
     return 0

@@ -553,6 +553,11 @@ FULL_CASES = [
     ("qwen", 64, "scattered", None, [3]),
     ("gpt", 64, "clustered", None, [0, 50]),
     ("gpt", 8, "scattered", None, [2, 7]),
+    # Batch scaling past 64 tokens: experts with more than 64 tokens are split into 64-token groups
+    # (DS: the shared expert serves all 256 tokens in four groups; GPT-OSS: 32 experts x 64 tokens).
+    ("ds", 256, "scattered", None, [0, 255]),
+    ("qwen", 256, "clustered", None, [7, 200]),
+    ("gpt", 512, "exact", 32, [1, 300, 511]),
 ]
 
 
