@@ -16,6 +16,8 @@
 //     (first grouped position of each expert).
 //  3. The passes again, placing each slot at first position of its expert +
 //     slots of that expert in earlier passes and wavefronts + rank.
+// With a single pass (S <= 1024) the matches are kept in registers between
+// steps 1 and 3 and the two scans are done as one.
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -54,6 +56,50 @@ __device__ __forceinline__ void union_block(const int32_t *idx, int S, int E, in
     int nbits = 0;
     while ((1 << nbits) < E) ++nbits;
     const int passes = (S + kUnionThreads - 1) / kUnionThreads;
+
+    if (passes == 1) {
+        // One pass (S <= 1024, every verification batch of up to 64 tokens x 16
+        // slots): the slots' matches stay in registers from counting to
+        // placement, and one scan of (count << 16 | used) gives both prefixes
+        // (count, union size and placed slots are all <= 1024 < 2^16).
+        for (int w = 0; w < kUnionWaves; ++w) wcnt[w][tid] = 0;
+        __syncthreads();
+        const int e = tid < S ? idx[tid] : -1;
+        const bool ok = (unsigned)e < (unsigned)E;
+        int rank, cnt;
+        bool top;
+        wave_match(e, ok, nbits, rank, top, cnt);
+        if (top) wcnt[wave][e] = cnt;
+        __syncthreads();
+        int c = 0;
+        if (tid < E)
+            for (int w = 0; w < kUnionWaves; ++w) c += wcnt[w][tid];
+        int tot = 0;
+        const int ex = block_exclusive_scan((c << 16) | (c > 0 ? 1 : 0), wave_tot, &tot);
+        const int pos = ex & 0xffff, start = ex >> 16, U = tot & 0xffff, placed = tot >> 16;
+        if (tid < E) {
+            counts[tid] = c;
+            if (c > 0) {
+                member_id[pos] = tid;
+                member_start[pos] = start;
+            }
+            // Per-wavefront counts of expert tid -> first position of each wavefront's slots.
+            int run = start;
+            for (int w = 0; w < kUnionWaves; ++w) {
+                const int n = wcnt[w][tid];
+                wcnt[w][tid] = run;
+                run += n;
+            }
+        }
+        __syncthreads();
+        for (int u = tid; u <= E; u += kUnionThreads) {
+            if (u < E) union_ids[u] = u < U ? member_id[u] : -1;
+            offsets[u] = u < U ? member_start[u] : placed;
+        }
+        if (tid == 0) *n_unique = U;
+        if (ok) perm[wcnt[wave][e] + rank] = tid;
+        return;
+    }
 
     // 1. Counts: per-wavefront matches, summed per expert over wavefronts and passes.
     int total = 0;  // thread e: slots routed to expert e
