@@ -16,6 +16,7 @@ verify_tokens(layer, x, idx, w, tokens, threads) -> y float64 [len(tokens), d]
 decode_table(kind)               -> float64 array of every code's value
 weight_at(fmt, w, s, n, c)       -> one decoded weight element
 expert_bytes(fmt, d, d_ff)       -> (weight bytes, scale bytes)
+mx_quantize(v)                   -> (quantised values, block exponents) of the MX activation mode
 """
 from __future__ import annotations
 
@@ -52,7 +53,7 @@ class _Layer(C.Structure):
                 ("sh_s_gate", C.c_void_p), ("sh_s_up", C.c_void_p), ("sh_s_down", C.c_void_p),
                 ("act", C.c_int), ("alpha", C.c_double), ("limit", C.c_double),
                 ("b_gate", C.POINTER(C.c_void_p)), ("b_up", C.POINTER(C.c_void_p)),
-                ("b_down", C.POINTER(C.c_void_p))]
+                ("b_down", C.POINTER(C.c_void_p)), ("act_fmt", C.c_int)]
 
 
 def lib():
@@ -73,6 +74,7 @@ def lib():
             L.orc_weight_at.restype = C.c_double
             L.orc_expert_bytes.argtypes = [C.c_int, C.c_long, C.c_long, C.POINTER(C.c_long),
                                            C.POINTER(C.c_long)]
+            L.orc_mx_quant.argtypes = [p, C.c_int, p]
             _lib = L
     return _lib
 
@@ -168,7 +170,8 @@ def verify_tokens(layer: dict, x, idx, w, tokens=None, threads: int = 1):
     the experts that are needed, plus optional sh_* arrays of the shared expert,
     optional fp32 biases b_gate/b_up [E, d_ff] and b_down [E, d] (same forms) and
     the activation: act 0 (SwiGLU, default) or 1 (GPT-OSS clamped SwiGLU with
-    alpha and limit).
+    alpha and limit), and act_fmt 1 for MX FP8 quantised projection inputs
+    (``mx_quantize``).
     """
     fmt, d, d_ff = int(layer["fmt"]), int(layer["d"]), int(layer["d_ff"])
     wdt = {0: np.uint16, 1: np.uint8, 2: np.uint8}[fmt]
@@ -196,6 +199,7 @@ def verify_tokens(layer: dict, x, idx, w, tokens=None, threads: int = 1):
     lay = _Layer()
     lay.fmt, lay.d, lay.d_ff, lay.n_experts = fmt, d, d_ff, n_exp
     lay.act = int(layer.get("act", 0))
+    lay.act_fmt = int(layer.get("act_fmt", 0))
     lay.alpha = float(layer.get("alpha", 1.702))
     lay.limit = float(layer.get("limit", 7.0))
     for name in ("b_gate", "b_up", "b_down"):
@@ -227,6 +231,18 @@ def verify_tokens(layer: dict, x, idx, w, tokens=None, threads: int = 1):
     if rc:
         raise ValueError(f"orc_verify_tokens rc={rc}")
     return y
+
+
+def mx_quantize(v) -> tuple[np.ndarray, np.ndarray]:
+    """OCP MX FP8 quantisation of one activation row (the optional act_fmt 1 mode):
+    returns the quantised fp64 values and the block exponents E, chunk-major."""
+    a = np.array(v, dtype=np.float64).reshape(-1)
+    K = a.size
+    exps = np.zeros((K + 127) // 128 * 4, np.int32)
+    rc = lib().orc_mx_quant(_ptr(a), K, _ptr(exps))
+    if rc:
+        raise ValueError(f"orc_mx_quant rc={rc}")
+    return a, exps
 
 
 def decode_table(kind: int) -> np.ndarray:

@@ -27,9 +27,13 @@
  *   2 MXFP4       W[n][c] = e2m1(nibble) * 2^(e8m0[n][c/32]-127) (OCP MX; two codes per byte,
  *                 low nibble = even c)
  *
- * Parity status: route, union, decode and the verify layer are pinned by the
- * tests under tests/ (brute force, closed forms, library cross-checks and the
- * paper's 44.04 MB byte count).
+ * Optional MX activation mode (act_fmt 1; not in the paper, an opt-in numeric
+ * mode): the inputs of both projections are quantised to OCP MX FP8 first (see
+ * orc_mx_quant below).
+ *
+ * Parity status: route, union, decode, the MX activation quantiser and the
+ * verify layer are pinned by the tests under tests/ (brute force, closed forms,
+ * library cross-checks and the paper's 44.04 MB byte count).
  */
 #include <math.h>
 #include <stdint.h>
@@ -295,6 +299,66 @@ int orc_union(const int32_t *idx, int T, int k, int E, int32_t *counts, int32_t 
     return 0;
 }
 
+/* ------------------------------------------------------------------ MX activation quantisation */
+
+/* OCP MX FP8 quantisation of one activation row of length K, in place
+ * (optional activation mode act_fmt 1; the paper does not quantise
+ * activations).  The row is taken in 128-element chunks (zero beyond K); block
+ * b = 0..3 of a chunk holds its elements 16b .. 16b+15 and 64+16b .. 64+16b+15,
+ * the 32 elements one lane of the FP8 operand of CDNA4's scaled FP4 x FP8
+ * matrix-core instruction holds.  A block's scale is 2^E with
+ * E = floor(log2(amax)) - 8 (8: exponent of 448, the largest e4m3fn normal),
+ * clamped to [-127, 127], and E = -127 when amax = 0.  Each element becomes the
+ * e4m3fn value nearest to v / 2^E, ties to the even code, magnitudes of 448 and
+ * more saturating to 448, subnormals (multiples of 2^-9) kept; the quantised
+ * value is that e4m3fn value times 2^E.  exps (optional) receives E of every
+ * block, chunk-major: (K + 127) / 128 * 4 entries. */
+static double e4m3_nearest(double a)  /* a >= 0, a < 448 */
+{
+    int p;
+    double step;
+    if (a == 0.0) return 0.0;
+    (void)frexp(a, &p);                  /* a = m 2^p, m in [0.5, 1): floor(log2 a) = p - 1 */
+    step = p - 1 < -6 ? ldexp(1.0, -9)   /* subnormal binade: multiples of 2^-9 */
+                      : ldexp(1.0, p - 1 - 3);
+    return rint(a / step) * step;        /* a / step < 16 is exact; rint rounds half to even */
+}
+
+int orc_mx_quant(double *v, int K, int32_t *exps)
+{
+    int nchunks = (K + 127) / 128, c, b, i;
+    if (!v || K < 0) return 1;
+    for (c = 0; c < nchunks; c++) {
+        for (b = 0; b < 4; b++) {
+            int idx[32];
+            double amax = 0.0, scale;
+            int E;
+            for (i = 0; i < 32; i++) idx[i] = 128 * c + (i < 16 ? 16 * b + i : 64 + 16 * b + (i - 16));
+            for (i = 0; i < 32; i++)
+                if (idx[i] < K && fabs(v[idx[i]]) > amax) amax = fabs(v[idx[i]]);
+            if (amax == 0.0) {
+                E = -127;
+            } else {
+                int p;
+                (void)frexp(amax, &p);
+                E = p - 1 - 8;
+                if (E < -127) E = -127;
+                if (E > 127) E = 127;
+            }
+            if (exps) exps[4 * c + b] = E;
+            scale = ldexp(1.0, E);
+            for (i = 0; i < 32; i++) {
+                double a, q;
+                if (idx[i] >= K) continue;
+                a = fabs(v[idx[i]]) / scale;
+                q = a >= 448.0 ? 448.0 : e4m3_nearest(a);
+                v[idx[i]] = (v[idx[i]] < 0.0 ? -q : q) * scale;
+            }
+        }
+    }
+    return 0;
+}
+
 /* ------------------------------------------------------------------ verify layer */
 
 typedef struct {
@@ -312,16 +376,18 @@ typedef struct {
     const void *const *b_gate; /* fp32 biases per routed expert ([d_ff], [d_ff], [d]); NULL array = none */
     const void *const *b_up;
     const void *const *b_down;
+    int act_fmt;               /* 0: exact bf16 inputs; 1: x and h quantised by orc_mx_quant */
 } orc_layer;
 
 /* One expert FFN.  g_n = sum_c x_c W_gate[n][c] + bg_n, v_n = sum_c x_c W_up[n][c] + bu_n
  * (biases NULL: zero).  act 0: h_n = silu(g_n) * v_n.  act 1 (GPT-OSS): g clamped
  * from above at `limit`, v clamped to [-limit, limit], h_n = g sigmoid(alpha g) (v + 1).
+ * act_fmt 1: h quantised by orc_mx_quant (x is quantised by the caller).
  * o[m] = sum_n h_n W_down[m][n] + bd_m. */
 static void swiglu_expert(int fmt, int d, int d_ff, const void *wg, const void *wu, const void *wd,
                           const void *sg, const void *su, const void *sd, int act, double alpha,
-                          double limit, const float *bg, const float *bu, const float *bd, const double *x,
-                          double *h, double *o)
+                          double limit, const float *bg, const float *bu, const float *bd, int act_fmt,
+                          const double *x, double *h, double *o)
 {
     int n, c, m;
     for (n = 0; n < d_ff; n++) {
@@ -341,6 +407,7 @@ static void swiglu_expert(int fmt, int d, int d_ff, const void *wg, const void *
             h[n] = g / (1.0 + exp(-alpha * g)) * (v + 1.0);
         }
     }
+    if (act_fmt == 1) orc_mx_quant(h, d_ff, NULL);
     for (m = 0; m < d; m++) {
         double acc = 0.0;
         for (n = 0; n < d_ff; n++) acc += h[n] * weight_at(fmt, wd, sd, d, d_ff, m, n);
@@ -381,6 +448,7 @@ int orc_verify_tokens(const orc_layer *L, const uint16_t *x, int T, int k, const
         double *h = (double *)malloc(sizeof(double) * (size_t)d_ff);
         if (!xt || !h) { bad = 1; free(xt); free(h); continue; }
         for (c = 0; c < d; c++) xt[c] = orc_bf16(x[(size_t)t * d + c]);
+        if (L->act_fmt == 1) orc_mx_quant(xt, d, NULL);
         if (j < k) {
             int e = idx[(size_t)t * k + j];
             swiglu_expert(L->fmt, d, d_ff, L->gate[e], L->up[e], L->down[e],
@@ -388,11 +456,12 @@ int orc_verify_tokens(const orc_layer *L, const uint16_t *x, int T, int k, const
                           L->s_down ? L->s_down[e] : NULL, L->act, L->alpha, L->limit,
                           L->b_gate ? (const float *)L->b_gate[e] : NULL,
                           L->b_up ? (const float *)L->b_up[e] : NULL,
-                          L->b_down ? (const float *)L->b_down[e] : NULL, xt, h, o + (size_t)q * d);
+                          L->b_down ? (const float *)L->b_down[e] : NULL, L->act_fmt, xt, h,
+                          o + (size_t)q * d);
         } else {
             swiglu_expert(L->fmt, d, d_ff, L->sh_gate, L->sh_up, L->sh_down, L->sh_s_gate,
-                          L->sh_s_up, L->sh_s_down, L->act, L->alpha, L->limit, NULL, NULL, NULL, xt, h,
-                          o + (size_t)q * d);
+                          L->sh_s_up, L->sh_s_down, L->act, L->alpha, L->limit, NULL, NULL, NULL, L->act_fmt,
+                          xt, h, o + (size_t)q * d);
         }
         free(xt);
         free(h);
