@@ -320,12 +320,12 @@ def variant_timing(T=64, steps=30, warmup=3, n_pool=8):
         torch.cuda.synchronize()
         return a.elapsed_time(b) * 1e3 / steps
 
-    t_plain, t_oai = steps_us(plain), steps_us(oai)
+    t_plain, t_oai, t_mx = steps_us(plain), steps_us(oai), steps_us(dict(plain, act_fmt=moe.MOE_ACTQ_MXFP8))
     per_expert = sum(synth.expert_bytes(sh.d, sh.d_ff, sh.fmt))  # weights + e8m0 scales, unpadded
     B = U * per_expert + 4 * T * sh.d + 4 * T * sh.E
     out = {"gpt_oss_T64_clustered": {"unique_experts_median": U, "plain_swiglu_us": t_plain,
                                      "gpt_oss_expert_us": t_oai, "GB_s_gpt_oss_expert": B / (t_oai * 1e-6) / 1e9,
-                                     "alg_bytes": B}}
+                                     "mx_fp8_activations_us": t_mx, "alg_bytes": B}}
     del plain, oai, ws
     torch.cuda.empty_cache()
 
@@ -362,16 +362,17 @@ def variant_timing(T=64, steps=30, warmup=3, n_pool=8):
     return out
 
 
-def shape_sweep(name, Us, T=64, steps=20, warmup=3, n_pool=8):
+def shape_sweep(name, Us, T=64, steps=20, warmup=3, n_pool=8, act_fmt=0):
     """Step latency and algorithmic GB/s vs U for another model shape (exact-U routing, a different
-    expert set every step, so weights are read cold: the sets rotate over all experts of the layer)."""
+    expert set every step, so weights are read cold: the sets rotate over all experts of the layer).
+    act_fmt 1: MX FP8 activations on the scaled FP4 x FP8 matrix-core instruction (MXFP4 only)."""
     import torch
     import synth
     import paper_2607_12696_amd as moe
     dev = torch.device("cuda:0")
     sh = synth.SHAPES[name]
     raw = synth.layer_weights(sh, seed=0, device=dev)
-    wd = moe.pack_layer(raw)
+    wd = dict(moe.pack_layer(raw), act_fmt=act_fmt)
     del raw
     x = synth.activations(T, sh.d, seed=1, device=dev)
     y = torch.empty_like(x)
@@ -393,13 +394,14 @@ def shape_sweep(name, Us, T=64, steps=20, warmup=3, n_pool=8):
         us = a.elapsed_time(b) * 1e3 / steps
         B = (U + (1 if sh.shared else 0)) * per_expert + 4 * T * sh.d + 4 * T * sh.E
         out.append({"U": U, "step_us": us, "GB_s": B / (us * 1e-6) / 1e9, "frac_of_8TBs": B / (us * 1e-6) / 8e12})
-        log(f"  {name} U={U:4d}: step {us:8.1f} us  {out[-1]['GB_s']:7.0f} GB/s")
+        log(f"  {name}{' MX act' if act_fmt else ''} U={U:4d}: step {us:8.1f} us  {out[-1]['GB_s']:7.0f} GB/s")
     del wd, ws
     torch.cuda.empty_cache()
-    return {"shape": name, "d": sh.d, "d_ff": sh.d_ff, "E": sh.E, "k": sh.k, "fmt": sh.fmt, "T": T, "points": out}
+    return {"shape": name, "d": sh.d, "d_ff": sh.d_ff, "E": sh.E, "k": sh.k, "fmt": sh.fmt, "act_fmt": act_fmt,
+            "T": T, "points": out}
 
 
-def token_sweep(name, Ms=(1, 4, 16, 32, 64), U=32, steps=20, warmup=3, n_pool=8):
+def token_sweep(name, Ms=(1, 4, 16, 32, 64), U=32, steps=20, warmup=3, n_pool=8, act_fmt=0):
     """Tokens per expert: exact-U routing with T = M * U / k gives every one of the U experts exactly
     M tokens (and the shared expert T).  Per-kernel medians (HIP events around each expert launch)
     show where the matrix-core work of a step starts to cost on top of the weight stream: the
@@ -410,7 +412,7 @@ def token_sweep(name, Ms=(1, 4, 16, 32, 64), U=32, steps=20, warmup=3, n_pool=8)
     dev = torch.device("cuda:0")
     sh = synth.SHAPES[name]
     raw = synth.layer_weights(sh, seed=0, device=dev)
-    wd = moe.pack_layer(raw)
+    wd = dict(moe.pack_layer(raw), act_fmt=act_fmt)
     del raw
     w_b, s_b = synth.expert_bytes(sh.d, sh.d_ff, sh.fmt)
     n_exp = U + (1 if sh.shared else 0)
@@ -452,12 +454,12 @@ def token_sweep(name, Ms=(1, 4, 16, 32, 64), U=32, steps=20, warmup=3, n_pool=8)
               "down_GB_s": dn_bytes / (med["down"] * 1e-6) / 1e9,
               "step_GB_s": n_exp * (w_b + s_b) / (med["step"] * 1e-6) / 1e9}
         out.append(pt)
-        log(f"  {name} M={M:3d} (T={T:4d}): step {pt['step_us']:7.1f} us, gate/up {pt['gateup_us']:6.1f} us "
+        log(f"  {name}{' MX act' if act_fmt else ''} M={M:3d} (T={T:4d}): step {pt['step_us']:7.1f} us, gate/up {pt['gateup_us']:6.1f} us "
             f"({pt['gateup_GB_s']:5.0f} GB/s), down {pt['down_us']:6.1f} us ({pt['down_GB_s']:5.0f} GB/s)")
         del x, y, ws, pool, r
     del wd
     torch.cuda.empty_cache()
-    return {"shape": name, "fmt": sh.fmt, "U": U, "points": out}
+    return {"shape": name, "fmt": sh.fmt, "act_fmt": act_fmt, "U": U, "points": out}
 
 
 def pct(v, q):
@@ -705,13 +707,18 @@ def main():
     ap.add_argument("--no-stack", action="store_true", help="skip the 8-layer draft-tree verification step")
     ap.add_argument("--stack-only", action="store_true", help="only the 8-layer draft-tree verification step")
     ap.add_argument("--tokens-only", action="store_true", help="only the tokens-per-expert sweep of the three shapes")
+    ap.add_argument("--mx-only", action="store_true", help="only the GPT-OSS shape with bf16 and MX FP8 activations")
     ap.add_argument("--profile", action="store_true", help="short run for rocprofv3 plus a calibration copy")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--pmc-out", default=PMC_SUMMARY, help="where --summarize-pmc writes its summary")
     args = ap.parse_args()
 
     if args.tokens_only:
-        print(json.dumps([token_sweep(n) for n in ("ds", "qwen", "gpt")]))
+        print(json.dumps([token_sweep(n) for n in ("ds", "qwen", "gpt")] + [token_sweep("gpt", act_fmt=1)]))
+        return 0
+    if args.mx_only:
+        print(json.dumps([token_sweep("gpt"), token_sweep("gpt", act_fmt=1), shape_sweep("gpt", [8, 32, 64, 128]),
+                          shape_sweep("gpt", [8, 32, 64, 128], act_fmt=1)]))
         return 0
     if args.stack_only:
         import torch
@@ -811,8 +818,9 @@ def main():
         del wl
         torch.cuda.empty_cache()
         variants = variant_timing()
-        others = [shape_sweep("qwen", [8, 32, 64, 128]), shape_sweep("gpt", [8, 32, 64, 128])]
-        tokens = [token_sweep(n) for n in ("ds", "qwen", "gpt")]
+        others = [shape_sweep("qwen", [8, 32, 64, 128]), shape_sweep("gpt", [8, 32, 64, 128]),
+                  shape_sweep("gpt", [8, 32, 64, 128], act_fmt=1)]
+        tokens = [token_sweep(n) for n in ("ds", "qwen", "gpt")] + [token_sweep("gpt", act_fmt=1)]
         log(f"GPT-OSS layer T=64: plain {variants['gpt_oss_T64_clustered']['plain_swiglu_us']:.1f} us, "
             f"GPT-OSS expert {variants['gpt_oss_T64_clustered']['gpt_oss_expert_us']:.1f} us; "
             f"grouped routing {variants['ds_routing_T64']['grouped_us']:.1f} us")

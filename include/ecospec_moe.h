@@ -80,6 +80,22 @@ typedef enum {
     MOE_ACT_SWIGLU_OAI = 1
 } moe_act_t;
 
+/* Precision of the projections' inputs (x for gate/up, the activation rows h
+ * for down).  MOE_ACTQ_BF16: x as given, h rounded to bf16, exact products.
+ * MOE_ACTQ_MXFP8 (opt-in; MOE_W_MXFP4 weights only): both inputs quantised to
+ * OCP MX FP8 and multiplied on the scaled FP4 x FP8 matrix-core instruction.
+ * A row is taken in blocks of 32 consecutive elements (the OCP MX block, and
+ * the K block the instruction's scales apply to).  A block's scale is 2^E,
+ * E = floor(log2(max |v|)) - 8 clamped to [-127, 127] (-127 for an all-zero
+ * block); each element becomes the e4m3fn value nearest to v / 2^E, ties to
+ * the even code, magnitudes from 448 up saturating to 448.  The paper keeps
+ * activations exact; this mode trades a few percent of y (relative to
+ * max |y|) for matrix-core work without weight decoding. */
+typedef enum {
+    MOE_ACTQ_BF16 = 0,
+    MOE_ACTQ_MXFP8 = 1
+} moe_actq_t;
+
 /* Weights of one MoE layer, in the streaming layout written by
  * moe_pack_weights; all pointers are device pointers.  The scale pointers
  * are NULL for MOE_W_BF16.  The sh_* fields describe one always-on shared
@@ -90,8 +106,10 @@ typedef enum {
  * [E][d_ff] and b_down [E][d] are optional fp32 biases of the routed experts
  * (NULL: none; 16-byte aligned): g and u get b_gate, b_up before the
  * activation and each expert output gets b_down before the gate weight.
- * The shared expert takes the activation but no biases.  A zero-initialised
- * struct tail (act 0, NULL biases) is the plain SwiGLU layer.
+ * The shared expert takes the activation but no biases.  act_fmt selects the
+ * precision of the projection inputs (moe_actq_t; MOE_ACTQ_MXFP8 needs
+ * MOE_W_MXFP4, else MOE_ERR_UNSUPPORTED).  A zero-initialised struct tail
+ * (act 0, NULL biases, act_fmt 0) is the plain SwiGLU layer.
  * w_up == NULL means W_gate and W_up were packed together by
  * moe_pack_gate_up into w_gate (likewise sh_up == NULL with sh_gate set);
  * s_up (sh_s_up) still points to the up scales.
@@ -108,6 +126,7 @@ typedef struct {
     int act; /* moe_act_t */
     float alpha, limit;
     const float *b_gate, *b_up, *b_down;
+    int act_fmt; /* moe_actq_t */
 } moe_weights_t;
 
 /* Routing of T tokens as produced by moe_route_topk + moe_expert_union

@@ -235,10 +235,10 @@ def verify_tokens(layer: dict, x, idx, w, tokens=None, threads: int = 1):
 
 def mx_quantize(v) -> tuple[np.ndarray, np.ndarray]:
     """OCP MX FP8 quantisation of one activation row (the optional act_fmt 1 mode):
-    returns the quantised fp64 values and the block exponents E, chunk-major."""
+    returns the quantised fp64 values and the exponent E of every block of 32."""
     a = np.array(v, dtype=np.float64).reshape(-1)
     K = a.size
-    exps = np.zeros((K + 127) // 128 * 4, np.int32)
+    exps = np.zeros((K + 31) // 32, np.int32)
     rc = lib().orc_mx_quant(_ptr(a), K, _ptr(exps))
     if rc:
         raise ValueError(f"orc_mx_quant rc={rc}")

@@ -303,16 +303,15 @@ int orc_union(const int32_t *idx, int T, int k, int E, int32_t *counts, int32_t 
 
 /* OCP MX FP8 quantisation of one activation row of length K, in place
  * (optional activation mode act_fmt 1; the paper does not quantise
- * activations).  The row is taken in 128-element chunks (zero beyond K); block
- * b = 0..3 of a chunk holds its elements 16b .. 16b+15 and 64+16b .. 64+16b+15,
- * the 32 elements one lane of the FP8 operand of CDNA4's scaled FP4 x FP8
- * matrix-core instruction holds.  A block's scale is 2^E with
- * E = floor(log2(amax)) - 8 (8: exponent of 448, the largest e4m3fn normal),
- * clamped to [-127, 127], and E = -127 when amax = 0.  Each element becomes the
- * e4m3fn value nearest to v / 2^E, ties to the even code, magnitudes of 448 and
- * more saturating to 448, subnormals (multiples of 2^-9) kept; the quantised
- * value is that e4m3fn value times 2^E.  exps (optional) receives E of every
- * block, chunk-major: (K + 127) / 128 * 4 entries. */
+ * activations).  The row is split into blocks of 32 consecutive elements (the
+ * last one zero-padded), the OCP MX block, which is also the K block the
+ * scales of CDNA4's scaled FP4 x FP8 matrix-core instruction apply to.  A
+ * block's scale is 2^E with E = floor(log2(amax)) - 8 (8: exponent of 448, the
+ * largest e4m3fn normal), clamped to [-127, 127], and E = -127 when amax = 0.
+ * Each element becomes the e4m3fn value nearest to v / 2^E, ties to the even
+ * code, magnitudes of 448 and more saturating to 448, subnormals (multiples of
+ * 2^-9) kept; the quantised value is that e4m3fn value times 2^E.  exps
+ * (optional) receives E of every block: (K + 31) / 32 entries. */
 static double e4m3_nearest(double a)  /* a >= 0, a < 448 */
 {
     int p;
@@ -326,34 +325,27 @@ static double e4m3_nearest(double a)  /* a >= 0, a < 448 */
 
 int orc_mx_quant(double *v, int K, int32_t *exps)
 {
-    int nchunks = (K + 127) / 128, c, b, i;
+    int nblocks = (K + 31) / 32, b, i;
     if (!v || K < 0) return 1;
-    for (c = 0; c < nchunks; c++) {
-        for (b = 0; b < 4; b++) {
-            int idx[32];
-            double amax = 0.0, scale;
-            int E;
-            for (i = 0; i < 32; i++) idx[i] = 128 * c + (i < 16 ? 16 * b + i : 64 + 16 * b + (i - 16));
-            for (i = 0; i < 32; i++)
-                if (idx[i] < K && fabs(v[idx[i]]) > amax) amax = fabs(v[idx[i]]);
-            if (amax == 0.0) {
-                E = -127;
-            } else {
-                int p;
-                (void)frexp(amax, &p);
-                E = p - 1 - 8;
-                if (E < -127) E = -127;
-                if (E > 127) E = 127;
-            }
-            if (exps) exps[4 * c + b] = E;
-            scale = ldexp(1.0, E);
-            for (i = 0; i < 32; i++) {
-                double a, q;
-                if (idx[i] >= K) continue;
-                a = fabs(v[idx[i]]) / scale;
-                q = a >= 448.0 ? 448.0 : e4m3_nearest(a);
-                v[idx[i]] = (v[idx[i]] < 0.0 ? -q : q) * scale;
-            }
+    for (b = 0; b < nblocks; b++) {
+        int lo = 32 * b, hi = 32 * b + 32 < K ? 32 * b + 32 : K, E;
+        double amax = 0.0, scale;
+        for (i = lo; i < hi; i++)
+            if (fabs(v[i]) > amax) amax = fabs(v[i]);
+        if (amax == 0.0) {
+            E = -127;
+        } else {
+            int p;
+            (void)frexp(amax, &p);
+            E = p - 1 - 8;
+            if (E < -127) E = -127;
+            if (E > 127) E = 127;
+        }
+        if (exps) exps[b] = E;
+        scale = ldexp(1.0, E);
+        for (i = lo; i < hi; i++) {
+            double a = fabs(v[i]) / scale, q = a >= 448.0 ? 448.0 : e4m3_nearest(a);
+            v[i] = (v[i] < 0.0 ? -q : q) * scale;
         }
     }
     return 0;

@@ -35,6 +35,7 @@ MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
 MOE_W_BF16, MOE_W_FP8_E4M3_B128, MOE_W_MXFP4 = 0, 1, 2
 MOE_SEL_COST_RATIO, MOE_SEL_CONFIDENCE, MOE_SEL_GLOBAL_COST, MOE_SEL_COST_DIFF = 0, 1, 2, 3
 MOE_ACT_SWIGLU, MOE_ACT_SWIGLU_OAI = 0, 1
+MOE_ACTQ_BF16, MOE_ACTQ_MXFP8 = 0, 1
 
 EXPORTED = ("moe_route_topk", "moe_route_union", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
             "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_pack_gate_up", "moe_select_tree",
@@ -52,7 +53,7 @@ class moe_weights_t(C.Structure):
         (n, C.c_void_p) for n in ("w_gate", "w_up", "w_down", "s_gate", "s_up", "s_down", "sh_gate", "sh_up",
                                   "sh_down", "sh_s_gate", "sh_s_up", "sh_s_down")] + [
         ("act", C.c_int), ("alpha", C.c_float), ("limit", C.c_float),
-        ("b_gate", C.c_void_p), ("b_up", C.c_void_p), ("b_down", C.c_void_p)]
+        ("b_gate", C.c_void_p), ("b_up", C.c_void_p), ("b_down", C.c_void_p), ("act_fmt", C.c_int)]
 
 
 class moe_routing_t(C.Structure):
@@ -302,7 +303,7 @@ def moe_pack_gate_up(fmt: int, w_gate, w_up, s_gate=None, s_up=None):
 def pack_layer(layer: dict, pair: bool = True) -> dict:
     """A layer dict (interchange layout, device tensors) with every matrix packed; with `pair`,
     W_gate and W_up as one pair (moe_pack_gate_up; the dict then has no "up" / "sh_up" entry)."""
-    out = {k: layer[k] for k in ("fmt", "d", "d_ff", "act", "alpha", "limit", "b_gate", "b_up", "b_down")
+    out = {k: layer[k] for k in ("fmt", "d", "d_ff", "act", "alpha", "limit", "b_gate", "b_up", "b_down", "act_fmt")
            if k in layer}
     out["E"] = int(layer.get("E", layer["gate"].shape[0]))
     fmt = int(layer["fmt"])
@@ -329,10 +330,11 @@ def pack_layer(layer: dict, pair: bool = True) -> dict:
 
 def weights_struct(w: dict) -> moe_weights_t:
     """moe_weights_t for a layer dict (keys fmt, d, d_ff, E, gate, up, down, optional s_*, sh_*,
-    fp32 biases b_gate / b_up [E, d_ff] and b_down [E, d], and act / alpha / limit)."""
+    fp32 biases b_gate / b_up [E, d_ff] and b_down [E, d], act / alpha / limit, and act_fmt)."""
     s = moe_weights_t()
     torch = _torch()
     s.act = int(w.get("act", MOE_ACT_SWIGLU))
+    s.act_fmt = int(w.get("act_fmt", MOE_ACTQ_BF16))
     s.alpha, s.limit = float(w.get("alpha", 1.702)), float(w.get("limit", 7.0))
     for name in ("b_gate", "b_up", "b_down"):
         b = w.get(name)

@@ -58,6 +58,8 @@ moe_status_t check_weights(const moe_weights_t *w)
     const void *bs[] = {w->b_gate, w->b_up, w->b_down};
     for (const void *p : bs)
         if (p && !aligned(p, 16)) return MOE_ERR_INVALID_ARG;
+    if (w->act_fmt != MOE_ACTQ_BF16 && w->act_fmt != MOE_ACTQ_MXFP8) return MOE_ERR_INVALID_ARG;
+    if (w->act_fmt == MOE_ACTQ_MXFP8 && w->fmt != MOE_W_MXFP4) return MOE_ERR_UNSUPPORTED;
     return MOE_OK;
 }
 
@@ -163,7 +165,8 @@ moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, siz
     const moe_status_t st = check_weights(w);
     if (st != MOE_OK) return st;
     if (T < 1 || k < 1 || k > kMaxK || k > w->E || (long)T * k > kMaxSlots) return MOE_ERR_INVALID_ARG;
-    const ecospec::VerifyWorkspace ws = ecospec::verify_workspace(w->d, w->d_ff, T, k, w->sh_gate != nullptr);
+    const ecospec::VerifyWorkspace ws =
+        ecospec::verify_workspace(w->d, w->d_ff, T, k, w->sh_gate != nullptr, w->act_fmt == MOE_ACTQ_MXFP8);
     if (ws.plan_cap > ecospec::kMaxGroups) return MOE_ERR_UNSUPPORTED;
     *bytes = ws.total;
     return MOE_OK;
@@ -181,7 +184,8 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     if (!r->topk_w || !r->union_ids || !r->n_unique || !r->offsets || !r->perm) return MOE_ERR_INVALID_ARG;
     if (w->b_down && !r->topk_idx) return MOE_ERR_INVALID_ARG;  // the down bias follows each slot's expert
     const bool shared = w->sh_gate != nullptr;
-    const ecospec::VerifyWorkspace ws = ecospec::verify_workspace(w->d, w->d_ff, r->T, r->k, shared);
+    const ecospec::VerifyWorkspace ws =
+        ecospec::verify_workspace(w->d, w->d_ff, r->T, r->k, shared, w->act_fmt == MOE_ACTQ_MXFP8);
     if (ws.plan_cap > ecospec::kMaxGroups) return MOE_ERR_UNSUPPORTED;
     if (workspace_bytes < ws.total) return MOE_ERR_WORKSPACE;
     const long rows = (long)r->T * r->k + (shared ? r->T : 0);
@@ -216,6 +220,7 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     a.b_gate = w->b_gate;
     a.b_up = w->b_up;
     a.b_down = w->b_down;
+    a.act_fmt = w->act_fmt;
     a.union_ids = r->union_ids;
     a.n_unique = r->n_unique;
     a.offsets = r->offsets;

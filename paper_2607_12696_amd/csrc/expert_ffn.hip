@@ -43,6 +43,17 @@
 // Outputs: gate/up writes the bf16 SwiGLU rows H at grouped positions; down
 // writes one fp32 row per (token, slot); combine applies the gate weights and
 // sums a token's k slots, then the shared expert, in a fixed order.
+//
+// MX activation mode (opt-in, MXFP4 weights): x and H are quantised to OCP MX
+// FP8 (x by a small pre-pass, H in the gate/up epilogue) and both projections
+// run on v_mfma_scale_f32_16x16x128_f8f6f4 (FP4 weights x FP8 activations,
+// e8m0 scales of both applied by the instruction).  A lane of that
+// instruction's FP4 operand holds 32 consecutive K of one row, exactly the
+// packed MXFP4 fragment and its scale.  The scales of both operands apply to
+// the same 32-wide K blocks (lane group g's scale to K 32g..32g+31 of the
+// 128), the plain OCP MX blocks; the data of the FP8 operand's lane group g is
+// K 16g..16g+15 and 64+16g..64+16g+15, so activation rows are stored in that
+// order (each 128-element chunk as four 32-byte lane runs).
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -124,6 +135,40 @@ __device__ __forceinline__ float e8m0_to_f32(uint32_t code)
     b = code == 0u ? 0x00400000u : b;
     b = code == 255u ? 0x7fc00000u : b;
     return __uint_as_float(b);
+}
+
+// MX FP8 activation quantisation.  A block's scale exponent from its largest
+// magnitude: E = floor(log2(amax)) - 8 (448, the largest e4m3fn value, is
+// 1.75 * 2^8), -127 for amax = 0 or below the fp32 normal range; E <= 119.
+__device__ __forceinline__ int mx_exponent(float amax)
+{
+    const int ef = (int)((__float_as_uint(amax) >> 23) & 0xffu);
+    return ef == 0 ? -127 : max(ef - 135, -127);
+}
+
+// 2^-E for a block exponent E in [-127, 119].
+__device__ __forceinline__ float mx_inv_scale(int E) { return __uint_as_float((uint32_t)(127 - E) << 23); }
+
+// e4m3fn code of v (already divided by the block scale): nearest value, ties
+// to the even code, magnitudes of 448 and above saturating to 448 (code
+// 0x7e), subnormals (multiples of 2^-9) kept, NaN to 0x7f.
+__device__ __forceinline__ uint32_t e4m3_code(float v)
+{
+    const uint32_t bits = __float_as_uint(v), sign = (bits >> 24) & 0x80u;
+    const float a = __uint_as_float(bits & 0x7fffffffu);
+    uint32_t code;
+    if (a != a) {
+        code = 0x7fu;
+    } else if (!(a < 448.f)) {
+        code = 0x7eu;
+    } else if (a < 0.015625f) {
+        code = (uint32_t)__builtin_rintf(a * 512.f);  // 0 .. 8; 8 is 2^-6, the code of the first normal
+    } else {
+        const uint32_t b = __float_as_uint(a), mant = b & 0x7fffffu;
+        const uint32_t r = (mant + 0x7ffffu + ((mant >> 20) & 1u)) >> 20;  // 3-bit mantissa, ties to even
+        code = (((b >> 23) - 120u) << 3) + r;  // r = 8 carries into the exponent field
+    }
+    return sign | code;
 }
 
 // bf16 A operand of sub-step s (the lane's weights 8s .. 8s+7 of a block;
@@ -388,12 +433,51 @@ __device__ __forceinline__ float activate(const VerifyArgs &a, float g, float u)
 // Finishes a wavefront's (tile 0, tile 1) accumulators of an item: gate/up ->
 // bf16 SwiGLU rows of H, down -> fp32 rows of O, both at grouped positions.  Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for
 // token column col of each 16-token block.
-template <bool DOWN>
+//
+// MX activation mode, gate/up: the SwiGLU rows go to the down launch as MX
+// FP8.  A band (128 rows) is one 128-element chunk of an H row; wavefront w's
+// 16 rows are half of the 32-row block w / 2, the other half being wavefront
+// w ^ 1's, so the two exchange their per-token maxima through LDS (every
+// wavefront of the workgroup takes part, also those past the last row, which
+// write the zero padding the down launch reads).  Row 16w + j of the chunk is
+// stored at byte 32 (w % 4) + 16 (w / 4) + j, the FP8 operand's lane order.
+template <bool DOWN, bool MXA>
 __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &d, int wave,
                                             const f32x4 (&acc)[2][kMB], const ItemBias &bias)
 {
     const VerifyArgs &a = P.a;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
+    if constexpr (!DOWN && MXA) {
+        __shared__ float red[kWG][kMB][16];
+        const bool rows_ok = tile_row<false>(d, wave, 0) < P.N;  // N % 32 == 0: a tile is all in or all out
+        float h[kMB][4];
+#pragma unroll
+        for (int mb = 0; mb < kMB; ++mb) {
+            const f32x4 g = acc[0][mb] + bias.g, v = acc[1][mb] + bias.u;
+            const bool live = rows_ok && mb * 16 + col < d.M;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) h[mb][i] = live ? activate(a, g[i], v[i]) : 0.f;
+            float m = fmaxf(fmaxf(fabsf(h[mb][0]), fabsf(h[mb][1])), fmaxf(fabsf(h[mb][2]), fabsf(h[mb][3])));
+            m = fmaxf(m, __shfl_xor(m, 16, kWave));
+            m = fmaxf(m, __shfl_xor(m, 32, kWave));
+            if (grp == 0) red[wave][mb][col] = m;
+        }
+        __syncthreads();
+        const int kp = P.nbands * P.band_rows;  // padded d_ff
+#pragma unroll
+        for (int mb = 0; mb < kMB; ++mb) {
+            const int r = mb * 16 + col;
+            if (r >= d.M) continue;
+            const int E = mx_exponent(fmaxf(red[wave][mb][col], red[wave ^ 1][mb][col]));
+            const float inv = mx_inv_scale(E);
+            const uint32_t q = e4m3_code(h[mb][0] * inv) | (e4m3_code(h[mb][1] * inv) << 8) |
+                               (e4m3_code(h[mb][2] * inv) << 16) | (e4m3_code(h[mb][3] * inv) << 24);
+            const size_t p = (size_t)(d.p0 + r);
+            *reinterpret_cast<uint32_t *>(a.hq + p * kp + d.n0 + 32 * (wave & 3) + 16 * (wave >> 2) + 4 * grp) = q;
+            if ((wave & 1) == 0 && grp == 0) a.hs[p * (kp / 32) + d.n0 / 32 + wave / 2] = (uint8_t)(E + 127);
+        }
+        return;
+    }
     if (tile_row<DOWN>(d, wave, 0) >= P.N) return;  // rows past the last band
 #pragma unroll
     for (int mb = 0; mb < kMB; ++mb) {
@@ -438,11 +522,12 @@ struct Source {
     uint32_t kstride;           // bytes from one 128-wide block of a tile to the next
     uint32_t q0, q1;            // scale offsets at step 0
     uint32_t boff[kBPass];      // lane offsets of this thread's activation rows at step 0 (kOff: no token)
+    uint32_t soff[kBPass];      // MX activations: offsets of the rows' block scales at step 0
     long ib, ie;                // the item's units [ib, ie)
     int item;
 };
 
-template <int FMT, bool DOWN>
+template <int FMT, bool DOWN, bool MXA>
 __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, const Split &sp, int item)
 {
     constexpr int NV = Fmt<FMT>::kVecs;
@@ -491,7 +576,8 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
     // 4*wave + q, q = lane / 16.  Their source rows (token of a grouped
     // position for gate/up, the grouped position itself for down) are read
     // through the scalar unit.
-    const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
+    // MX activations: rows of nblocks * 128 e4m3fn codes and nblocks * 4 scales.
+    const uint32_t brow_bytes = MXA ? (uint32_t)nblocks * kMacroK : (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
     const int q = lane >> 4;
 #pragma unroll
     for (int i = 0; i < kBPass; ++i) {
@@ -510,6 +596,7 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
             row = q == qq ? v : row;
         }
         src.boff[i] = row >= 0 ? (uint32_t)row * brow_bytes + (uint32_t)bc * 16u : kOff;
+        src.soff[i] = row >= 0 ? (uint32_t)row * (uint32_t)nblocks * 4u + (uint32_t)(bc & 1) * 4u : kOff;
     }
 }
 
@@ -557,6 +644,51 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
         } else {
             acc[0][mb] = part[0][mb];
             acc[1][mb] = part[1][mb];
+        }
+    }
+}
+
+// MX activation mode: LDS geometry of one step's FP8 activation tile (64
+// tokens x 256 codes, rows padded by 16 bytes) followed by its scales (8 per
+// token: 4 blocks of each of the step's two 128-wide chunks).
+constexpr int kRowQ = 256 + 16;
+constexpr int kScaleQ = kMB * 16 * kRowQ;
+
+typedef __attribute__((ext_vector_type(8))) int i32x8;
+
+// One MXFP4 macro step of a wavefront with MX FP8 activations: per 128-wide
+// block, one v_mfma_scale_f32_16x16x128_f8f6f4 per tile and token block.  The
+// A operand is the lane's packed FP4 fragment (K 32grp..32grp+31 of its row)
+// with its e8m0 code; the B operand is token col's codes of K 16grp..16grp+15
+// and 64+16grp..64+16grp+15 (stored contiguously) with the scale of block grp
+// (K 32grp..32grp+31), which the instruction applies to that K block.
+template <int NMB>
+__device__ __forceinline__ void contract_mx(const WFrag<FMT_MXFP4> (&wv)[2], const uint8_t *buf,
+                                            f32x4 (&acc)[2][kMB])
+{
+    const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
+    const uint8_t *bp = buf + col * kRowQ + grp * 32;
+    const uint8_t *sp = buf + kScaleQ + col * 8 + grp;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        i32x8 bv[NMB];
+        int sb[NMB];
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) {
+            const u32x4 lo = *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kRowQ + b * 128);
+            const u32x4 hi = *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kRowQ + b * 128 + 16);
+            bv[mb] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+            sb[mb] = sp[mb * 16 * 8 + b * 4];
+        }
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const u32x4 w = wv[t].v[b];
+            const i32x8 av = i32x8{(int)w[0], (int)w[1], (int)w[2], (int)w[3], 0, 0, 0, 0};
+            const int sa = (int)((wv[t].code >> (wv[t].shift + 8 * b)) & 0xffu);
+#pragma unroll
+            for (int mb = 0; mb < NMB; ++mb)
+                acc[t][mb] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv[mb], acc[t][mb], 4, 0, 0, sa, 0,
+                                                                              sb[mb]);
         }
     }
 }
@@ -645,9 +777,11 @@ __device__ __forceinline__ int partial_offset(int wave, int t, int mb, int lane)
 // Persistent stream over the workgroup's unit range [x0, x1).  The loads of
 // unit u + PD - 1 are issued while unit u is contracted, across item
 // boundaries: one pipeline for the whole range, never drained in between.
-template <int FMT, bool DOWN, int PD>
+template <int FMT, bool DOWN, int PD, bool MXA>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void expert_ffn_kernel(FfnParams P)
 {
+    static_assert(!MXA || FMT == FMT_MXFP4, "MX activations take MXFP4 weights");
+    static_assert(!MXA || 2 * (kScaleQ + kMB * 16 * 8) <= 2 * BTile<Fmt<FMT>::kBlocks>::kBuf, "MX tile fits the LDS");
     constexpr int NV = Fmt<FMT>::kVecs, SB = Fmt<FMT>::kBlocks;
     constexpr int BROW = BTile<SB>::kRow, BBUF = BTile<SB>::kBuf;
     constexpr uint32_t BLK = 1024u * NV;  // bytes of one 16 x 128 block of a tile
@@ -674,20 +808,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         if (!DOWN) write_fix_record(P, pl, sp, w, x0, x1);
     }
     if (x0 >= x1) return;
-    const uint32_t brow_bytes = (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
-    const rsrc_t rb = DOWN ? make_rsrc(a.h, (uint32_t)(a.T * a.k + (a.sh_gate ? a.T : 0)) * brow_bytes)
-                           : make_rsrc(a.x, (uint32_t)a.T * brow_bytes);
+    const uint32_t rows = (uint32_t)(DOWN ? a.T * a.k + (a.sh_gate ? a.T : 0) : a.T);
+    // Activation rows: bf16 x or H, or (MX) e4m3fn codes of K padded to nblocks * 128 and their block scales.
+    const uint32_t brow_bytes = MXA ? (uint32_t)P.nblocks * kMacroK : (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
+    const rsrc_t rb = make_rsrc(MXA ? static_cast<const void *>(DOWN ? a.hq : a.xq)
+                                    : static_cast<const void *>(DOWN ? a.h : a.x), rows * brow_bytes);
+    const rsrc_t rsa = make_rsrc(DOWN ? a.hs : a.xs, MXA ? rows * (uint32_t)P.nblocks * 4u : 0u);
 
     Source src;
-    set_source<FMT, DOWN>(src, P, sp, (int)(x0 / nsteps));
+    set_source<FMT, DOWN, MXA>(src, P, sp, (int)(x0 / nsteps));
 
     WFrag<FMT> wf[PD][2];
     u32x4 bst[PD][kBPass][SB];
+    uint32_t sst[PD][kBPass];  // MX: the rows' block scales of a step (threads bc < 2)
     // Loads of unit v into ring slot `slot`; a unit past the range loads zeros
     // (offsets beyond every buffer), so every path issues the same loads and
     // the compiler's wait counts stay exact.
     auto issue = [&](int slot, long v) {
-        if (v >= src.ie && v < x1) set_source<FMT, DOWN>(src, P, sp, src.item + 1);
+        if (v >= src.ie && v < x1) set_source<FMT, DOWN, MXA>(src, P, sp, src.item + 1);
         const bool ok = v < x1;
         const uint32_t step = (uint32_t)(v - src.ib);
 #pragma unroll
@@ -716,10 +854,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                     wf[slot][0].shift = wf[slot][1].shift = (int)(kb & 3u) * 8;
                 }
             }
-            const bool kok = ok && (int)kb * kMacroK + bc * 8 < K;
+            if constexpr (!MXA) {
+                const bool kok = ok && (int)kb * kMacroK + bc * 8 < K;
 #pragma unroll
-            for (int i = 0; i < kBPass; ++i)
-                bst[slot][i][b] = load16<0>(rb, (kok && src.boff[i] != kOff) ? src.boff[i] + kb * 256u : kOff);
+                for (int i = 0; i < kBPass; ++i)
+                    bst[slot][i][b] = load16<0>(rb, (kok && src.boff[i] != kOff) ? src.boff[i] + kb * 256u : kOff);
+            }
+        }
+        if constexpr (MXA) {
+            // A step's 2 x 128 codes of a row are 256 contiguous bytes (16 per thread),
+            // its 8 block scales two dwords (threads bc = 0, 1).
+            const bool aok = ok && (int)(step * SB + (bc >> 3)) < P.nblocks;
+            const bool sok = ok && bc < 2 && (int)(step * SB + (bc & 1)) < P.nblocks;
+#pragma unroll
+            for (int i = 0; i < kBPass; ++i) {
+                bst[slot][i][0] = load16<0>(rb, (aok && src.boff[i] != kOff) ? src.boff[i] + step * 256u : kOff);
+                sst[slot][i] = __builtin_amdgcn_raw_buffer_load_b32(
+                    rsa, (int)((sok && src.soff[i] != kOff) ? src.soff[i] + step * 8u : kOff), 0, 0);
+            }
         }
     };
 
@@ -740,23 +892,42 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         const int nmb = (cd.M + 15) / 16;
         uint8_t *buf = lds + par * BBUF;
         // After the previous step's barrier no wavefront still reads this buffer.
+        if constexpr (MXA) {
 #pragma unroll
-        for (int i = 0; i < kBPass; ++i)
+            for (int i = 0; i < kBPass; ++i) {
+                *reinterpret_cast<u32x4 *>(buf + (i * kBRowsPerPass + br) * kRowQ + bc * 16) = bst[slot][i][0];
+                if (bc < 2)
+                    *reinterpret_cast<uint32_t *>(buf + kScaleQ + (i * kBRowsPerPass + br) * 8 + bc * 4) = sst[slot][i];
+            }
+        } else {
 #pragma unroll
-            for (int b = 0; b < SB; ++b)
-                *reinterpret_cast<u32x4 *>(buf + (i * kBRowsPerPass + br) * BROW + b * 256 + bc * 16) = bst[slot][i][b];
+            for (int i = 0; i < kBPass; ++i)
+#pragma unroll
+                for (int b = 0; b < SB; ++b)
+                    *reinterpret_cast<u32x4 *>(buf + (i * kBRowsPerPass + br) * BROW + b * 256 + bc * 16) =
+                        bst[slot][i][b];
+        }
         __syncthreads();
-        switch (nmb) {
-        case 1: contract<FMT, 1>(wf[slot], buf, acc); break;
-        case 2: contract<FMT, 2>(wf[slot], buf, acc); break;
-        case 3: contract<FMT, 3>(wf[slot], buf, acc); break;
-        default: contract<FMT, 4>(wf[slot], buf, acc); break;
+        if constexpr (MXA) {
+            switch (nmb) {
+            case 1: contract_mx<1>(wf[slot], buf, acc); break;
+            case 2: contract_mx<2>(wf[slot], buf, acc); break;
+            case 3: contract_mx<3>(wf[slot], buf, acc); break;
+            default: contract_mx<4>(wf[slot], buf, acc); break;
+            }
+        } else {
+            switch (nmb) {
+            case 1: contract<FMT, 1>(wf[slot], buf, acc); break;
+            case 2: contract<FMT, 2>(wf[slot], buf, acc); break;
+            case 3: contract<FMT, 3>(wf[slot], buf, acc); break;
+            default: contract<FMT, 4>(wf[slot], buf, acc); break;
+            }
         }
         // Item boundary: finish the item (or park its partial sums if it is
         // cut at either end of the range) and move on to the next one.
         if (u + 1 == cib + nsteps || u + 1 == x1) {
             if (cib >= x0 && cib + nsteps <= x1) {
-                finish_item<DOWN>(P, cd, wave, acc, cbias);
+                finish_item<DOWN, MXA>(P, cd, wave, acc, cbias);
             } else {
                 float *dst = P.partials + ((size_t)w * 2 + (cib <= x0 ? 0 : 1)) * kPartialFloats;
 #pragma unroll
@@ -797,7 +968,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 // position and (token group, row in the group), one grouped position per
 // thread.  The kernel boundary makes the expert kernel's records and partial
 // sums visible here.
-template <bool DOWN>
+template <bool DOWN, bool MXA>
 __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
 {
     const int lane = lane_id();
@@ -860,7 +1031,47 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
             add(P.partials + ((size_t)v * 2 + ((ib <= v0 && v0 < ie) ? 0 : 1)) * kPartialFloats);
         }
     }
-    finish_item<DOWN>(P, d, wave, acc, load_bias<DOWN>(P, d, wave));
+    finish_item<DOWN, MXA>(P, d, wave, acc, load_bias<DOWN>(P, d, wave));
+}
+
+// MX activation mode: x [T][K] bf16 -> e4m3fn codes [T][kp] in the FP8
+// operand's lane order and e8m0 scales [T][kp / 32] (kp = K padded to a
+// multiple of 128, zeros beyond K), one thread per block of 32 consecutive
+// elements.  Block g of a chunk is K 32g..32g+31; its first 16 codes go to
+// chunk byte 64 (g % 2) + 16 (g / 2), its last 16 to 32 bytes further.
+__global__ __launch_bounds__(256) void mx_quant_x_kernel(const uint16_t *__restrict__ x, int T, int K, int kp,
+                                                         uint8_t *__restrict__ xq, uint8_t *__restrict__ xs)
+{
+    const int nb = kp / 32;
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= T * nb) return;
+    const int row = i / nb, blk = i - row * nb, c = blk >> 2, g = blk & 3;
+    float v[32];
+    u32x4 w[4] = {u32x4{0u, 0u, 0u, 0u}, u32x4{0u, 0u, 0u, 0u}, u32x4{0u, 0u, 0u, 0u}, u32x4{0u, 0u, 0u, 0u}};
+    if (32 * blk < K) {  // K % 32 == 0: a block is all in range or all out
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(x + (size_t)row * K + 32 * blk);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = src[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+        const uint32_t word = w[j >> 3][(j >> 1) & 3];
+        v[j] = bf16_bits_to_f32((uint16_t)(j & 1 ? word >> 16 : word & 0xffffu));
+    }
+    float amax = 0.f;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) amax = fmaxf(amax, fabsf(v[j]));
+    const int E = mx_exponent(amax);
+    const float inv = mx_inv_scale(E);
+    u32x4 q[2];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        q[j >> 2][j & 3] = e4m3_code(v[4 * j] * inv) | (e4m3_code(v[4 * j + 1] * inv) << 8) |
+                           (e4m3_code(v[4 * j + 2] * inv) << 16) | (e4m3_code(v[4 * j + 3] * inv) << 24);
+    uint8_t *dst = xq + (size_t)row * kp + c * 128 + 64 * (g & 1) + 16 * (g >> 1);
+    *reinterpret_cast<u32x4 *>(dst) = q[0];
+    *reinterpret_cast<u32x4 *>(dst + 32) = q[1];
+    xs[(size_t)row * nb + blk] = (uint8_t)(E + 127);
 }
 
 // Token groups when some expert may have more than 64 tokens (T > 64):
@@ -997,7 +1208,7 @@ static int plan_capacity(int T, int k, bool shared)
     return (int)(1025 + (rows + kTokGroup - 1) / kTokGroup);
 }
 
-VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared)
+VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared, bool mx)
 {
     auto align = [](size_t v) { return (v + 255) & ~(size_t)255; };
     const size_t rows = (size_t)T * k + (shared ? (size_t)T : 0);
@@ -1016,7 +1227,11 @@ VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared)
     w.map_bytes = (size_t)T * k * 4 * 2;  // grouped position, (group, row) per routed slot
     w.cut_offset = w.map_offset + align(w.map_bytes);
     w.cut_bytes = (size_t)w.plan_cap * ((d + 32 * kWG - 1) / (32 * kWG)) * 8;
-    w.total = w.cut_offset + align(w.cut_bytes);
+    // MX activations: x codes + scales, then H codes + scales (rows padded to multiples of 128).
+    const size_t kpd = (size_t)(d + kMacroK - 1) / kMacroK * kMacroK, kpf = (size_t)(d_ff + kMacroK - 1) / kMacroK * kMacroK;
+    w.mx_offset = w.cut_offset + align(w.cut_bytes);
+    w.mx_bytes = mx ? align((size_t)T * kpd) + align((size_t)T * kpd / 32) + align(rows * kpf) + align(rows * kpf / 32) : 0;
+    w.total = w.mx_offset + align(w.mx_bytes);
     return w;
 }
 
@@ -1025,7 +1240,7 @@ static hipError_t mark(hipEvent_t const *events, int i, hipStream_t stream)
     return (events && events[i]) ? hipEventRecord(events[i], stream) : hipSuccess;
 }
 
-template <int FMT>
+template <int FMT, bool MXA>
 static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const VerifyWorkspace &ws, hipStream_t stream,
                              hipEvent_t const *events)
 {
@@ -1046,6 +1261,19 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     if ((err = mark(events, 0, stream)) != hipSuccess) return err;
+    if constexpr (MXA) {
+        auto align = [](size_t v) { return (v + 255) & ~(size_t)255; };
+        const size_t rows = (size_t)a.T * a.k + (a.sh_gate ? (size_t)a.T : 0);
+        const int kpd = (a.d + kMacroK - 1) / kMacroK * kMacroK, kpf = (a.d_ff + kMacroK - 1) / kMacroK * kMacroK;
+        a.xq = ws_base + ws.mx_offset;
+        a.xs = a.xq + align((size_t)a.T * kpd);
+        a.hq = a.xs + align((size_t)a.T * kpd / 32);
+        a.hs = a.hq + align(rows * kpf);
+        const int n = a.T * (kpd / 32);
+        hipLaunchKernelGGL(mx_quant_x_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a.x, a.T, a.d, kpd, a.xq,
+                           a.xs);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
     FfnParams g{};
     g.a = a;
     g.N = a.d_ff;
@@ -1061,11 +1289,11 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     g.fix = g.ranges + (size_t)kMaxWorkers * 2;
     g.cut = reinterpret_cast<long long *>(ws_base + ws.cut_offset);
     g.plan = grouped ? plan : nullptr;
-    hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD>), dim3(G), dim3(kThreads), 0, stream, g);
+    hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD, MXA>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = mark(events, 1, stream)) != hipSuccess) return err;
     const int map_blocks = (a.T * a.k + kThreads - 1) / kThreads;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false>), dim3(G + map_blocks), dim3(kThreads), 0, stream, g);
+    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false, MXA>), dim3(G + map_blocks), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     FfnParams dn = g;
@@ -1076,7 +1304,7 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     dn.band_rows = 32 * kWG;
     dn.nbands = (a.d + dn.band_rows - 1) / dn.band_rows;
     if ((err = mark(events, 2, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD>), dim3(G), dim3(kThreads), 0, stream, dn);
+    hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD, MXA>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     // Combine also adds up the down items cut between workgroups.
@@ -1092,9 +1320,11 @@ hipError_t launch_verify(const VerifyArgs &a, void *workspace, const VerifyWorks
 {
     uint8_t *base = static_cast<uint8_t *>(workspace);
     switch (a.fmt) {
-    case FMT_BF16: return launch_fmt<FMT_BF16>(a, base, ws, stream, events);
-    case FMT_FP8: return launch_fmt<FMT_FP8>(a, base, ws, stream, events);
-    case FMT_MXFP4: return launch_fmt<FMT_MXFP4>(a, base, ws, stream, events);
+    case FMT_BF16: return launch_fmt<FMT_BF16, false>(a, base, ws, stream, events);
+    case FMT_FP8: return launch_fmt<FMT_FP8, false>(a, base, ws, stream, events);
+    case FMT_MXFP4:
+        return a.act_fmt == 1 ? launch_fmt<FMT_MXFP4, true>(a, base, ws, stream, events)
+                              : launch_fmt<FMT_MXFP4, false>(a, base, ws, stream, events);
     default: return hipErrorInvalidValue;
     }
 }

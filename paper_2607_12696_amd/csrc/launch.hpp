@@ -45,6 +45,14 @@ struct VerifyArgs {
     float *o;           // workspace: [T*k (+T)][d] fp32 expert outputs at grouped positions (shared: T*k + t)
     int32_t *inv;       // workspace: [T*k] grouped position of each routed slot
     int32_t *gidx;      // workspace: [T*k] (token group << 6 | row in the group) of each routed slot
+    // MX activation mode (act_fmt 1, MXFP4 weights only): x and the SwiGLU rows
+    // are the projections' inputs as OCP MX FP8 (one e8m0 code per 32
+    // consecutive elements), rows padded to the next multiple of 128 elements
+    // and each 128-element chunk stored in the FP8 operand's lane order (lane
+    // group g: elements 16g..16g+15, then 64+16g..64+16g+15).
+    int act_fmt;
+    uint8_t *xq, *xs;  // workspace: [T][Kp(d)] e4m3fn codes, [T][Kp(d)/32] e8m0 codes
+    uint8_t *hq, *hs;  // workspace: [T*k (+T)][Kp(d_ff)], [T*k (+T)][Kp(d_ff)/32]
 };
 
 // Upper bound on the workgroups of a verify grid (sizes the partial-sum slots).
@@ -58,11 +66,12 @@ constexpr int kTimingMarks = 5;  // events recorded by the timed entry point
 // per-slot maps for the combine kernel; the cut-item table of the down launch.
 struct VerifyWorkspace {
     size_t h_offset, h_bytes, o_offset, o_bytes, p_offset, p_bytes, plan_offset, plan_bytes, map_offset, map_bytes,
-        cut_offset, cut_bytes;
+        cut_offset, cut_bytes, mx_offset, mx_bytes;
     int plan_cap;
     size_t total;
 };
-VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared);
+// mx: room for the MX activation mode's quantised x and SwiGLU rows.
+VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared, bool mx);
 
 // events: kTimingMarks optional marks (before gate/up, before its fix-up, before
 // down, before combine, after combine).

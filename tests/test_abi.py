@@ -244,6 +244,25 @@ def test_plain_activation_ignores_alpha_and_limit():
     assert _ws(w, 8, 2)[0] == moe.MOE_OK
 
 
+def test_mx_activation_format_validated():
+    # act_fmt: 0 or 1; MX FP8 activations only with MXFP4 weights; they need room for the quantised rows.
+    w = _weights(fmt=2, d=320, d_ff=160)
+    st0, n0 = _ws(w, 64, 2)
+    assert st0 == moe.MOE_OK
+    w.act_fmt = moe.MOE_ACTQ_MXFP8
+    st1, n1 = _ws(w, 64, 2)
+    assert st1 == moe.MOE_OK
+    # x: 64 rows x 384 codes + 12 scales; H: 128 rows x 256 codes + 8 scales (each region 256-byte aligned).
+    assert n1 - n0 == 64 * 384 + 768 + 128 * 256 + 1024
+    for bad in (2, -1):
+        w.act_fmt = bad
+        assert _ws(w, 64, 2)[0] == moe.MOE_ERR_INVALID_ARG
+    for fmt in (0, 1):
+        w = _weights(fmt=fmt, d=256, d_ff=128)
+        w.act_fmt = moe.MOE_ACTQ_MXFP8
+        assert _ws(w, 8, 2)[0] == moe.MOE_ERR_UNSUPPORTED
+
+
 @pytest.mark.parametrize("name", ["b_gate", "b_up", "b_down"])
 def test_misaligned_bias_rejected(name):
     w = _weights()

@@ -513,6 +513,89 @@ def test_workspace_contents_do_not_matter():
     assert torch.equal(y1, y2)
 
 
+# ----------------------------------------------------------------------------- MX activation mode
+
+# MXFP4 weights with MX FP8 activations on the scaled FP4 x FP8 matrix-core instruction, against the
+# oracle's act_fmt 1 definition.  The GPU's SwiGLU rows are fp32 where the oracle's are fp64, so a block
+# exponent or an element code can differ where a value lies on a rounding boundary; each such case moves
+# y by far less than the tolerance.  The result must also sit much closer to the quantised definition
+# than to the exact-input layer (the quantisation itself moves y by a few percent).
+MX_SHAPES = {
+    "mxfp4": SMALL["mxfp4"],  # d 320, d_ff 160: ragged 128-element chunks on both projections
+    "mxfp4_sh": synth.Shape("mxfp4_sh", 256, 96, 12, 3, synth.FMT_MXFP4, 1, True),  # shared expert, d_ff < 128
+}
+_mx_layers = {}
+
+
+def mx_layer(name):
+    if name not in _mx_layers:
+        _mx_layers[name] = synth.layer_weights(MX_SHAPES[name], seed=23)
+    return _mx_layers[name]
+
+
+def check_mx(layer, sh, T, seed, kind="scattered", rows=None, oai=False):
+    x = synth.activations(T, sh.d, seed=seed)
+    lg = routed_logits(kind, T, sh, seed=seed + 1, U=min(sh.E, 32))
+    dl = dict(to_dev(layer), act_fmt=moe.MOE_ACTQ_MXFP8)
+    y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), dl, sh.k, sh.score)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), sh.k, sh.score)
+    y_mx = oracle.verify_tokens(dict(layer, act_fmt=1), x, idx_o, w_o, tokens=rows, threads=8)
+    y_plain = oracle.verify_tokens(layer, x, idx_o, w_o, tokens=rows, threads=8)
+    yg = y.float().cpu().numpy()
+    if rows is not None:
+        yg = yg[rows]
+    err, err_plain = y_err(yg, y_mx), y_err(yg, y_plain)
+    note(f"  rel err vs MX oracle {err:.3e}, vs exact-input oracle {err_plain:.3e}")
+    assert err <= YTOL
+    assert err < 0.25 * err_plain
+    return y, x, lg, dl
+
+
+@pytest.mark.parametrize("name", list(MX_SHAPES))
+@pytest.mark.parametrize("T", [1, 8, 37, 64, 130])
+def test_verify_mx_activations_match_mx_oracle(name, T):
+    sh = MX_SHAPES[name]
+    note(f"verify MX activations shape={name} T={T}")
+    check_mx(mx_layer(name), sh, T, seed=100 + T)
+
+
+def test_verify_mx_activations_gpt_oss_expert():
+    sh = MX_SHAPES["mxfp4"]
+    note("verify MX activations with the GPT-OSS expert (biases, clamped SwiGLU)")
+    check_mx(with_oai(mx_layer("mxfp4"), sh, seed=9), sh, 37, seed=300)
+
+
+def test_verify_mx_activations_deterministic_and_workspace_independent():
+    sh = MX_SHAPES["mxfp4_sh"]
+    y, x, lg, dl = check_mx(mx_layer("mxfp4_sh"), sh, 64, seed=400, kind="clustered")
+    nbytes = moe.moe_verify_workspace_size(dl, 64, sh.k)
+    ws = torch.full((nbytes,), 0xFF, dtype=torch.uint8, device=DEV)  # 0xff: e4m3fn NaN codes everywhere
+    y2, _ = moe.moe_verify_step(x.to(DEV), lg.to(DEV), dl, sh.k, sh.score, workspace=ws)
+    assert torch.equal(y, y2)
+
+
+@pytest.mark.parametrize("T,kind,U,rows", [(64, "clustered", None, [0, 33, 63]), (512, "exact", 32, [5, 400])])
+def test_full_gpt_mx_activations_sampled_rows(T, kind, U, rows):
+    sh = synth.SHAPES["gpt"]
+    note(f"full GPT-OSS shape, MX activations T={T} routing={kind} rows={rows}")
+    raw, dl = full_layer("gpt")
+    x = synth.activations(T, sh.d, seed=51)
+    lg = routed_logits(kind, T, sh, seed=51, U=U)
+    y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), dict(dl, act_fmt=moe.MOE_ACTQ_MXFP8), sh.k, sh.score)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), sh.k, sh.score)
+    used = sorted(set(idx_o[rows].reshape(-1).tolist()))
+    hl = host_experts(raw, used)
+    y_mx = oracle.verify_tokens(dict(hl, act_fmt=1), x, idx_o, w_o, tokens=rows, threads=16)
+    y_plain = oracle.verify_tokens(hl, x, idx_o, w_o, tokens=rows, threads=16)
+    yg = y.float().cpu().numpy()[rows]
+    err, err_plain = y_err(yg, y_mx), y_err(yg, y_plain)
+    note(f"  U={int(r.n_unique.item())} rel err vs MX oracle {err:.3e}, vs exact-input oracle {err_plain:.3e}")
+    assert err <= YTOL and err < 0.25 * err_plain
+    assert torch.isfinite(y.float()).all()
+
+
 # ----------------------------------------------------------------------------- full model shapes, sampled rows
 
 _full = {}
@@ -536,7 +619,7 @@ def host_experts(dl, experts):
     for n in ("gate", "up", "down", "s_gate", "s_up", "s_down", "b_gate", "b_up", "b_down"):
         if n in dl:
             out[n] = {e: dl[n][e].cpu() for e in experts}
-    for n in ("act", "alpha", "limit"):
+    for n in ("act", "alpha", "limit", "act_fmt"):
         if n in dl:
             out[n] = dl[n]
     for n in ("sh_gate", "sh_up", "sh_down", "sh_s_gate", "sh_s_up", "sh_s_down"):

@@ -1,10 +1,9 @@
 """Pins for the oracle's MX activation quantiser and the act_fmt 1 layer (CPU only).
 
 The optional MX activation mode quantises the inputs of both projections to
-OCP MX FP8: e4m3fn elements with one power-of-two scale 2^E per block of 32,
-E = floor(log2(amax)) - 8, nearest value with ties to the even code, magnitudes
-of 448 and more saturating.  A block is elements 16b..16b+15 and
-64+16b..64+16b+15 of each 128-element chunk.  The reference here builds the
+OCP MX FP8: e4m3fn elements with one power-of-two scale 2^E per block of 32
+consecutive elements, E = floor(log2(amax)) - 8, nearest value with ties to the
+even code, magnitudes of 448 and more saturating.  The reference here builds the
 e4m3fn value grid from the format's definition, takes the exponent from
 math.frexp, picks the nearest grid value by search, and lists each block's
 elements explicitly, so that a wrong exponent, a wrong rounding direction, a
@@ -55,12 +54,7 @@ def _nearest(a):
 
 
 def _blocks(K):
-    out = []
-    for c in range((K + 127) // 128):
-        for b in range(4):
-            idx = [128 * c + 16 * b + i for i in range(16)] + [128 * c + 64 + 16 * b + i for i in range(16)]
-            out.append([i for i in idx if i < K])
-    return out
+    return [[i for i in range(32 * b, 32 * b + 32) if i < K] for b in range((K + 31) // 32)]
 
 
 def ref_quant(v):
@@ -90,7 +84,7 @@ def _rows(seed, K, n):
     return rows
 
 
-@pytest.mark.parametrize("K", [128, 256, 2880, 96, 200])
+@pytest.mark.parametrize("K", [128, 256, 2880, 96, 200, 50])
 def test_quantiser_matches_brute_force(K):
     for v in _rows(K, K, 4):
         for row in (v, torch.tensor(v).to(torch.bfloat16).to(torch.float64).numpy()):
@@ -104,11 +98,7 @@ def test_quantiser_agrees_with_torch_float8_cast():
     # In-range rounding (|v / 2^E| < 448) against PyTorch's float32 -> float8_e4m3fn cast.
     for v in _rows(7, 1024, 6):
         q, e = oracle.mx_quantize(v)
-        scale = np.empty(v.size)
-        for c in range(v.size // 128):
-            for b in range(4):
-                for base in (16 * b, 64 + 16 * b):
-                    scale[128 * c + base:128 * c + base + 16] = 2.0 ** e[4 * c + b]
+        scale = np.repeat(np.exp2(e.astype(np.float64)), 32)
         a = v / scale
         ok = np.abs(a) < 448
         t = torch.tensor(a[ok], dtype=torch.float32).to(torch.float8_e4m3fn).to(torch.float64).numpy()
@@ -118,37 +108,33 @@ def test_quantiser_agrees_with_torch_float8_cast():
 def test_closed_forms_and_ties():
     v = np.zeros(128)
     v[[0, 1, 2, 3]] = [1.0, 1.0 / 3.0, -2.5, 1.925]          # block 0: amax 2.5 -> E = -7
-    v[16:22] = [256.0, 8.5, 9.5, -8.5, 500.0 / 512, 0.0]      # block 1: amax 256 -> E = 0
-    v[96] = 300.0                                             # block 2 (64 + 32): E = 0
-    v[32] = 2.0 ** -20                                        # block 2 as well: tiny next to 300
+    v[32:38] = [256.0, 8.5, 9.5, -8.5, 500.0 / 512, 0.0]      # block 1: amax 256 -> E = 0
+    v[96] = 300.0                                             # block 3: E = 0
+    v[127] = 2.0 ** -20                                       # block 3 as well: tiny next to 300
     q, e = oracle.mx_quantize(v)
-    assert list(e) == [-7, 0, 0, -127]
+    assert list(e) == [-7, 0, -127, 0]
     assert list(q[:4]) == [1.0, 0.34375, -2.5, 1.875]        # 128; 42.67 -> 44; 320; 246.4 -> 240 (x 2^-7)
     # 8.5 and 9.5 are ties (to the even code: 8, 10); 0.977 rounds up to 1.0 on the 1/16 grid
-    assert list(q[16:22]) == [256.0, 8.0, 10.0, -8.0, 1.0, 0.0]
-    assert q[96] == 288.0 and q[32] == 0.0                   # 300 -> 288 (step 32); 2^-20 underflows
+    assert list(q[32:38]) == [256.0, 8.0, 10.0, -8.0, 1.0, 0.0]
+    assert q[96] == 288.0 and q[127] == 0.0                  # 300 -> 288 (step 32); 2^-20 underflows
     # Saturation: a block whose maximum lies in [448, 512) * 2^E.
-    s = np.zeros(128)
-    s[5], s[70] = 500.0 * 2.0 ** -3, -470.0 * 2.0 ** -3
+    s = np.zeros(64)
+    s[5], s[20] = 500.0 * 2.0 ** -3, -470.0 * 2.0 ** -3
     q, e = oracle.mx_quantize(s)
-    assert e[0] == -3 and q[5] == 448.0 * 2.0 ** -3 and q[70] == -448.0 * 2.0 ** -3
+    assert e[0] == -3 and q[5] == 448.0 * 2.0 ** -3 and q[20] == -448.0 * 2.0 ** -3
 
 
 def test_block_grouping():
-    # One large element raises the exponent of its own block only.
+    # One large element raises the exponent of its own block of 32 only.
     rng = np.random.default_rng(3)
     v = rng.standard_normal(384)
-    _, e0 = oracle.mx_quantize(v)
-    for pos, blk in [(128 + 64 + 16 * 2 + 5, 4 + 2), (16 * 3 + 15, 3), (256 + 64 + 7, 8 + 0)]:
+    q0, e0 = oracle.mx_quantize(v)
+    for pos in (229, 63, 64, 0, 383):
         w = v.copy()
         w[pos] = 1e6
         q, e = oracle.mx_quantize(w)
-        changed = np.nonzero(e != e0)[0].tolist()
-        assert changed == [blk]
-        c, b = divmod(blk, 4)
-        members = [128 * c + 16 * b + i for i in range(16)] + [128 * c + 64 + 16 * b + i for i in range(16)]
-        others = np.setdiff1d(np.arange(384), members)
-        q0, _ = oracle.mx_quantize(v)
+        assert np.nonzero(e != e0)[0].tolist() == [pos // 32]
+        others = np.setdiff1d(np.arange(384), np.arange(pos // 32 * 32, pos // 32 * 32 + 32))
         assert np.array_equal(q[others], q0[others])
 
 
@@ -163,7 +149,7 @@ def test_representable_rows_are_unchanged_and_zero_blocks():
         blk0 = _blocks(256)[0]  # every element of block 0 lies on its grid
         assert np.array_equal(q[blk0], v[blk0])
     q, e = oracle.mx_quantize(np.zeros(200))
-    assert np.all(q == 0) and np.all(e == -127) and e.size == 8
+    assert np.all(q == 0) and np.all(e == -127) and e.size == 7
 
 
 def _ffn_mx(x, Wg, Wu, Wd):
