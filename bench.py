@@ -300,7 +300,9 @@ def variant_timing(T=64, steps=30, warmup=3, n_pool=8):
     x = synth.activations(T, sh.d, seed=1, device=dev)
     pool = [synth.routes_to_logits(synth.routes_clustered(T, sh.E, sh.k, 0.8, seed=50 + i), sh.E, seed=i,
                                    device=dev) for i in range(n_pool)]
-    ws = torch.empty(moe.moe_verify_workspace_size(plain, T, sh.k), dtype=torch.uint8, device=dev)
+    # The MX-activation layout needs the most workspace of the three variants.
+    ws = torch.empty(moe.moe_verify_workspace_size(dict(plain, act_fmt=moe.MOE_ACTQ_MXFP8), T, sh.k),
+                     dtype=torch.uint8, device=dev)
     y = torch.empty_like(x)
     uniq = []
     for lg in pool:
