@@ -284,8 +284,13 @@ moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, siz
  *   256-byte aligned; its contents on entry do not matter.
  * Arithmetic: weights decoded exactly to bf16, bf16 matrix cores with fp32
  * accumulation, FP8 block scales applied to fp32 partial sums, the SwiGLU
- * intermediate rounded to bf16, y rounded to bf16.  Deterministic: the same
- * inputs give bit-identical y.
+ * intermediate rounded to bf16, y rounded to bf16.  With act_fmt =
+ * MOE_ACTQ_MXFP8 (MXFP4 weights) x and the SwiGLU intermediate are quantised
+ * to MX FP8 instead (moe_actq_t) and multiplied on the scaled FP4 x FP8
+ * matrix cores, fp32 accumulation.  Deterministic: the same inputs give
+ * bit-identical y.
+ * Limits: T*d*2, (T*k + T)*d_ff*2 and (T*k + T)*d*4 bytes each below 2 GiB
+ * (else MOE_ERR_UNSUPPORTED), plus those of moe_verify_workspace_size.
  */
 moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
                               void *workspace, size_t workspace_bytes, void *stream);

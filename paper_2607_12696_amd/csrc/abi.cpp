@@ -189,7 +189,9 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     if (ws.plan_cap > ecospec::kMaxGroups) return MOE_ERR_UNSUPPORTED;
     if (workspace_bytes < ws.total) return MOE_ERR_WORKSPACE;
     const long rows = (long)r->T * r->k + (shared ? r->T : 0);
-    if ((long)r->T * w->d * 2 >= (1L << 31) || rows * w->d_ff * 2 >= (1L << 31)) return MOE_ERR_UNSUPPORTED;
+    // x, H and O are addressed through 32-bit buffer ranges.
+    if ((long)r->T * w->d * 2 >= (1L << 31) || rows * w->d_ff * 2 >= (1L << 31) || rows * w->d * 4 >= (1L << 31))
+        return MOE_ERR_UNSUPPORTED;
 
     ecospec::VerifyArgs a{};
     a.fmt = w->fmt;

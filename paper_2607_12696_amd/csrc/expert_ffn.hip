@@ -1007,6 +1007,7 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
     d.M = (int)ld_s64(rec + 3);
     d.n0 = (int)(item % P.nbands) * P.band_rows;
     const int nmb = (d.M + 15) / 16;  // only the live token blocks were parked
+    const ItemBias bias = load_bias<DOWN>(P, d, wave);  // in flight with the partial sums
     f32x4 acc[2][kMB];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -1020,8 +1021,30 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
                 if (mb < nmb) acc[t][mb] += *reinterpret_cast<const f32x4 *>(src + partial_offset<DOWN>(wave, t, mb, lane));
     };
     if (cut >> 62) {
+        // Up to three contributors: every load is issued before the first sum (one round trip;
+        // absent contributors and dead token blocks read zeros), then added in workgroup order.
         const int cnt = (int)((cut >> 60) & 3);
-        for (int i = 0; i < cnt; ++i) add(P.partials + (size_t)((cut >> (20 * i)) & 0xfffff) * kPartialFloats);
+        const rsrc_t rp = make_rsrc(P.partials, (uint32_t)((size_t)P.workers * 2 * kPartialFloats * 4));
+        f32x4 v[3][2][kMB];
+#pragma unroll
+        for (int i = 0; i < 3; ++i) {
+            const uint32_t slot = (uint32_t)((cut >> (20 * i)) & 0xfffff);
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int mb = 0; mb < kMB; ++mb)
+                    v[i][t][mb] = __builtin_bit_cast(
+                        f32x4, load16<0>(rp, (i < cnt && mb < nmb)
+                                                 ? (slot * kPartialFloats + (uint32_t)partial_offset<DOWN>(wave, t, mb, lane)) * 4u
+                                                 : kOff));
+        }
+#pragma unroll
+        for (int i = 0; i < 3; ++i)
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int mb = 0; mb < kMB; ++mb)
+                    if (i < cnt && mb < nmb) acc[t][mb] += v[i][t][mb];
     } else {
         // More than three contributors: each one's slot follows from its range.
         const long ib = (long)item * P.nsteps, ie = ib + P.nsteps;
@@ -1031,7 +1054,7 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
             add(P.partials + ((size_t)v * 2 + ((ib <= v0 && v0 < ie) ? 0 : 1)) * kPartialFloats);
         }
     }
-    finish_item<DOWN, MXA>(P, d, wave, acc, load_bias<DOWN>(P, d, wave));
+    finish_item<DOWN, MXA>(P, d, wave, acc, bias);
 }
 
 // MX activation mode: x [T][K] bf16 -> e4m3fn codes [T][kp] in the FP8
@@ -1109,17 +1132,23 @@ __global__ __launch_bounds__(256) void plan_kernel(VerifyArgs a, int32_t *plan)
 // fix-up would have stored).  `cut` is the item's record_cuts entry.
 __device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, long item, int p, int r, int c)
 {
-    if (cut < 0) return *reinterpret_cast<const f32x4 *>(D.a.o + (size_t)p * D.a.d + c);
     const int off = r * D.band_rows + c % D.band_rows;  // partial_offset<true>
-    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (cut >> 62) {
-        const int cnt = (int)((cut >> 60) & 3);
-        for (int i = 0; i < cnt; ++i) {
-            const long ps = (cut >> (20 * i)) & 0xfffff;
-            s += *reinterpret_cast<const f32x4 *>(D.partials + (size_t)ps * kPartialFloats + off);
-        }
-        return s;
+    if (cut < 0 || (cut >> 62)) {
+        // A whole item's O row, or up to three parked partial sums: all loads issued at once
+        // (absent ones read zeros) and added in workgroup order.
+        const int cnt = cut < 0 ? 0 : (int)((cut >> 60) & 3);
+        const rsrc_t ro = make_rsrc(D.a.o, (uint32_t)((size_t)(D.a.T * D.a.k + (D.a.sh_gate ? D.a.T : 0)) * D.a.d * 4));
+        const rsrc_t rp = make_rsrc(D.partials, (uint32_t)((size_t)D.workers * 2 * kPartialFloats * 4));
+        const f32x4 v0 = __builtin_bit_cast(
+            f32x4, cut < 0 ? load16<0>(ro, (uint32_t)((size_t)p * D.a.d + c) * 4u)
+                           : load16<0>(rp, (uint32_t)((cut & 0xfffff) * kPartialFloats + off) * 4u));
+        const f32x4 v1 = __builtin_bit_cast(
+            f32x4, load16<0>(rp, cnt > 1 ? (uint32_t)(((cut >> 20) & 0xfffff) * kPartialFloats + off) * 4u : kOff));
+        const f32x4 v2 = __builtin_bit_cast(
+            f32x4, load16<0>(rp, cnt > 2 ? (uint32_t)(((cut >> 40) & 0xfffff) * kPartialFloats + off) * 4u : kOff));
+        return cnt > 2 ? v0 + v1 + v2 : cnt > 1 ? v0 + v1 : v0;
     }
+    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
     // More than three contributors: each one's slot follows from its range.
     const long ib = item * D.nsteps, ie = ib + D.nsteps;
     for (int v = (int)(cut >> 16) & 0xffff, w1 = (int)cut & 0xffff; v <= w1; ++v) {
