@@ -203,6 +203,18 @@ def test_pack_gate_up_rejects():
     assert L.moe_pack_gate_up(*bad) == moe.MOE_ERR_UNSUPPORTED
 
 
+def test_verify_layer_rejects_outputs_past_2gib():
+    # O (fp32 rows of T*k + T slots x d) is addressed through a 32-bit buffer range: DS shape with T = 8400
+    # gives 75600 x 7168 x 4 bytes = 2.17 GB; every other limit (groups, H, x) still holds.
+    L = moe.lib()
+    w = _weights(1, 7168, 2048, 256, shared=True)
+    T = 8400
+    st, need = _ws(w, T, 8)
+    assert st == moe.MOE_OK
+    r = _routing(T, 8, 256)
+    assert L.moe_verify_layer(FAKE, C.byref(w), C.byref(r), 2 * FAKE, 4 * FAKE, need, None) == moe.MOE_ERR_UNSUPPORTED
+
+
 def test_misaligned_weight_rejected():
     w = _weights()
     w.w_up = FAKE + 8
