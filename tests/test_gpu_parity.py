@@ -343,6 +343,26 @@ def test_verify_small_matches_oracle(name, T):
     assert err <= YTOL
 
 
+@pytest.mark.parametrize("name", ["toy", "fp8", "mxfp4", "bf16_tail"])
+@pytest.mark.parametrize("T", [1, 64, 130])
+def test_verify_identical_routing_matches_oracle(name, T):
+    # Degenerate draft: every token routes to the same k experts (U = k, each expert serves all T tokens,
+    # in several 64-token groups when T > 64).
+    sh = SMALL[name]
+    note(f"verify identical routing shape={name} T={T}")
+    layer = small_layer(name)
+    x = synth.activations(T, sh.d, seed=T + 40)
+    lg = routed_logits("exact", T, sh, seed=T + 41, U=sh.k)
+    y, r = moe.moe_verify_step(x.to(DEV), lg.to(DEV), to_dev(layer), sh.k, sh.score)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route(lg.numpy(), sh.k, sh.score)
+    assert int(r.n_unique.item()) == sh.k
+    y_ref = oracle.verify_tokens(layer, x, idx_o, w_o, threads=8)
+    err = y_err(y.float().cpu().numpy(), y_ref)
+    note(f"  rel err {err:.3e}")
+    assert err <= YTOL
+
+
 # Limits of the verify path: T * k above the 4096 routed slots whose token rows the expert kernels stage in
 # LDS (the rows then come through scalar loads), E = 1024 with k = 64, and one token with k = 64.
 LIMIT_CASES = [
@@ -662,6 +682,32 @@ def test_full_gpt_oss_variant_sampled_rows():
     note(f"  U={int(r.n_unique.item())} rel err {err:.3e}")
     assert err <= YTOL
     assert torch.isfinite(y.float()).all()
+
+
+def test_full_ds_grouped_routing_sampled_rows():
+    # DeepSeek-V3 routing end to end: group-limited top-8 with correction bias and routed scaling, union,
+    # verify.  Rows are compared where the fp64 routing decision clears the fp32 tolerance, so both sides
+    # route those tokens identically.
+    sh = synth.SHAPES["ds"]
+    T, G, TG, scale = 64, 8, 4, 2.5
+    raw, dl = full_layer("ds")
+    x = synth.activations(T, sh.d, seed=77)
+    lg = synth.logits_scattered(T, sh.E, seed=78)
+    b = synth.router_bias(sh.E, seed=79)
+    idx_g, w_g = moe.moe_route_topk_grouped(lg.to(DEV), b.to(DEV), sh.k, G, TG, scale)
+    r = moe.moe_expert_union(idx_g, sh.E, topk_w=w_g)
+    y = moe.moe_verify_layer(x.to(DEV), dl, r)
+    torch.cuda.synchronize()
+    idx_o, w_o = oracle.route_grouped(lg.numpy(), b.numpy(), sh.k, G, TG, scale)
+    rows = [t for t in range(T) if _grouped_margins_ok(lg.numpy(), b.numpy(), sh.k, G, TG, t)][:3]
+    assert len(rows) == 3
+    assert np.array_equal(idx_g.cpu().numpy()[rows], idx_o[rows])
+    note(f"full DS grouped routing rows={rows}")
+    hl = host_experts(raw, sorted(set(idx_o[rows].reshape(-1).tolist())))
+    y_ref = oracle.verify_tokens(hl, x, idx_o, w_o, tokens=rows, threads=16)
+    err = y_err(y.float().cpu().numpy()[rows], y_ref)
+    note(f"  U={int(r.n_unique.item())} rel err {err:.3e}")
+    assert err <= YTOL
 
 
 @pytest.mark.parametrize("name,T,kind,U,rows", FULL_CASES)
