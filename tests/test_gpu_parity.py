@@ -739,13 +739,15 @@ def test_full_shape_sampled_rows(name, T, kind, U, rows):
 
 # ----------------------------------------------------------------------------- HIP graph capture
 
-@pytest.mark.parametrize("name,T", [("fp8", 64), ("mxfp4", 130), ("bf16_tail", 37)])
-def test_graph_replay_matches_eager(name, T):
+@pytest.mark.parametrize("name,T,act_fmt", [("fp8", 64, 0), ("mxfp4", 130, 0), ("bf16_tail", 37, 0),
+                                             ("mxfp4", 64, 1)])
+def test_graph_replay_matches_eager(name, T, act_fmt):
     # The whole step (route, union, verify) captured once and replayed with new routing each time, with eager
     # work and synchronisations between the replays; every replay equals the eager step bit for bit.
+    # act_fmt 1: MX FP8 activations (one more kernel, the x quantisation, in the captured step).
     sh = SMALL[name]
-    note(f"graph replay shape={name} T={T}")
-    dl = to_dev(small_layer(name))
+    note(f"graph replay shape={name} T={T} act_fmt={act_fmt}")
+    dl = dict(to_dev(small_layer(name)), act_fmt=act_fmt)
     x = synth.activations(T, sh.d, seed=71).to(DEV)
     lg = torch.empty(T, sh.E, dtype=torch.float32, device=DEV)
     ws = torch.empty(moe.moe_verify_workspace_size(dl, T, sh.k), dtype=torch.uint8, device=DEV)
