@@ -32,13 +32,15 @@
 // around loads.
 //
 // Work split ("stream-K").  All (item, step) units of a launch are laid end
-// to end and cut into equal contiguous ranges, one per workgroup of a
-// persistent grid, so every workgroup streams the same number of bytes
-// whatever the number of distinct experts.  An item fully inside a range is
-// finished in registers; an item cut between workgroups leaves fp32 partial
-// sums in the workspace, and a small second kernel adds them in workgroup
-// order and finishes it (the kernel boundary makes them visible across the
-// chip's L2 slices; the fixed order keeps the result deterministic).
+// to end and cut into contiguous ranges of equal modelled cost (a step's
+// weight bytes plus its contraction work, which grows with the item's token
+// blocks), one per workgroup of a persistent grid, so the workgroups finish
+// together whatever the number of distinct experts.  An item fully inside a
+// range is finished in registers; an item cut between workgroups leaves fp32
+// partial sums in the workspace, added in workgroup order by a small fix-up
+// kernel (gate/up) or by the combine kernel as it reads O (down): the kernel
+// boundary makes them visible across the XCDs' L2 caches, and the fixed order
+// keeps the result deterministic.
 //
 // Outputs: gate/up writes the bf16 SwiGLU rows H at grouped positions; down
 // writes one fp32 row per (token, slot); combine applies the gate weights and
