@@ -777,8 +777,8 @@ __device__ __forceinline__ int partial_offset(int wave, int t, int mb, int lane)
 }
 
 // Persistent stream over the workgroup's unit range [x0, x1).  The loads of
-// unit u + PD - 1 are issued while unit u is contracted, across item
-// boundaries: one pipeline for the whole range, never drained in between.
+// the unit PD - 1 places ahead are issued while a unit is contracted, across
+// item boundaries: one pipeline for the whole range, never drained in between.
 template <int FMT, bool DOWN, int PD, bool MXA>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void expert_ffn_kernel(FfnParams P)
 {
@@ -817,18 +817,28 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                                     : static_cast<const void *>(DOWN ? a.h : a.x), rows * brow_bytes);
     const rsrc_t rsa = make_rsrc(DOWN ? a.hs : a.xs, MXA ? rows * (uint32_t)P.nblocks * 4u : 0u);
 
+    // Processing order: from the range's first item boundary to its end, then
+    // the head piece before that boundary.  All workgroups thus start their
+    // whole items at step 0 and walk K in phase: measured, the chip streams
+    // ~10% faster per step than with every range at its own K offset.  Each
+    // piece is still summed in K order, so the results do not change.
+    const long n = x1 - x0;
+    const long rot = (x0 + nsteps - 1) / nsteps * nsteps < x1 ? (x0 + nsteps - 1) / nsteps * nsteps - x0 : 0;
+    auto unit_of = [&](long i) { return i < n - rot ? x0 + rot + i : x0 + i - (n - rot); };
+
     Source src;
-    set_source<FMT, DOWN, MXA>(src, P, sp, (int)(x0 / nsteps));
+    set_source<FMT, DOWN, MXA>(src, P, sp, (int)(unit_of(0) / nsteps));
 
     WFrag<FMT> wf[PD][2];
     u32x4 bst[PD][kBPass][SB];
     uint32_t sst[PD][kBPass];  // MX: the rows' block scales of a step (threads bc < 2)
-    // Loads of unit v into ring slot `slot`; a unit past the range loads zeros
-    // (offsets beyond every buffer), so every path issues the same loads and
-    // the compiler's wait counts stay exact.
-    auto issue = [&](int slot, long v) {
-        if (v >= src.ie && v < x1) set_source<FMT, DOWN, MXA>(src, P, sp, src.item + 1);
-        const bool ok = v < x1;
+    // Loads of the i-th unit of the sequence into ring slot `slot`; past the
+    // range the loads read zeros (offsets beyond every buffer), so every path
+    // issues the same loads and the compiler's wait counts stay exact.
+    auto issue = [&](int slot, long i) {
+        const bool ok = i < n;
+        const long v = ok ? unit_of(i) : src.ib;
+        if (ok && (v < src.ib || v >= src.ie)) set_source<FMT, DOWN, MXA>(src, P, sp, (int)(v / nsteps));
         const uint32_t step = (uint32_t)(v - src.ib);
 #pragma unroll
         for (int b = 0; b < SB; ++b) {
@@ -878,7 +888,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     };
 
     // The item being contracted.
-    int citem = (int)(x0 / nsteps);
+    int citem = (int)(unit_of(0) / nsteps);
     ItemDesc cd = describe_lds<DOWN>(P, sp, citem);
     ItemBias cbias = load_bias<DOWN>(P, cd, wave);
     long cib = (long)citem * nsteps;
@@ -888,9 +898,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
         for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    auto body = [&](int slot, int par, long u) {
-        issue((slot + PD - 1) % PD, u + PD - 1);
-        if (u >= x1) return;  // the last round of the unrolled loop runs past the range
+    auto body = [&](int slot, int par, long i) {
+        issue((slot + PD - 1) % PD, i + PD - 1);
+        if (i >= n) return;  // the last round of the unrolled loop runs past the range
+        const long u = unit_of(i);
         const int nmb = (cd.M + 15) / 16;
         uint8_t *buf = lds + par * BBUF;
         // After the previous step's barrier no wavefront still reads this buffer.
@@ -925,9 +936,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             default: contract<FMT, 4>(wf[slot], buf, acc); break;
             }
         }
-        // Item boundary: finish the item (or park its partial sums if it is
-        // cut at either end of the range) and move on to the next one.
-        if (u + 1 == cib + nsteps || u + 1 == x1) {
+        // End of a piece (an item boundary, the range's end or the end of the
+        // sequence): finish the item, or park its partial sums if it is cut at
+        // either end of the range, and move on to the next piece.
+        const long un = i + 1 < n ? unit_of(i + 1) : -1;
+        if (u + 1 == cib + nsteps || un != u + 1) {
             if (cib >= x0 && cib + nsteps <= x1) {
                 finish_item<DOWN, MXA>(P, cd, wave, acc, cbias);
             } else {
@@ -943,9 +956,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (u + 1 < x1) {
-                ++citem;
-                cib += nsteps;
+            if (un >= 0) {
+                citem = (int)(un / nsteps);
+                cib = (long)citem * nsteps;
                 cd = describe_lds<DOWN>(P, sp, citem);
                 cbias = load_bias<DOWN>(P, cd, wave);
             }
@@ -953,11 +966,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     };
 
 #pragma unroll
-    for (int j = 0; j < PD - 1; ++j) issue(j, x0 + j);
+    for (int j = 0; j < PD - 1; ++j) issue(j, j);
     constexpr int UN = PD % 2 ? 2 * PD : PD;  // ring slots and LDS parity repeat together
-    for (long u = x0; u < x1; u += UN) {
+    for (long i0 = 0; i0 < n; i0 += UN) {
 #pragma unroll
-        for (int j = 0; j < UN; ++j) body(j % PD, j & 1, u + j);
+        for (int j = 0; j < UN; ++j) body(j % PD, j & 1, i0 + j);
     }
     if (DOWN) record_cuts(P, pl, sp, x0, x1);
 }
