@@ -819,9 +819,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 
     // Processing order: from the range's first item boundary to its end, then
     // the head piece before that boundary.  All workgroups thus start their
-    // whole items at step 0 and walk K in phase: measured, the chip streams
-    // ~10% faster per step than with every range at its own K offset.  Each
-    // piece is still summed in K order, so the results do not change.
+    // whole items at step 0 and walk K in phase, which streams faster than
+    // ranges at scattered K offsets (measured: gate/up -2% at 32 experts,
+    // -1.2% at 128).  Each piece is still summed in K order, so the results do
+    // not change.
     const long n = x1 - x0;
     const long rot = (x0 + nsteps - 1) / nsteps * nsteps < x1 ? (x0 + nsteps - 1) / nsteps * nsteps - x0 : 0;
     auto unit_of = [&](long i) { return i < n - rot ? x0 + rot + i : x0 + i - (n - rot); };
