@@ -140,7 +140,8 @@ class Workload:
             wd = dict(routed_packed)
             wd["sh_gate"], wd["sh_s_gate"], wd["sh_s_up"] = moe.moe_pack_gate_up(
                 sh.fmt, cp["sh_gate"], cp["sh_up"], cp["sh_s_gate"], cp["sh_s_up"])
-            wd["sh_down"], wd["sh_s_down"] = moe.moe_pack_weights(sh.fmt, cp["sh_down"], cp["sh_s_down"])
+            pack_down = moe.moe_pack_down if wd.get("down_paired") else moe.moe_pack_weights
+            wd["sh_down"], wd["sh_s_down"] = pack_down(sh.fmt, cp["sh_down"], cp["sh_s_down"])
             self.wdicts.append(wd)
         torch.cuda.synchronize()
         nbytes = moe.moe_verify_workspace_size(self.wdicts[0], T, sh.k)

@@ -112,7 +112,9 @@ typedef enum {
  * (act 0, NULL biases, act_fmt 0) is the plain SwiGLU layer.
  * w_up == NULL means W_gate and W_up were packed together by
  * moe_pack_gate_up into w_gate (likewise sh_up == NULL with sh_gate set);
- * s_up (sh_s_up) still points to the up scales.
+ * s_up (sh_s_up) still points to the up scales.  down_paired = 1 means
+ * w_down and sh_down were packed by moe_pack_down (0: moe_pack_weights; any
+ * other value is MOE_ERR_INVALID_ARG).
  * Requirements: d % 32 == 0, d_ff % 32 == 0, and for FP8 d % 128 == 0 and
  * d_ff % 128 == 0; each packed matrix below 2 GiB; 16-byte aligned pointers.
  * Other shapes return MOE_ERR_UNSUPPORTED. */
@@ -127,6 +129,7 @@ typedef struct {
     float alpha, limit;
     const float *b_gate, *b_up, *b_down;
     int act_fmt; /* moe_actq_t */
+    int down_paired;
 } moe_weights_t;
 
 /* Routing of T tokens as produced by moe_route_topk + moe_expert_union
@@ -187,6 +190,20 @@ moe_status_t moe_packed_size(int fmt, int E, int N, int K, size_t *weight_bytes,
  */
 moe_status_t moe_pack_gate_up(int fmt, int E, int N, int K, const void *w_gate, const void *s_gate, const void *w_up,
                               const void *s_up, void *w_packed, void *s_gate_packed, void *s_up_packed, void *stream);
+
+/*
+ * W_down (E x N x K, N = d, K = d_ff) with the two 16-row tiles that one
+ * down wavefront streams interleaved: the streaming layout of
+ * moe_pack_weights, except that block (2p + j, kb), j = 0, 1, sits at byte
+ * offset ((p*Kp/128 + kb)*2 + j) * B, so the pair's blocks of one K step
+ * form one contiguous run.  Same sizes as moe_pack_weights; the scales are
+ * laid out exactly as moe_pack_weights lays them out.  A layer packed this
+ * way sets down_paired = 1 in moe_weights_t (for w_down and sh_down alike).
+ * Requirements as for moe_pack_weights, and N % 32 == 0
+ * (MOE_ERR_UNSUPPORTED otherwise).
+ */
+moe_status_t moe_pack_down(int fmt, int E, int N, int K, const void *w, const void *s, void *w_packed, void *s_packed,
+                           void *stream);
 moe_status_t moe_pack_weights(int fmt, int E, int N, int K, const void *w, const void *s, void *w_packed,
                               void *s_packed, void *stream);
 

@@ -13,6 +13,7 @@ the library has not been built, importing the functions that need it raises
     moe_expert_union(topk_idx, E)               -> Routing
     moe_verify_workspace_size(weights, T, k)    -> bytes
     moe_pack_weights(fmt, w, s)                 -> (w_packed, s_packed)   once per model load
+    moe_pack_gate_up / moe_pack_down            -> the paired layouts pack_layer uses by default
     moe_verify_layer(x, weights, routing)       -> y   (weights packed)
     moe_select_tree(parent, P, pred, E, budget) -> (selected, marginal_cost)
     moe_route_union(logits, k, score)           -> Routing   (route + union in one call)
@@ -38,8 +39,8 @@ MOE_ACT_SWIGLU, MOE_ACT_SWIGLU_OAI = 0, 1
 MOE_ACTQ_BF16, MOE_ACTQ_MXFP8 = 0, 1
 
 EXPORTED = ("moe_route_topk", "moe_route_union", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
-            "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_pack_gate_up", "moe_select_tree",
-            "moe_status_string", "moe_last_error")
+            "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_pack_gate_up", "moe_pack_down",
+            "moe_select_tree", "moe_status_string", "moe_last_error")
 
 
 class MoeError(RuntimeError):
@@ -53,7 +54,8 @@ class moe_weights_t(C.Structure):
         (n, C.c_void_p) for n in ("w_gate", "w_up", "w_down", "s_gate", "s_up", "s_down", "sh_gate", "sh_up",
                                   "sh_down", "sh_s_gate", "sh_s_up", "sh_s_down")] + [
         ("act", C.c_int), ("alpha", C.c_float), ("limit", C.c_float),
-        ("b_gate", C.c_void_p), ("b_up", C.c_void_p), ("b_down", C.c_void_p), ("act_fmt", C.c_int)]
+        ("b_gate", C.c_void_p), ("b_up", C.c_void_p), ("b_down", C.c_void_p), ("act_fmt", C.c_int),
+        ("down_paired", C.c_int)]
 
 
 class moe_routing_t(C.Structure):
@@ -87,13 +89,14 @@ def lib() -> C.CDLL:
             L.moe_packed_size.argtypes = [i, i, i, i, C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]
             L.moe_pack_weights.argtypes = [i, i, i, i, p, p, p, p, p]
             L.moe_pack_gate_up.argtypes = [i, i, i, i, p, p, p, p, p, p, p, p]
+            L.moe_pack_down.argtypes = [i, i, i, i, p, p, p, p, p]
             L.moe_select_tree.argtypes = [i, p, p, i, i, p, i, p, i, C.c_double, C.c_double, i, p, p, p]
             L.moe_status_string.argtypes = [i]
             L.moe_status_string.restype = C.c_char_p
             L.moe_last_error.restype = C.c_char_p
             for f in ("moe_route_topk", "moe_route_union", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
                       "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_pack_gate_up",
-                      "moe_select_tree"):
+                      "moe_pack_down", "moe_select_tree"):
                 getattr(L, f).restype = i
             _lib = L
     return _lib
@@ -300,11 +303,28 @@ def moe_pack_gate_up(fmt: int, w_gate, w_up, s_gate=None, s_up=None):
     return wp, sgp, sup
 
 
-def pack_layer(layer: dict, pair: bool = True) -> dict:
+def moe_pack_down(fmt: int, w, s=None):
+    """Pack stacked device W_down [E, N, K(/2)] (+ scales) with each wavefront's two row tiles
+    interleaved.  Returns (w_packed, s_packed) like moe_pack_weights."""
+    torch = _torch()
+    E, N = w.shape[0], w.shape[1]
+    K = w.shape[2] * (2 if fmt == MOE_W_MXFP4 else 1)
+    wb, sb = moe_packed_size(fmt, E, N, K)
+    wp = torch.empty(wb, dtype=torch.uint8, device=w.device)
+    sp = torch.empty(sb, dtype=torch.uint8, device=w.device) if sb else None
+    _check("moe_pack_down", lib().moe_pack_down(fmt, E, N, K, _dev_ptr(w, "w"), _dev_ptr(s, "s"),
+                                                  _dev_ptr(wp, "w_packed"), _dev_ptr(sp, "s_packed"), _stream(w)))
+    return wp, sp
+
+
+def pack_layer(layer: dict, pair: bool = True, down_pair: bool = True) -> dict:
     """A layer dict (interchange layout, device tensors) with every matrix packed; with `pair`,
-    W_gate and W_up as one pair (moe_pack_gate_up; the dict then has no "up" / "sh_up" entry)."""
+    W_gate and W_up as one pair (moe_pack_gate_up; the dict then has no "up" / "sh_up" entry);
+    with `down_pair`, W_down by moe_pack_down (the dict then has down_paired = 1)."""
     out = {k: layer[k] for k in ("fmt", "d", "d_ff", "act", "alpha", "limit", "b_gate", "b_up", "b_down", "act_fmt")
            if k in layer}
+    if down_pair:
+        out["down_paired"] = 1
     out["E"] = int(layer.get("E", layer["gate"].shape[0]))
     fmt = int(layer["fmt"])
     for prefix in ("", "sh_"):
@@ -319,7 +339,8 @@ def pack_layer(layer: dict, pair: bool = True) -> dict:
         for name in names:
             if layer.get(prefix + name) is None:
                 continue
-            wp, sp = moe_pack_weights(fmt, layer[prefix + name], layer.get(prefix + "s_" + name))
+            pack = moe_pack_down if name == "down" and down_pair else moe_pack_weights
+            wp, sp = pack(fmt, layer[prefix + name], layer.get(prefix + "s_" + name))
             out[prefix + name] = wp
             if sp is not None:
                 out[prefix + "s_" + name] = sp
@@ -335,6 +356,7 @@ def weights_struct(w: dict) -> moe_weights_t:
     torch = _torch()
     s.act = int(w.get("act", MOE_ACT_SWIGLU))
     s.act_fmt = int(w.get("act_fmt", MOE_ACTQ_BF16))
+    s.down_paired = int(w.get("down_paired", 0))
     s.alpha, s.limit = float(w.get("alpha", 1.702)), float(w.get("limit", 7.0))
     for name in ("b_gate", "b_up", "b_down"):
         b = w.get(name)

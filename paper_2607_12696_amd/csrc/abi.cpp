@@ -60,6 +60,7 @@ moe_status_t check_weights(const moe_weights_t *w)
         if (p && !aligned(p, 16)) return MOE_ERR_INVALID_ARG;
     if (w->act_fmt != MOE_ACTQ_BF16 && w->act_fmt != MOE_ACTQ_MXFP8) return MOE_ERR_INVALID_ARG;
     if (w->act_fmt == MOE_ACTQ_MXFP8 && w->fmt != MOE_W_MXFP4) return MOE_ERR_UNSUPPORTED;
+    if (w->down_paired != 0 && w->down_paired != 1) return MOE_ERR_INVALID_ARG;
     return MOE_OK;
 }
 
@@ -205,6 +206,7 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     a.gu_pair = w->w_up == nullptr;
     a.sh_gu_pair = w->sh_gate != nullptr && w->sh_up == nullptr;
     a.w_down = static_cast<const uint8_t *>(w->w_down);
+    a.down_pair = w->down_paired == 1;
     a.s_gate = w->s_gate;
     a.s_up = w->s_up;
     a.s_down = w->s_down;
@@ -274,6 +276,17 @@ moe_status_t moe_pack_weights(int fmt, int E, int N, int K, const void *w, const
     if (!w || !w_packed || w == w_packed || !aligned(w, 16) || !aligned(w_packed, 16)) return MOE_ERR_INVALID_ARG;
     if (fmt != MOE_W_BF16 && (!s || !s_packed || s == s_packed)) return MOE_ERR_INVALID_ARG;
     return from_hip(ecospec::launch_pack(fmt, E, N, K, w, s, w_packed, s_packed, (hipStream_t)stream));
+}
+
+moe_status_t moe_pack_down(int fmt, int E, int N, int K, const void *w, const void *s, void *w_packed, void *s_packed,
+                           void *stream)
+{
+    const moe_status_t st = check_pack(fmt, E, N, K);
+    if (st != MOE_OK) return st;
+    if (N % 32) return MOE_ERR_UNSUPPORTED;  // whole pairs of 16-row tiles
+    if (!w || !w_packed || w == w_packed || !aligned(w, 16) || !aligned(w_packed, 16)) return MOE_ERR_INVALID_ARG;
+    if (fmt != MOE_W_BF16 && (!s || !s_packed || s == s_packed)) return MOE_ERR_INVALID_ARG;
+    return from_hip(ecospec::launch_pack_down(fmt, E, N, K, w, s, w_packed, s_packed, (hipStream_t)stream));
 }
 
 moe_status_t moe_pack_gate_up(int fmt, int E, int N, int K, const void *w_gate, const void *s_gate, const void *w_up,

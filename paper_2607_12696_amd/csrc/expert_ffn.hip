@@ -350,7 +350,8 @@ struct ItemDesc {
     int M;                   // tokens in the group (<= 64)
     int e;                   // expert id (-1: the shared expert)
     bool shared;
-    bool pair;               // gate/up: the two matrices packed as one pair at wa (wb == wa)
+    bool pair;               // gate/up: the two matrices packed as one pair at wa (wb == wa);
+                             // down: the wavefront's two row tiles interleaved per block
 };
 
 // What a workgroup needs to know about an item, from the schedule in LDS.
@@ -385,6 +386,7 @@ __device__ __forceinline__ ItemDesc describe_lds(const FfnParams &P, const Split
     } else {
         d.wa = d.wb = (d.shared ? a.sh_down : a.w_down) + e * mat;
         d.sa = d.sb = d.shared ? a.sh_s_down : sptr(a.s_down);
+        d.pair = a.down_pair;
     }
     return d;
 }
@@ -548,7 +550,13 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
         (uint32_t)((size_t)P.N * nblocks * kMacroK * (FMT == FMT_BF16 ? 2 : 1) / (FMT == FMT_MXFP4 ? 2 : 1));
     const int row0 = tile_row<DOWN>(d, wave, 0), row1 = tile_row<DOWN>(d, wave, 1);
     const bool arow_ok = row0 < P.N;
-    if (d.pair) {
+    if (DOWN && d.pair) {
+        // Row tiles 2p and 2p + 1 interleaved block by block: one contiguous run per block.
+        src.ra0 = src.ra1 = make_rsrc(d.wa, mat_bytes);
+        src.kstride = 2u * BLK;
+        src.a0 = arow_ok ? (uint32_t)(row0 / 32) * nblocks * 2u * BLK + lane * 16u : kOff;
+        src.a1 = arow_ok ? src.a0 + BLK : kOff;
+    } else if (d.pair) {
         // Gate block then up block of the same rows: one contiguous run per block.
         src.ra0 = src.ra1 = make_rsrc(d.wa, 2u * mat_bytes);
         src.kstride = 2u * BLK;

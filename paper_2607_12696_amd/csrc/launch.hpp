@@ -30,6 +30,7 @@ struct VerifyArgs {
     int fmt, d, d_ff, E, T, k;
     const uint8_t *w_gate, *w_up, *w_down;  // routed experts, stacked [E]
     bool gu_pair, sh_gu_pair;               // W_gate and W_up packed as one pair in w_gate / sh_gate
+    bool down_pair;                         // W_down (and sh_down) packed with row tiles 2p, 2p+1 interleaved
     const void *s_gate, *s_up, *s_down;
     const uint8_t *sh_gate, *sh_up, *sh_down;  // shared expert or null
     const void *sh_s_gate, *sh_s_up, *sh_s_down;
@@ -85,5 +86,7 @@ hipError_t launch_pack_gate_up(int fmt, int E, int N, int K, const void *wg, con
                                const void *su, void *wp, void *sgp, void *sup, hipStream_t stream);
 hipError_t launch_pack(int fmt, int E, int N, int K, const void *w, const void *s, void *wp, void *sp,
                        hipStream_t stream);
+hipError_t launch_pack_down(int fmt, int E, int N, int K, const void *w, const void *s, void *wp, void *sp,
+                            hipStream_t stream);
 
 }  // namespace ecospec

@@ -15,6 +15,9 @@
 // (rb, kb) of the pair is the gate block followed by the up block, so a
 // wavefront reads both tiles of a step as one contiguous run (one stream
 // instead of two, measured 4% more bandwidth in the kernel's geometry).
+// W_down likewise (moe_pack_down): row tiles 2p and 2p + 1 (the two tiles of
+// one down wavefront) are interleaved block by block, block (2p + j, kb) at
+// ((p * Kp/128 + kb) * 2 + j) * B.
 //
 // MXFP4 scales move to the same blocking, four blocks to a 256-byte quad: in
 // quad q of row tile rb, the 4 bytes at offset 4*l (l = c + 16*g) are the
@@ -30,10 +33,11 @@ namespace ecospec {
 // One thread writes one 16-byte lane vector of the packed matrix.  pair = 2
 // packs W_gate and W_up together: block (rb, kb) of the pair holds the gate
 // block and then the up block (`which` = 0 / 1), so the verify kernel reads
-// both tiles of a step as one contiguous run.
+// both tiles of a step as one contiguous run.  tile_pairs = 1 interleaves row
+// tiles 2p and 2p + 1 of one matrix the same way (pair = 1).
 __global__ __launch_bounds__(256) void pack_weights_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict__ dst,
                                                            int E, int N, int K, int num, int den, int vecs, int pair,
-                                                           int which)
+                                                           int which, int tile_pairs)
 {
     const int nkb = (K + 127) / 128;
     const size_t per_block = (size_t)vecs * 64;  // lane vectors per block
@@ -55,8 +59,9 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const uint8_t *__rest
             const uint8_t *p = src + e * src_mat + (size_t)(rb * 16 + c) * src_row + (size_t)k0 * num / den;
             v = *reinterpret_cast<const u32x4 *>(p);
         }
-        uint8_t *o = dst + e * dst_mat + (((size_t)rb * nkb + kb) * pair + which) * ((size_t)vecs * 1024) +
-                     (size_t)i * 1024 + (size_t)l * 16;
+        const size_t blk = tile_pairs ? ((size_t)(rb >> 1) * nkb + kb) * 2 + (rb & 1)
+                                      : ((size_t)rb * nkb + kb) * pair + which;
+        uint8_t *o = dst + e * dst_mat + blk * ((size_t)vecs * 1024) + (size_t)i * 1024 + (size_t)l * 16;
         *reinterpret_cast<u32x4 *>(o) = v;
     }
 }
@@ -94,13 +99,13 @@ size_t packed_scale_bytes(int fmt, int N, int K)
 }
 
 static hipError_t pack_matrix(int fmt, int E, int N, int K, const void *w, void *wp, int pair, int which,
-                              hipStream_t stream)
+                              hipStream_t stream, int tile_pairs = 0)
 {
     const int num = fmt == 0 ? 2 : 1, den = fmt == 2 ? 2 : 1, vecs = fmt == 0 ? 4 : fmt == 1 ? 2 : 1;
     const size_t vec_total = (size_t)E * (N / 16) * ((K + 127) / 128) * vecs * 64;
     const int grid = (int)((vec_total + 255) / 256 < 65536 ? (vec_total + 255) / 256 : 65536);
     hipLaunchKernelGGL(pack_weights_kernel, dim3(grid), dim3(256), 0, stream, static_cast<const uint8_t *>(w),
-                       static_cast<uint8_t *>(wp), E, N, K, num, den, vecs, pair, which);
+                       static_cast<uint8_t *>(wp), E, N, K, num, den, vecs, pair, which, tile_pairs);
     return hipGetLastError();
 }
 
@@ -124,6 +129,14 @@ hipError_t launch_pack(int fmt, int E, int N, int K, const void *w, const void *
     hipError_t err = pack_matrix(fmt, E, N, K, w, wp, 1, 0, stream);
     if (err != hipSuccess) return err;
     return pack_scales(fmt, E, N, K, s, sp, stream);
+}
+
+hipError_t launch_pack_down(int fmt, int E, int N, int K, const void *w, const void *s, void *wp, void *sp,
+                            hipStream_t stream)
+{
+    hipError_t err = pack_matrix(fmt, E, N, K, w, wp, 1, 0, stream, 1);
+    if (err == hipSuccess) err = pack_scales(fmt, E, N, K, s, sp, stream);
+    return err;
 }
 
 hipError_t launch_pack_gate_up(int fmt, int E, int N, int K, const void *wg, const void *sg, const void *wu,

@@ -203,6 +203,26 @@ def test_pack_gate_up_rejects():
     assert L.moe_pack_gate_up(*bad) == moe.MOE_ERR_UNSUPPORTED
 
 
+def test_pack_down_rejects():
+    L = moe.lib()
+    args = [1, 2, 256, 256, FAKE, FAKE, 2 * FAKE, 3 * FAKE, None]
+    bad = list(args); bad[4] = None  # no w
+    assert L.moe_pack_down(*bad) == moe.MOE_ERR_INVALID_ARG
+    bad = list(args); bad[6] = FAKE  # packed buffer aliases w
+    assert L.moe_pack_down(*bad) == moe.MOE_ERR_INVALID_ARG
+    bad = list(args); bad[7] = None  # FP8 needs its scales
+    assert L.moe_pack_down(*bad) == moe.MOE_ERR_INVALID_ARG
+    bad = [0, 2, 48, 256, FAKE, None, 2 * FAKE, None, None]  # 3 row tiles: no whole pairs
+    assert L.moe_pack_down(*bad) == moe.MOE_ERR_UNSUPPORTED
+
+
+def test_down_paired_flag_validated():
+    w = _weights()
+    for v, st in ((0, moe.MOE_OK), (1, moe.MOE_OK), (2, moe.MOE_ERR_INVALID_ARG), (-1, moe.MOE_ERR_INVALID_ARG)):
+        w.down_paired = v
+        assert _ws(w, 8, 2)[0] == st
+
+
 def test_verify_layer_rejects_outputs_past_2gib():
     # O (fp32 rows of T*k + T slots x d) is addressed through a 32-bit buffer range: DS shape with T = 8400
     # gives 75600 x 7168 x 4 bytes = 2.17 GB; every other limit (groups, H, x) still holds.

@@ -30,10 +30,11 @@ def note(msg):
     sys.stdout.flush()
 
 
-def to_dev(layer, pair=True):
+def to_dev(layer, pair=True, down_pair=True):
     """Device copy of an interchange-layout layer, packed for the verify kernels (W_gate and W_up as one
-    pair unless pair=False)."""
-    return moe.pack_layer({k: (v.to(DEV) if hasattr(v, "to") else v) for k, v in layer.items()}, pair=pair)
+    pair unless pair=False; W_down with its row tiles paired unless down_pair=False)."""
+    return moe.pack_layer({k: (v.to(DEV) if hasattr(v, "to") else v) for k, v in layer.items()}, pair=pair,
+                          down_pair=down_pair)
 
 
 def y_err(y_gpu, y_ref):
@@ -475,6 +476,46 @@ def test_pack_gate_up_pair_layout(fmt, N, K):
         assert np.array_equal(sup.cpu().numpy(), _expected_packed(fmt, wu, su)[1])
 
 
+@pytest.mark.parametrize("fmt,N,K", [(0, 32, 96), (1, 256, 384), (2, 64, 160), (2, 96, 640), (0, 64, 2880)])
+def test_pack_down_pair_layout(fmt, N, K):
+    # Blocks (2p + j, kb) of the standard layout, reordered to ((p * Kp/128 + kb) * 2 + j); scales unchanged.
+    note(f"pack down pair fmt={fmt} N={N} K={K}")
+    E = 2
+    mk = {0: synth.weights_bf16, 1: synth.weights_fp8_b128, 2: synth.weights_mxfp4}[fmt]
+    w, s = (mk(E, N, K, seed=4, tag="d"), None) if fmt == 0 else mk(E, N, K, seed=4, tag="d")
+    wp, sp = moe.moe_pack_down(fmt, w.to(DEV), None if s is None else s.to(DEV))
+    torch.cuda.synchronize()
+    ew, es = _expected_packed(fmt, w, s)
+    blk = {0: 4096, 1: 2048, 2: 1024}[fmt]
+    nkb = (K + 127) // 128
+    ew = ew.reshape(E, N // 32, 2, nkb, blk).transpose(0, 1, 3, 2, 4).reshape(-1)
+    assert np.array_equal(wp.cpu().numpy(), ew)
+    if fmt:
+        assert np.array_equal(sp.cpu().numpy(), es)
+
+
+@pytest.mark.parametrize("name", ["toy", "fp8", "fp8_wide", "mxfp4", "bf16_tail", "one"])
+@pytest.mark.parametrize("T", [5, 64, 130])
+def test_standard_and_paired_down_layouts_agree(name, T):
+    # W_down packed by moe_pack_weights or moe_pack_down: the same arithmetic in the same order, so the
+    # same bits (the shared expert's W_down is paired too where the shape has one).
+    sh = SMALL[name]
+    note(f"down layouts shape={name} T={T}")
+    layer = small_layer(name)
+    x = synth.activations(T, sh.d, seed=T + 19).to(DEV)
+    lg = synth.logits_scattered(T, sh.E, seed=T + 18).to(DEV)
+    for pair in (True, False):
+        y_std, _ = moe.moe_verify_step(x, lg, to_dev(layer, pair=pair, down_pair=False), sh.k, sh.score)
+        y_dp, _ = moe.moe_verify_step(x, lg, to_dev(layer, pair=pair, down_pair=True), sh.k, sh.score)
+        torch.cuda.synchronize()
+        assert torch.equal(y_std, y_dp)
+    if sh.fmt == synth.FMT_MXFP4:
+        y_std, _ = moe.moe_verify_step(x, lg, dict(to_dev(layer, down_pair=False), act_fmt=1), sh.k, sh.score)
+        y_dp, _ = moe.moe_verify_step(x, lg, dict(to_dev(layer, down_pair=True), act_fmt=1), sh.k, sh.score)
+        torch.cuda.synchronize()
+        assert torch.equal(y_std, y_dp)
+
+
 @pytest.mark.parametrize("name", ["toy", "fp8", "mxfp4"])
 def test_verify_is_deterministic(name):
     sh = SMALL[name]
@@ -662,6 +703,27 @@ FULL_CASES = [
     ("qwen", 256, "clustered", None, [7, 200]),
     ("gpt", 512, "exact", 32, [1, 300, 511]),
 ]
+
+
+@pytest.mark.parametrize("name,T", [("ds", 64), ("qwen", 256), ("gpt", 64)])
+def test_full_paired_down_layout_is_bit_identical(name, T):
+    # Full-size W_down packed by moe_pack_down (routed and shared; the default packing) gives the standard
+    # layout's y (moe_pack_weights) bit for bit.
+    sh = synth.SHAPES[name]
+    raw, dl = full_layer(name)
+    assert dl["down_paired"] == 1
+    note(f"full {name} paired down T={T}")
+    std = dict(dl, down_paired=0)
+    for prefix in ("", "sh_"):
+        if raw.get(prefix + "down") is not None:
+            std[prefix + "down"], _ = moe.moe_pack_weights(sh.fmt, raw[prefix + "down"], raw.get(prefix + "s_down"))
+    x = synth.activations(T, sh.d, seed=51).to(DEV)
+    lg = routed_logits("scattered", T, sh, seed=52).to(DEV)
+    y0, _ = moe.moe_verify_step(x, lg, std, sh.k, sh.score)
+    y1, _ = moe.moe_verify_step(x, lg, dl, sh.k, sh.score)
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1)
+    del std
 
 
 def test_full_gpt_oss_variant_sampled_rows():
