@@ -20,7 +20,9 @@
 // Streaming.  Weights are read in the packed layout (pack.hip): each macro
 // step of a 16-row tile is 1-4 KiB of contiguous memory, fetched with 16-byte
 // buffer loads that are already the A operand of v_mfma_f32_16x16x32_bf16
-// (weights on the 16-row side, tokens on the 16-column side).  FP8 and MXFP4
+// (weights on the 16-row side, tokens on the 16-column side).  In the paired
+// layouts (gate with up, or a down wavefront's two tiles) a wavefront's two
+// tiles of a step are one contiguous run.  FP8 and MXFP4
 // codes are decoded exactly to bf16 in registers (v_cvt_scalef32_pk_bf16_fp8
 // with unit scale; v_cvt_scalef32_pk_bf16_fp4 with the e8m0 power of two); FP8
 // 128x128 block scales multiply the fp32 partial sum of each macro step (one
@@ -59,7 +61,9 @@
 #include "device.hpp"
 #include "launch.hpp"
 
-// Compile-time tuning: macro steps in flight per wavefront, per format.
+// Compile-time tuning: macro steps in flight per wavefront, per format (each
+// the fastest measured: bf16 and MXFP4 steps are 8 KiB per wavefront, MXFP4
+// also with the decode's registers; FP8 steps 4 KiB).
 #ifndef ECOSPEC_PD_BF16
 #define ECOSPEC_PD_BF16 2
 #endif
@@ -67,7 +71,7 @@
 #define ECOSPEC_PD_FP8 3
 #endif
 #ifndef ECOSPEC_PD_FP4
-#define ECOSPEC_PD_FP4 3
+#define ECOSPEC_PD_FP4 2
 #endif
 #ifndef ECOSPEC_WG_WAVES
 #define ECOSPEC_WG_WAVES 8
