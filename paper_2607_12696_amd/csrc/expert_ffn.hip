@@ -250,12 +250,28 @@ __device__ __forceinline__ Plan load_plan(const FfnParams &P)
 // the range ends, as an equal split does.
 
 // Relative per-step cost of a token group: a weight part set by the bytes a
-// step streams and a contraction part per 16-token block (measured on the FP8
-// kernels, scaled by bytes per weight for the other formats).
-template <int FMT>
+// step streams and a contraction part per 16-token block.  The weight parts
+// are the fastest measured under uneven token counts per expert (clustered
+// routing, T = 64 and 256) per format and activation mode.
+#ifndef ECOSPEC_COST_BF16
+#define ECOSPEC_COST_BF16 29
+#endif
+#ifndef ECOSPEC_COST_FP8
+#define ECOSPEC_COST_FP8 13
+#endif
+#ifndef ECOSPEC_COST_FP4
+#define ECOSPEC_COST_FP4 8
+#endif
+#ifndef ECOSPEC_COST_FP4_MX
+#define ECOSPEC_COST_FP4_MX 16
+#endif
+template <int FMT, bool MXA>
 __device__ __forceinline__ int group_cost(int M)
 {
-    constexpr int A = FMT == FMT_BF16 ? 29 : FMT == FMT_FP8 ? 13 : 5;
+    constexpr int A = FMT == FMT_BF16 ? ECOSPEC_COST_BF16
+                    : FMT == FMT_FP8  ? ECOSPEC_COST_FP8
+                    : MXA             ? ECOSPEC_COST_FP4_MX
+                                      : ECOSPEC_COST_FP4;
     return A + 3 * ((M + 15) / 16);
 }
 
@@ -275,7 +291,7 @@ struct Split {
 };
 
 // Fills sp.cw and the groups' metadata for the launch (whole workgroup).
-template <int FMT>
+template <int FMT, bool MXA>
 __device__ __forceinline__ void build_costs(const FfnParams &P, const Plan &pl, Split &sp)
 {
     const VerifyArgs &a = P.a;
@@ -293,7 +309,7 @@ __device__ __forceinline__ void build_costs(const FfnParams &P, const Plan &pl, 
             sp.gM[g] = min(kTokGroup, Mu - tg * kTokGroup);
             sp.gp0[g] = (shared ? S : a.offsets[u]) + tg * kTokGroup;
             sp.ge[g] = shared ? -1 : a.union_ids[u];
-            c = group_cost<FMT>(sp.gM[g]);
+            c = group_cost<FMT, MXA>(sp.gM[g]);
         }
         int tot = 0;
         const int ex = block_exclusive_scan(c, sp.wave_tot, &tot);
@@ -812,7 +828,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const Plan pl = load_plan(P);
     const int nsteps = P.nsteps, K = P.K;
     __shared__ Split sp;
-    build_costs<FMT>(P, pl, sp);
+    build_costs<FMT, MXA>(P, pl, sp);
     build_bounds(sp, pl.n_groups, (long)P.nbands * nsteps, P.workers);
     long x0, x1;
     worker_range(sp, w, x0, x1);
