@@ -109,7 +109,9 @@ typedef enum {
  * The shared expert takes the activation but no biases.  act_fmt selects the
  * precision of the projection inputs (moe_actq_t; MOE_ACTQ_MXFP8 needs
  * MOE_W_MXFP4, else MOE_ERR_UNSUPPORTED).  A zero-initialised struct tail
- * (act 0, NULL biases, act_fmt 0) is the plain SwiGLU layer.
+ * (act 0, NULL biases, act_fmt 0, down_paired 0) is the plain SwiGLU layer
+ * with W_down packed by moe_pack_weights; callers zero-initialise the whole
+ * struct, since fields are only ever added at its end.
  * w_up == NULL means W_gate and W_up were packed together by
  * moe_pack_gate_up into w_gate (likewise sh_up == NULL with sh_gate set);
  * s_up (sh_s_up) still points to the up scales.  down_paired = 1 means
