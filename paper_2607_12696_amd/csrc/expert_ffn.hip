@@ -60,6 +60,7 @@
 // order (each 128-element chunk as four 32-byte lane runs).
 #include "device.hpp"
 #include "launch.hpp"
+#include "split.hpp"
 
 // Compile-time tuning: macro steps in flight per wavefront, per format (each
 // the fastest measured: bf16 and MXFP4 steps are 8 KiB per wavefront, MXFP4
@@ -324,17 +325,7 @@ __device__ __forceinline__ void build_costs(const FfnParams &P, const Plan &pl, 
 // search over the groups' cost prefix.
 __device__ __forceinline__ long first_unit(const Split &sp, int n_groups, long K, long W, long long target)
 {
-    const long long C = (long long)sp.cw[n_groups] * K;
-    if (target <= 0) return 0;
-    if (target >= C * W) return (long)n_groups * K;
-    int lo = 0, hi = n_groups - 1;  // last group g with cw[g] * K * W < target
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if ((long long)sp.cw[mid] * K * W < target) lo = mid; else hi = mid - 1;
-    }
-    const long long base = (long long)sp.cw[lo] * K * W, cg = sp.cw[lo + 1] - sp.cw[lo];
-    const long long r = (target - base + cg * W - 1) / (cg * W);
-    return r >= K ? (long)(lo + 1) * K : (long)lo * K + (long)r;
+    return split::first_unit(sp.cw, n_groups, K, W, target);
 }
 
 // Every workgroup's first unit, into sp.bound (whole workgroup).
@@ -355,10 +346,7 @@ __device__ __forceinline__ void worker_range(const Split &sp, int w, long &x0, l
 // Workgroup whose range holds unit x.
 __device__ __forceinline__ int owner_of(const Split &sp, int n_groups, long K, int W, long x)
 {
-    const int g = (int)(x / K);
-    const long long cg = sp.cw[g + 1] - sp.cw[g];
-    const long long px = (long long)sp.cw[g] * K + (x - (long long)g * K) * cg;
-    return (int)(px * W / ((long long)sp.cw[n_groups] * K));
+    return split::owner_of(sp.cw, n_groups, K, W, x);
 }
 
 // What a workgroup needs to know about one item.
@@ -731,19 +719,7 @@ __device__ __forceinline__ void contract_mx(const WFrag<FMT_MXFP4> (&wv)[2], con
 __device__ __forceinline__ long long contributors(const FfnParams &P, const Plan &pl, const Split &sp, long ib,
                                                   long ie)
 {
-    const long KU = (long)P.nbands * P.nsteps;
-    const int w0 = owner_of(sp, pl.n_groups, KU, P.workers, ib);
-    const int w1 = owner_of(sp, pl.n_groups, KU, P.workers, ie - 1);
-    long long packed = 0;
-    int cnt = 0;
-    for (int v = w0; v <= w1; ++v) {
-        long v0, v1;
-        worker_range(sp, v, v0, v1);
-        if (v0 >= v1) continue;
-        if (cnt < 3) packed |= (long long)(2 * v + ((ib <= v0 && v0 < ie) ? 0 : 1)) << (20 * cnt);
-        ++cnt;
-    }
-    return cnt <= 3 ? ((1ll << 62) | ((long long)cnt << 60) | packed) : (long long)((w0 << 16) | w1);
+    return split::contributors(sp.cw, sp.bound, pl.n_groups, (long)P.nbands * P.nsteps, P.workers, ib, ie);
 }
 
 // Down launch: for the combine kernel, how each item this range touches is to
@@ -775,15 +751,13 @@ __device__ __forceinline__ void write_fix_record(const FfnParams &P, const Plan 
 {
     long long r[4] = {-1, 0, 0, 0};
     const long ns = P.nsteps;
-    if (x0 < x1) {
-        const long item = x0 / ns, ib = item * ns, ie = ib + ns;
-        if (ib < x0 && ie <= x1) {
-            const int gi = (int)(item / P.nbands);
-            r[0] = item;
-            r[1] = contributors(P, pl, sp, ib, ie);
-            r[2] = (long long)(uint32_t)sp.gp0[gi] | ((long long)(sp.ge[gi] + 1) << 32);
-            r[3] = sp.gM[gi];
-        }
+    const long item = split::finished_item(x0, x1, ns);
+    if (item >= 0) {
+        const int gi = (int)(item / P.nbands);
+        r[0] = item;
+        r[1] = contributors(P, pl, sp, item * ns, item * ns + ns);
+        r[2] = (long long)(uint32_t)sp.gp0[gi] | ((long long)(sp.ge[gi] + 1) << 32);
+        r[3] = sp.gM[gi];
     }
     long long *dst = P.fix + 4 * (size_t)w;
     dst[0] = r[0];
@@ -1064,15 +1038,15 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
             for (int mb = 0; mb < kMB; ++mb)
                 if (mb < nmb) acc[t][mb] += *reinterpret_cast<const f32x4 *>(src + partial_offset<DOWN>(wave, t, mb, lane));
     };
-    if (cut >> 62) {
+    if (split::packed_contributors(cut)) {
         // Up to three contributors: every load is issued before the first sum (one round trip;
         // absent contributors and dead token blocks read zeros), then added in workgroup order.
-        const int cnt = (int)((cut >> 60) & 3);
+        const int cnt = split::packed_count(cut);
         const rsrc_t rp = make_rsrc(P.partials, (uint32_t)((size_t)P.workers * 2 * kPartialFloats * 4));
         f32x4 v[3][2][kMB];
 #pragma unroll
         for (int i = 0; i < 3; ++i) {
-            const uint32_t slot = (uint32_t)((cut >> (20 * i)) & 0xfffff);
+            const uint32_t slot = (uint32_t)split::packed_slot(cut, i);
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -1092,10 +1066,10 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
     } else {
         // More than three contributors: each one's slot follows from its range.
         const long ib = (long)item * P.nsteps, ie = ib + P.nsteps;
-        for (int v = (int)(cut >> 16) & 0xffff, w1 = (int)cut & 0xffff; v <= w1; ++v) {
-            const long v0 = (long)ld_s64(P.ranges + 2 * v), v1 = (long)ld_s64(P.ranges + 2 * v + 1);
-            if (v0 >= v1) continue;
-            add(P.partials + ((size_t)v * 2 + ((ib <= v0 && v0 < ie) ? 0 : 1)) * kPartialFloats);
+        for (int v = split::first_worker(cut), w1 = split::last_worker(cut); v <= w1; ++v) {
+            const int slot = split::piece_slot(v, (long)ld_s64(P.ranges + 2 * v), (long)ld_s64(P.ranges + 2 * v + 1),
+                                               ib, ie);
+            if (slot >= 0) add(P.partials + (size_t)slot * kPartialFloats);
         }
     }
     finish_item<DOWN, MXA>(P, d, wave, acc, bias);
@@ -1177,29 +1151,27 @@ __global__ __launch_bounds__(256) void plan_kernel(VerifyArgs a, int32_t *plan)
 __device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, long item, int p, int r, int c)
 {
     const int off = r * D.band_rows + c % D.band_rows;  // partial_offset<true>
-    if (cut < 0 || (cut >> 62)) {
+    if (cut < 0 || split::packed_contributors(cut)) {
         // A whole item's O row, or up to three parked partial sums: all loads issued at once
         // (absent ones read zeros) and added in workgroup order.
-        const int cnt = cut < 0 ? 0 : (int)((cut >> 60) & 3);
+        const int cnt = cut < 0 ? 0 : split::packed_count(cut);
         const rsrc_t ro = make_rsrc(D.a.o, (uint32_t)((size_t)(D.a.T * D.a.k + (D.a.sh_gate ? D.a.T : 0)) * D.a.d * 4));
         const rsrc_t rp = make_rsrc(D.partials, (uint32_t)((size_t)D.workers * 2 * kPartialFloats * 4));
         const f32x4 v0 = __builtin_bit_cast(
             f32x4, cut < 0 ? load16<0>(ro, (uint32_t)((size_t)p * D.a.d + c) * 4u)
-                           : load16<0>(rp, (uint32_t)((cut & 0xfffff) * kPartialFloats + off) * 4u));
+                           : load16<0>(rp, (uint32_t)(split::packed_slot(cut, 0) * kPartialFloats + off) * 4u));
         const f32x4 v1 = __builtin_bit_cast(
-            f32x4, load16<0>(rp, cnt > 1 ? (uint32_t)(((cut >> 20) & 0xfffff) * kPartialFloats + off) * 4u : kOff));
+            f32x4, load16<0>(rp, cnt > 1 ? (uint32_t)(split::packed_slot(cut, 1) * kPartialFloats + off) * 4u : kOff));
         const f32x4 v2 = __builtin_bit_cast(
-            f32x4, load16<0>(rp, cnt > 2 ? (uint32_t)(((cut >> 40) & 0xfffff) * kPartialFloats + off) * 4u : kOff));
+            f32x4, load16<0>(rp, cnt > 2 ? (uint32_t)(split::packed_slot(cut, 2) * kPartialFloats + off) * 4u : kOff));
         return cnt > 2 ? v0 + v1 + v2 : cnt > 1 ? v0 + v1 : v0;
     }
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
     // More than three contributors: each one's slot follows from its range.
     const long ib = item * D.nsteps, ie = ib + D.nsteps;
-    for (int v = (int)(cut >> 16) & 0xffff, w1 = (int)cut & 0xffff; v <= w1; ++v) {
-        const long v0 = D.ranges[2 * v], v1 = D.ranges[2 * v + 1];
-        if (v0 >= v1) continue;
-        const int slot = (ib <= v0 && v0 < ie) ? 0 : 1;
-        s += *reinterpret_cast<const f32x4 *>(D.partials + ((size_t)v * 2 + slot) * kPartialFloats + off);
+    for (int v = split::first_worker(cut), w1 = split::last_worker(cut); v <= w1; ++v) {
+        const int slot = split::piece_slot(v, (long)D.ranges[2 * v], (long)D.ranges[2 * v + 1], ib, ie);
+        if (slot >= 0) s += *reinterpret_cast<const f32x4 *>(D.partials + (size_t)slot * kPartialFloats + off);
     }
     return s;
 }

@@ -131,3 +131,31 @@ def test_initial_buffer_discounts_costs():
     B0 = sel.traj(parent, pred, 0)
     S, costs = sel.select(parent, P, pred, 3, B0=B0)
     assert S[0] == 0 and costs[0] == 0
+
+
+@pytest.mark.parametrize("case", ["one_layer", "two_layers"])
+@pytest.mark.parametrize("mode", sel.MODES)
+def test_hand_worked_tree_every_mode(golden, case, mode):
+    # Picks and marginal costs worked out by hand (tests/golden/selector_modes.json): Eq. 9 with the buffer
+    # update of Algorithm 1, the confidence order, Eq. 10 without the buffer, and P - lambda * DeltaCost.
+    g = golden["selector_modes"][case]
+    S, costs = sel.select(g["parent"], g["P"], g["pred"], g["budget"], eps=g["eps"], mode=mode, lam=g["lambda"])
+    assert S == g["expect"][mode]["nodes"]
+    assert costs == g["expect"][mode]["costs"]
+
+
+def test_hand_worked_tree_scores(golden):
+    # The footprints and round-2 scores of the hand computation (four decimals as written there).
+    g = golden["selector_modes"]["one_layer"]
+    par, P, pred, eps, lam = g["parent"], g["P"], g["pred"], g["eps"], g["lambda"]
+    assert [len(sel.traj(par, pred, i)) for i in range(4)] == [4, 8, 6, 9]
+    for node, s in g["expect_global_scores"].items():
+        i = int(node)
+        assert round(P[i] / (len(sel.traj(par, pred, i)) + eps), 4) == s
+    B = sel.traj(par, pred, 0)
+    for node, s in g["expect_scores_round2"]["cost_ratio"].items():
+        i = int(node)
+        assert round(P[i] / (len(sel.traj(par, pred, i) - B) + eps), 4) == s
+    for node, s in g["expect_scores_round2"]["cost_diff"].items():
+        i = int(node)
+        assert round(P[i] - lam * len(sel.traj(par, pred, i) - B), 4) == s

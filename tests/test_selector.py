@@ -67,3 +67,14 @@ def test_rejects_bad_trees():
         moe.moe_select_tree([-1, 0, 0], [1, .5, .2], pred, 4, 2, eps=0.0)  # eps must be > 0 for Eq. 9
     with pytest.raises(moe.MoeError):
         moe.moe_select_tree([-1, 0, 0], [1, .5, .2], pred, 4, 2, mode=7)
+
+
+@pytest.mark.parametrize("case", ["one_layer", "two_layers"])
+@pytest.mark.parametrize("mode", list(MODES))
+def test_hand_worked_tree_every_mode(golden, case, mode):
+    g = golden["selector_modes"][case]
+    pred = np.array(g["pred"], np.int32)
+    s, c = moe.moe_select_tree(g["parent"], g["P"], pred, g["E"], g["budget"], eps=g["eps"], lam=g["lambda"],
+                               mode=MODES[mode])
+    assert list(s) == g["expect"][mode]["nodes"]
+    assert list(c) == g["expect"][mode]["costs"]
