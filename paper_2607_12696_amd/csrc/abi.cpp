@@ -44,6 +44,7 @@ moe_status_t check_weights(const moe_weights_t *w)
     // Every packed matrix is addressed through a 32-bit buffer range below 2^31 bytes.
     const size_t pair = (!w->w_up || (sh && !w->sh_up)) ? 2 : 1;
     if (ecospec::packed_matrix_bytes(w->fmt, w->d_ff, w->d) * pair >= (1UL << 31)) return MOE_ERR_UNSUPPORTED;
+    if (ecospec::packed_matrix_bytes(w->fmt, w->d, w->d_ff) >= (1UL << 31)) return MOE_ERR_UNSUPPORTED;
     const void *mats[] = {w->w_gate, w->w_up, w->w_down, w->sh_gate, w->sh_up, w->sh_down};
     for (const void *p : mats)
         if (p && !aligned(p, 16)) return MOE_ERR_INVALID_ARG;
@@ -182,8 +183,8 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     if (!aligned(x, 16) || !aligned(y, 16) || !aligned(workspace, 256)) return MOE_ERR_INVALID_ARG;
     if (r->T < 1 || r->k < 1 || r->k > kMaxK || r->k > w->E || r->E != w->E || (long)r->T * r->k > kMaxSlots)
         return MOE_ERR_INVALID_ARG;
-    if (!r->topk_w || !r->union_ids || !r->n_unique || !r->offsets || !r->perm) return MOE_ERR_INVALID_ARG;
-    if (w->b_down && !r->topk_idx) return MOE_ERR_INVALID_ARG;  // the down bias follows each slot's expert
+    if (!r->topk_idx || !r->topk_w || !r->union_ids || !r->n_unique || !r->offsets || !r->perm)
+        return MOE_ERR_INVALID_ARG;
     const bool shared = w->sh_gate != nullptr;
     const ecospec::VerifyWorkspace ws =
         ecospec::verify_workspace(w->d, w->d_ff, r->T, r->k, shared, w->act_fmt == MOE_ACTQ_MXFP8);

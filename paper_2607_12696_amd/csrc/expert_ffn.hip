@@ -1001,7 +1001,9 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
         const int U = *a.n_unique;
         for (int u = threadIdx.x; u <= U; u += kThreads) off_s[u] = a.offsets[u];
         __syncthreads();
-        if (p >= S) return;
+        // Positions past the placed slots (slots whose expert lies outside [0, E) are never placed)
+        // hold no slot of this call.
+        if (p >= off_s[U] || (unsigned)slot >= (unsigned)S) return;
         int lo = 0, hi = U - 1;  // the union member u with off_s[u] <= p < off_s[u + 1]
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
@@ -1195,22 +1197,27 @@ __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
         float wj[CH];
         long long cj[CH];
         f32x4 vj[CH], bj[CH];
+        bool ok[CH];
 #pragma unroll
         for (int q = 0; q < CH; ++q) {
             const int slot = t * a.k + min(j0 + q, a.k - 1);
-            pj[q] = a.inv[slot];
-            gj[q] = a.gidx[slot];
+            // A slot whose expert lies outside [0, E) was never placed: it adds nothing and its
+            // (unwritten) map entries are not read.
+            const int e = a.topk_idx[slot];
+            ok[q] = j0 + q < a.k && (unsigned)e < (unsigned)a.E;
+            pj[q] = ok[q] ? a.inv[slot] : 0;
+            gj[q] = ok[q] ? a.gidx[slot] : 0;
             wj[q] = a.topk_w[slot];
-            bj[q] = a.b_down ? *reinterpret_cast<const f32x4 *>(a.b_down + (size_t)a.topk_idx[slot] * a.d + c)
-                             : f32x4{0.f, 0.f, 0.f, 0.f};
+            bj[q] = a.b_down && ok[q] ? *reinterpret_cast<const f32x4 *>(a.b_down + (size_t)e * a.d + c)
+                                      : f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
-        for (int q = 0; q < CH; ++q) cj[q] = D.cut[(long)(gj[q] >> 6) * D.nbands + band];
+        for (int q = 0; q < CH; ++q) cj[q] = ok[q] ? D.cut[(long)(gj[q] >> 6) * D.nbands + band] : -1;
 #pragma unroll
         for (int q = 0; q < CH; ++q) vj[q] = expert_out(D, cj[q], (long)(gj[q] >> 6) * D.nbands + band, pj[q], gj[q] & 63, c);
 #pragma unroll
         for (int q = 0; q < CH; ++q)
-            if (j0 + q < a.k) s += wj[q] * (a.b_down ? vj[q] + bj[q] : vj[q]);
+            if (ok[q]) s += wj[q] * (a.b_down ? vj[q] + bj[q] : vj[q]);
     }
     if (a.sh_gate) {
         // The shared expert's token groups are the last ceil(T / 64).

@@ -304,14 +304,27 @@ def test_misaligned_bias_rejected(name):
     assert _ws(w, 8, 2)[0] == moe.MOE_ERR_INVALID_ARG
 
 
-def test_down_bias_needs_topk_idx():
+@pytest.mark.parametrize("down_bias", [False, True])
+def test_verify_needs_topk_idx(down_bias):
+    # The combine reads each slot's expert (to skip slots outside [0, E) and to pick the down bias).
     L = moe.lib()
     w, r = _weights(), _routing()
-    w.b_down = FAKE
+    if down_bias:
+        w.b_down = FAKE
     st, need = _ws(w, 8, 2)
     assert st == moe.MOE_OK
     r.topk_idx = None
     assert L.moe_verify_layer(FAKE, C.byref(w), C.byref(r), 2 * FAKE, 4 * FAKE, need, None) == moe.MOE_ERR_INVALID_ARG
+
+
+def test_down_matrix_over_2GiB_rejected():
+    # W_down [d][d_ff] is bounded like W_gate / W_up: with d_ff padded to 128 it can be the larger matrix.
+    w = _weights()
+    w.fmt, w.d, w.d_ff = 0, 32, 32
+    assert _ws(w, 8, 2)[0] == moe.MOE_OK
+    w.d, w.d_ff = 262144 + 32, 4064  # W_down 262176 x 4096 bf16 >= 2 GiB, W_gate 4064 x 262176 < 2 GiB (unpaired)
+    w.w_up = FAKE
+    assert _ws(w, 8, 2)[0] == moe.MOE_ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("fmt,E,N,K,status", [

@@ -157,8 +157,10 @@ def test_router_from_hidden_matches_oracle(T, d, E, k, score):
     tol = d * 2.0 ** -24 * oracle.router_logits(_abs_bits(x), _abs_bits(w)) + 1e-30
     assert np.all(np.abs(lg - ref) <= tol)
     idx = idx_g.cpu().numpy()
+    # The top-k ranks exactly the fp32 logits it writes out: bit for bit the oracle's top-k of those logits.
+    assert np.array_equal(oracle.route(lg_g.cpu().numpy(), k, score)[0], idx)
+    # Against the fp64 logits: the same selection wherever the order is decided by more than the tolerance.
     exact = check_topk_against_reference(idx, ref, tol, k)
-    assert exact.mean() >= 0.9
     # Gate weights against the oracle's (fp64 logits) where the selection is the oracle's; the logit error
     # moves a weight by at most 2 * max tol.
     idx_o, w_o = oracle.route(ref.astype(np.float32), k, score)
@@ -193,6 +195,33 @@ def _grouped_margins_ok(lg, b, k, G, TG, t):
     return np.diff(cs).min() < -2 * C_TOL if cs.size > 1 else True
 
 
+def check_grouped_selection(sel, lg_row, b, k, G, TG):
+    """A group-limited selection `sel` (in rank order) that the fp32 path may have made for one token:
+    scores c = sigmoid(l) + bias known to within C_TOL, group scores (sums of two) to within 2 * C_TOL.
+      - k distinct experts from at most TG groups;
+      - each selected expert's group could be among the TG best: fewer than TG groups certainly score higher;
+      - the selection is in rank order within tolerance;
+      - no eligible expert certainly beats a selected one, where eligible means in a group that is certainly
+        kept (fewer than TG other groups could score at least as high) or in one of the selection's groups."""
+    s = 1.0 / (1.0 + np.exp(-lg_row.astype(np.float64)))
+    c = s + (0.0 if b is None else b.astype(np.float64))
+    E = c.size
+    n = E // G
+    gs = np.sort(c.reshape(G, n), axis=1)[:, ::-1][:, :2].sum(1)
+    sel = [int(e) for e in sel]
+    assert len(set(sel)) == k and all(0 <= e < E for e in sel), sel
+    groups = {e // n for e in sel}
+    assert len(groups) <= TG, sel
+    for g in groups:
+        assert np.sum(gs > gs[g] + 4 * C_TOL) < TG, (g, sel)
+    for j in range(k - 1):
+        assert c[sel[j]] >= c[sel[j + 1]] - 2 * C_TOL, (j, sel)
+    certain = {g for g in range(G) if np.sum(gs >= gs[g] - 4 * C_TOL) - 1 < TG}
+    eligible = [e for e in range(E) if e // n in certain | groups and e not in sel]
+    if eligible:
+        assert c[eligible].max() <= c[sel].min() + 2 * C_TOL, sel
+
+
 @pytest.mark.parametrize("T,E,G,TG,k,bias", GROUPED_CASES)
 def test_grouped_route_matches_oracle(T, E, G, TG, k, bias):
     note(f"grouped route T={T} E={E} G={G} TG={TG} k={k} bias={bias}")
@@ -202,16 +231,20 @@ def test_grouped_route_matches_oracle(T, E, G, TG, k, bias):
     torch.cuda.synchronize()
     idx_o, w_o = oracle.route_grouped(lg.numpy(), None if b is None else b.numpy(), k, G, TG, 2.5)
     ig, wg = idx_g.cpu().numpy(), w_g.cpu().numpy().astype(np.float64)
+    bn = None if b is None else b.numpy()
     decided = 0
     for t in range(T):
         same = list(ig[t]) == list(idx_o[t])
-        if _grouped_margins_ok(lg.numpy(), None if b is None else b.numpy(), k, G, TG, t):
+        if _grouped_margins_ok(lg.numpy(), bn, k, G, TG, t):
             decided += 1
             assert same, (t, list(ig[t]), list(idx_o[t]))
+        else:  # a near-tie in the fp64 reference: any selection the fp32 path can justify
+            check_grouped_selection(ig[t], lg.numpy()[t], bn, k, G, TG)
         if same:
             assert np.abs(wg[t] - w_o[t]).max() <= 2.5 * WTOL, t
-        assert len(set(ig[t])) == k and len(set(int(e) // (E // G) for e in ig[t])) <= TG
-    assert decided >= 0.9 * T
+    # Not a tolerance: random logits leave only a few tokens within 1e-6 of a tie, so the bit-exact
+    # comparison above must have covered most of them (a test that compares nothing would pass vacuously).
+    assert decided >= 0.5 * T
 
 
 def test_grouped_route_exact_ties():
@@ -316,6 +349,10 @@ SMALL = {
     "fp8_wide": synth.Shape("fp8_wide", 384, 128, 8, 2, synth.FMT_FP8, 1, True),
     "mxfp4": synth.Shape("mxfp4", 320, 160, 16, 4, synth.FMT_MXFP4, 0, False),
     "one": synth.Shape("one", 64, 32, 1, 1, synth.FMT_BF16, 0, False),
+    # Few units per launch, so one item is spread over many workgroups (16 at T = 1 on 256 of them): the
+    # finishing of cut items walks the ranges instead of reading three packed slots.
+    "wide": synth.Shape("wide", 2048, 2048, 4, 1, synth.FMT_BF16, 0, False),
+    "wide_fp8": synth.Shape("wide_fp8", 1024, 1024, 4, 1, synth.FMT_FP8, 1, True),
 }
 
 _small_layers = {}
@@ -344,7 +381,19 @@ def test_verify_small_matches_oracle(name, T):
     assert err <= YTOL
 
 
-@pytest.mark.parametrize("name", ["toy", "fp8", "mxfp4", "bf16_tail"])
+def test_wide_shapes_spread_items_over_more_than_three_workgroups():
+    # The split of this device's grid (one workgroup per compute unit) puts more than three ranges on the
+    # items of the wide shapes at T = 1, so their parity runs above finish cut items by walking the ranges
+    # (gate/up fix-up and combine alike).
+    from test_split_bookkeeping import brute_owner, kernel_costs
+    W = min(torch.cuda.get_device_properties(0).multi_processor_count, 512)
+    for fmt, n_exp, nbands, nsteps in [("bf16", 1, 16, 16), ("bf16", 1, 8, 16),   # wide: gate/up, down
+                                       ("fp8", 2, 8, 8), ("fp8", 2, 4, 8)]:      # wide_fp8 (+ shared)
+        own = brute_owner(kernel_costs(fmt, [1] * n_exp), nbands * nsteps, W)
+        assert max(len(set(r)) for r in own.reshape(-1, nsteps).tolist()) > 3, (fmt, nbands, nsteps)
+
+
+@pytest.mark.parametrize("name", ["toy", "fp8", "mxfp4", "bf16_tail", "wide"])
 @pytest.mark.parametrize("T", [1, 64, 130])
 def test_verify_identical_routing_matches_oracle(name, T):
     # Degenerate draft: every token routes to the same k experts (U = k, each expert serves all T tokens,
@@ -689,18 +738,35 @@ def host_experts(dl, experts):
     return out
 
 
+def cover_rows(idx, base):
+    """`base` rows plus, greedily, rows whose experts are not yet compared, until every expert the call
+    routes to appears in some compared row (every expert's items are then checked against the oracle)."""
+    rows = sorted(set(base))
+    need = set(idx.reshape(-1).tolist()) - set(idx[rows].reshape(-1).tolist())
+    while need:
+        t = max(range(len(idx)), key=lambda r: (len(need & set(idx[r].tolist())), -r))
+        rows.append(t)
+        need -= set(idx[t].tolist())
+    return sorted(set(rows))
+
+
+# (shape, T, routing, U, rows): rows are compared with the oracle, plus as many more as it takes to cover every
+# routed expert ("all": every row).
 FULL_CASES = [
-    ("ds", 64, "exact", 32, [0, 17, 63]),
+    ("ds", 64, "exact", 32, "all"),          # the benchmark's workload: every row of the step
     ("ds", 8, "scattered", None, [0, 7]),
     ("ds", 64, "exact", 256, [5, 40]),
-    ("qwen", 32, "clustered", None, [0, 31]),
-    ("qwen", 64, "scattered", None, [3]),
-    ("gpt", 64, "clustered", None, [0, 50]),
-    ("gpt", 8, "scattered", None, [2, 7]),
+    ("ds", 1, "scattered", None, "all"),     # one token: k experts, each item spread over many workgroups
     # Batch scaling past 64 tokens: experts with more than 64 tokens are split into 64-token groups
     # (DS: the shared expert serves all 256 tokens in four groups; GPT-OSS: 32 experts x 64 tokens).
     ("ds", 256, "scattered", None, [0, 255]),
+    ("qwen", 32, "clustered", None, [0, 31]),
+    ("qwen", 64, "scattered", None, [3]),
+    ("qwen", 1, "scattered", None, "all"),   # gate/up items of four contributors
     ("qwen", 256, "clustered", None, [7, 200]),
+    ("gpt", 64, "clustered", None, [0, 50]),
+    ("gpt", 8, "scattered", None, [2, 7]),
+    ("gpt", 1, "scattered", None, "all"),    # gate/up items of four and down items of six contributors
     ("gpt", 512, "exact", 32, [1, 300, 511]),
 ]
 
@@ -773,7 +839,7 @@ def test_full_ds_grouped_routing_sampled_rows():
 
 
 @pytest.mark.parametrize("name,T,kind,U,rows", FULL_CASES)
-def test_full_shape_sampled_rows(name, T, kind, U, rows):
+def test_full_shape_matches_oracle(name, T, kind, U, rows):
     sh = synth.SHAPES[name]
     note(f"full shape={name} T={T} routing={kind} U={U} rows={rows}")
     raw, dl = full_layer(name)
@@ -787,11 +853,13 @@ def test_full_shape_sampled_rows(name, T, kind, U, rows):
     if U is not None:
         assert u["n_unique"] == U
     assert np.array_equal(r.perm.cpu().numpy(), u["perm"])
+    rows = list(range(T)) if rows == "all" else cover_rows(idx_o, rows)
     used = sorted(set(idx_o[rows].reshape(-1).tolist()))
+    assert used == sorted(u["union_ids"][:u["n_unique"]].tolist())  # every routed expert is compared
     hl = host_experts(raw, used)
     y_ref = oracle.verify_tokens(hl, x, idx_o, w_o, tokens=rows, threads=16)
     err = y_err(y.float().cpu().numpy()[rows], y_ref)
-    note(f"  U={u['n_unique']} rel err {err:.3e}")
+    note(f"  U={u['n_unique']} rows compared {len(rows)} rel err {err:.3e}")
     assert err <= YTOL
     # Every row: finite, and equal to a second run bit for bit.
     y2, _ = moe.moe_verify_step(x.to(DEV), lg.to(DEV), dl, sh.k, sh.score)
