@@ -168,7 +168,8 @@ moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, siz
     if (st != MOE_OK) return st;
     if (T < 1 || k < 1 || k > kMaxK || k > w->E || (long)T * k > kMaxSlots) return MOE_ERR_INVALID_ARG;
     const ecospec::VerifyWorkspace ws =
-        ecospec::verify_workspace(w->d, w->d_ff, T, k, w->sh_gate != nullptr, w->act_fmt == MOE_ACTQ_MXFP8);
+        ecospec::verify_workspace(w->d, w->d_ff, T, k, w->sh_gate != nullptr, w->act_fmt == MOE_ACTQ_MXFP8,
+                                  ecospec::verify_workers());
     if (ws.plan_cap > ecospec::kMaxGroups) return MOE_ERR_UNSUPPORTED;
     *bytes = ws.total;
     return MOE_OK;
@@ -187,7 +188,8 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
         return MOE_ERR_INVALID_ARG;
     const bool shared = w->sh_gate != nullptr;
     const ecospec::VerifyWorkspace ws =
-        ecospec::verify_workspace(w->d, w->d_ff, r->T, r->k, shared, w->act_fmt == MOE_ACTQ_MXFP8);
+        ecospec::verify_workspace(w->d, w->d_ff, r->T, r->k, shared, w->act_fmt == MOE_ACTQ_MXFP8,
+                                  ecospec::verify_workers());
     if (ws.plan_cap > ecospec::kMaxGroups) return MOE_ERR_UNSUPPORTED;
     if (workspace_bytes < ws.total) return MOE_ERR_WORKSPACE;
     const long rows = (long)r->T * r->k + (shared ? r->T : 0);

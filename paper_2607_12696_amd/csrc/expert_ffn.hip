@@ -93,7 +93,12 @@ constexpr int kThreads = kWG * kWave;
 constexpr int kBRowsPerPass = kThreads / 16;         // activation rows staged per pass (16 threads per row)
 constexpr int kBPass = kTokGroup / kBRowsPerPass;    // passes per step
 constexpr int kAuxNT = 2;               // nontemporal: streamed weights should not displace activations
-constexpr int kPartialFloats = kWG * 2 * kMB * 4 * kWave;  // one workgroup's accumulators
+// Floats of one partial-sum slot: a workgroup's accumulators of the live token
+// blocks (a token group holds at most min(T, 64) tokens).
+constexpr int partial_floats(int T)
+{
+    return kWG * 2 * 4 * kWave * (((T < kTokGroup ? T : kTokGroup) + 15) / 16);
+}
 
 // Wave-uniform loads through the constant address space (scalar memory).
 __device__ __forceinline__ int ld_s(const int32_t *p)
@@ -218,7 +223,8 @@ struct FfnParams {
     int band_rows;        // rows per item: 16 * kWG (gate/up) or 32 * kWG (down)
     int nbands;           // bands per expert: ceil(N / band_rows)
     int workers;          // workgroups of the main kernel's grid
-    float *partials;      // [workers][2][kPartialFloats]
+    float *partials;      // [workers][2][slot_floats]
+    int slot_floats;      // floats per partial-sum slot: partial_floats(T)
     long long *ranges;    // [workers][2]: unit range [x0, x1) of each workgroup, written by the expert kernel
     long long *fix;       // gate/up only: [workers][4] fix-up record of each workgroup (see write_fix_record)
     long long *cut;       // down only: [groups * nbands] how combine reads each item (see record_cuts)
@@ -773,7 +779,7 @@ __device__ __forceinline__ void write_fix_record(const FfnParams &P, const Plan 
 template <bool DOWN>
 __device__ __forceinline__ int partial_offset(int wave, int t, int mb, int lane)
 {
-    if (!DOWN) return (((wave * 2 + t) * kMB + mb) * kWave + lane) * 4;
+    if (!DOWN) return (((mb * kWG + wave) * 2 + t) * kWave + lane) * 4;
     const int col = lane & 15, grp = lane >> 4;
     return (mb * 16 + col) * (32 * kWG) + 32 * wave + 16 * t + 4 * grp;
 }
@@ -947,7 +953,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             if (cib >= x0 && cib + nsteps <= x1) {
                 finish_item<DOWN, MXA>(P, cd, wave, acc, cbias);
             } else {
-                float *dst = P.partials + ((size_t)w * 2 + (cib <= x0 ? 0 : 1)) * kPartialFloats;
+                float *dst = P.partials + ((size_t)w * 2 + (cib <= x0 ? 0 : 1)) * P.slot_floats;
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -1044,7 +1050,7 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
         // Up to three contributors: every load is issued before the first sum (one round trip;
         // absent contributors and dead token blocks read zeros), then added in workgroup order.
         const int cnt = split::packed_count(cut);
-        const rsrc_t rp = make_rsrc(P.partials, (uint32_t)((size_t)P.workers * 2 * kPartialFloats * 4));
+        const rsrc_t rp = make_rsrc(P.partials, (uint32_t)((size_t)P.workers * 2 * P.slot_floats * 4));
         f32x4 v[3][2][kMB];
 #pragma unroll
         for (int i = 0; i < 3; ++i) {
@@ -1055,7 +1061,7 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
                 for (int mb = 0; mb < kMB; ++mb)
                     v[i][t][mb] = __builtin_bit_cast(
                         f32x4, load16<0>(rp, (i < cnt && mb < nmb)
-                                                 ? (slot * kPartialFloats + (uint32_t)partial_offset<DOWN>(wave, t, mb, lane)) * 4u
+                                                 ? (slot * (uint32_t)P.slot_floats + (uint32_t)partial_offset<DOWN>(wave, t, mb, lane)) * 4u
                                                  : kOff));
         }
 #pragma unroll
@@ -1071,7 +1077,7 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
         for (int v = split::first_worker(cut), w1 = split::last_worker(cut); v <= w1; ++v) {
             const int slot = split::piece_slot(v, (long)ld_s64(P.ranges + 2 * v), (long)ld_s64(P.ranges + 2 * v + 1),
                                                ib, ie);
-            if (slot >= 0) add(P.partials + (size_t)slot * kPartialFloats);
+            if (slot >= 0) add(P.partials + (size_t)slot * P.slot_floats);
         }
     }
     finish_item<DOWN, MXA>(P, d, wave, acc, bias);
@@ -1158,14 +1164,14 @@ __device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, l
         // (absent ones read zeros) and added in workgroup order.
         const int cnt = cut < 0 ? 0 : split::packed_count(cut);
         const rsrc_t ro = make_rsrc(D.a.o, (uint32_t)((size_t)(D.a.T * D.a.k + (D.a.sh_gate ? D.a.T : 0)) * D.a.d * 4));
-        const rsrc_t rp = make_rsrc(D.partials, (uint32_t)((size_t)D.workers * 2 * kPartialFloats * 4));
+        const rsrc_t rp = make_rsrc(D.partials, (uint32_t)((size_t)D.workers * 2 * D.slot_floats * 4));
         const f32x4 v0 = __builtin_bit_cast(
             f32x4, cut < 0 ? load16<0>(ro, (uint32_t)((size_t)p * D.a.d + c) * 4u)
-                           : load16<0>(rp, (uint32_t)(split::packed_slot(cut, 0) * kPartialFloats + off) * 4u));
+                           : load16<0>(rp, (uint32_t)(split::packed_slot(cut, 0) * D.slot_floats + off) * 4u));
         const f32x4 v1 = __builtin_bit_cast(
-            f32x4, load16<0>(rp, cnt > 1 ? (uint32_t)(split::packed_slot(cut, 1) * kPartialFloats + off) * 4u : kOff));
+            f32x4, load16<0>(rp, cnt > 1 ? (uint32_t)(split::packed_slot(cut, 1) * D.slot_floats + off) * 4u : kOff));
         const f32x4 v2 = __builtin_bit_cast(
-            f32x4, load16<0>(rp, cnt > 2 ? (uint32_t)(split::packed_slot(cut, 2) * kPartialFloats + off) * 4u : kOff));
+            f32x4, load16<0>(rp, cnt > 2 ? (uint32_t)(split::packed_slot(cut, 2) * D.slot_floats + off) * 4u : kOff));
         return cnt > 2 ? v0 + v1 + v2 : cnt > 1 ? v0 + v1 : v0;
     }
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -1173,7 +1179,7 @@ __device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, l
     const long ib = item * D.nsteps, ie = ib + D.nsteps;
     for (int v = split::first_worker(cut), w1 = split::last_worker(cut); v <= w1; ++v) {
         const int slot = split::piece_slot(v, (long)D.ranges[2 * v], (long)D.ranges[2 * v + 1], ib, ie);
-        if (slot >= 0) s += *reinterpret_cast<const f32x4 *>(D.partials + (size_t)slot * kPartialFloats + off);
+        if (slot >= 0) s += *reinterpret_cast<const f32x4 *>(D.partials + (size_t)slot * D.slot_floats + off);
     }
     return s;
 }
@@ -1246,7 +1252,7 @@ static int device_cus()
     return cached_cus;
 }
 
-static int workers()
+int verify_workers()
 {
     const int w = device_cus() * ECOSPEC_WG_PER_CU;
     return w < kMaxWorkers ? w : kMaxWorkers;
@@ -1260,7 +1266,7 @@ static int plan_capacity(int T, int k, bool shared)
     return (int)(1025 + (rows + kTokGroup - 1) / kTokGroup);
 }
 
-VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared, bool mx)
+VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared, bool mx, int workers)
 {
     auto align = [](size_t v) { return (v + 255) & ~(size_t)255; };
     const size_t rows = (size_t)T * k + (shared ? (size_t)T : 0);
@@ -1271,7 +1277,9 @@ VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared, boo
     w.o_bytes = rows * d * 4;
     w.p_offset = w.o_offset + align(w.o_bytes);
     // partial sums, unit ranges, fix-up records
-    w.p_bytes = (size_t)kMaxWorkers * 2 * kPartialFloats * 4 + (size_t)kMaxWorkers * 2 * 8 + (size_t)kMaxWorkers * 4 * 8;
+    w.workers = workers;
+    w.slot_floats = partial_floats(T);
+    w.p_bytes = (size_t)workers * 2 * w.slot_floats * 4 + (size_t)workers * 2 * 8 + (size_t)workers * 4 * 8;
     w.plan_cap = plan_capacity(T, k, shared);
     w.plan_offset = w.p_offset + align(w.p_bytes);
     w.plan_bytes = (8 + 2 * (size_t)kMaxGroups + 1026) * 4;  // groups, then first group per expert
@@ -1297,7 +1305,7 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
                              hipEvent_t const *events)
 {
     constexpr int PD = FMT == FMT_BF16 ? ECOSPEC_PD_BF16 : FMT == FMT_FP8 ? ECOSPEC_PD_FP8 : ECOSPEC_PD_FP4;
-    const int G = workers();
+    const int G = ws.workers;
     const bool grouped = args.T > kTokGroup;  // some expert may need several token groups
     VerifyArgs a = args;
     a.h = reinterpret_cast<uint16_t *>(ws_base + ws.h_offset);
@@ -1337,8 +1345,9 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     g.nbands = (a.d_ff + g.band_rows - 1) / g.band_rows;
     g.workers = G;
     g.partials = partials;
-    g.ranges = reinterpret_cast<long long *>(partials + (size_t)kMaxWorkers * 2 * kPartialFloats);
-    g.fix = g.ranges + (size_t)kMaxWorkers * 2;
+    g.slot_floats = ws.slot_floats;
+    g.ranges = reinterpret_cast<long long *>(partials + (size_t)G * 2 * ws.slot_floats);
+    g.fix = g.ranges + (size_t)G * 2;
     g.cut = reinterpret_cast<long long *>(ws_base + ws.cut_offset);
     g.plan = grouped ? plan : nullptr;
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD, MXA>), dim3(G), dim3(kThreads), 0, stream, g);

@@ -69,10 +69,15 @@ struct VerifyWorkspace {
     size_t h_offset, h_bytes, o_offset, o_bytes, p_offset, p_bytes, plan_offset, plan_bytes, map_offset, map_bytes,
         cut_offset, cut_bytes, mx_offset, mx_bytes;
     int plan_cap;
+    int workers;      // workgroups of the expert kernels' grid (one per compute unit)
+    int slot_floats;  // floats per partial-sum slot (two slots per workgroup)
     size_t total;
 };
-// mx: room for the MX activation mode's quantised x and SwiGLU rows.
-VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared, bool mx);
+// Workgroups of the expert kernels' grid on the current device.
+int verify_workers();
+// mx: room for the MX activation mode's quantised x and SwiGLU rows; workers:
+// the grid the call will launch (the partial-sum slots are sized by it).
+VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared, bool mx, int workers);
 
 // events: kTimingMarks optional marks (before gate/up, before its fix-up, before
 // down, before combine, after combine).

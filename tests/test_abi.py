@@ -348,3 +348,13 @@ def test_binding_refuses_host_tensors():
     torch = pytest.importorskip("torch")
     with pytest.raises(ValueError):
         moe.moe_route_topk(torch.zeros(2, 16), 2, 0)
+
+
+def test_workspace_scales_with_tokens():
+    # Partial-sum slots hold only the live 16-token blocks and one pair per workgroup of the grid, so a
+    # one-token call needs far less than a 64-token one (DeepSeek-V3.1 shape: under 16 MiB at T = 1).
+    w = _weights(1, 7168, 2048, 256, shared=True)
+    st1, n1 = _ws(w, 1, 8)
+    st64, n64 = _ws(w, 64, 8)
+    assert st1 == st64 == moe.MOE_OK
+    assert n1 < 16 << 20 and n64 < 64 << 20 and n1 < n64 / 4
