@@ -315,6 +315,25 @@ moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_r
                               void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * moe_verify_layer without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, results and limits as
+ * moe_verify_layer; the workspace is a fixed array of the library of
+ * MOE_NOALLOC_SCRATCH_BYTES per GPU (each GPU the library runs on holds its
+ * own copy until the process ends).  A call whose moe_verify_workspace_size
+ * exceeds it returns MOE_ERR_WORKSPACE (moe_last_error says how much it
+ * needs), before anything is enqueued.  Nothing is allocated, freed or
+ * cleared.  All calls on one GPU share the array and it keeps the last call's
+ * contents: calls ordered on one stream are safe, calls that overlap on one
+ * GPU (other streams, unordered host threads) race.  DeepSeek-V3.1-shaped FP8
+ * layers fit up to about T = 96 tokens, Qwen3-shaped bf16 layers up to about
+ * T = 128.
+ */
+#define MOE_NOALLOC_SCRATCH_BYTES (64u << 20)
+moe_status_t moe_verify_layer_noalloc(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
+                                      void *stream);
+
+/*
  * moe_verify_layer with timing marks: identical work and arguments, and in
  * addition records the caller's events on `stream` around its kernels:
  *   events[0] before the gate/up expert kernel, events[1] after it (before

@@ -40,7 +40,7 @@ MOE_ACTQ_BF16, MOE_ACTQ_MXFP8 = 0, 1
 
 EXPORTED = ("moe_route_topk", "moe_route_union", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
             "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_pack_gate_up", "moe_pack_down",
-            "moe_select_tree", "moe_status_string", "moe_last_error")
+            "moe_select_tree", "moe_status_string", "moe_last_error", "moe_verify_layer_noalloc")
 
 
 class MoeError(RuntimeError):
@@ -84,6 +84,7 @@ def lib() -> C.CDLL:
             L.moe_expert_union.argtypes = [p, i, i, i, p, p, p, p, p, p]
             L.moe_verify_workspace_size.argtypes = [C.POINTER(moe_weights_t), i, i, C.POINTER(C.c_size_t)]
             L.moe_verify_layer.argtypes = [p, C.POINTER(moe_weights_t), C.POINTER(moe_routing_t), p, p, C.c_size_t, p]
+            L.moe_verify_layer_noalloc.argtypes = [p, C.POINTER(moe_weights_t), C.POINTER(moe_routing_t), p, p]
             L.moe_verify_layer_timed.argtypes = [p, C.POINTER(moe_weights_t), C.POINTER(moe_routing_t), p, p,
                                                  C.c_size_t, p, C.POINTER(C.c_void_p)]
             L.moe_packed_size.argtypes = [i, i, i, i, C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]
@@ -95,7 +96,7 @@ def lib() -> C.CDLL:
             L.moe_status_string.restype = C.c_char_p
             L.moe_last_error.restype = C.c_char_p
             for f in ("moe_route_topk", "moe_route_union", "moe_route_topk_grouped", "moe_router_workspace_size", "moe_route_topk_hidden", "moe_expert_union", "moe_verify_workspace_size", "moe_verify_layer",
-                      "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_pack_gate_up",
+                      "moe_verify_layer_noalloc", "moe_verify_layer_timed", "moe_packed_size", "moe_pack_weights", "moe_pack_gate_up",
                       "moe_pack_down", "moe_select_tree"):
                 getattr(L, f).restype = i
             _lib = L
@@ -395,6 +396,23 @@ def moe_verify_layer(x, weights: dict, routing: Routing, y=None, workspace=None)
     _check("moe_verify_layer", lib().moe_verify_layer(
         _dev_ptr(x, "x"), C.byref(ws), C.byref(rs), _dev_ptr(y, "y"), _dev_ptr(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _stream(x)))
+    return y
+
+
+def moe_verify_layer_noalloc(x, weights: dict, routing: Routing, y=None):
+    """moe_verify_layer on the library's fixed per-GPU scratch (no workspace argument, nothing allocated
+    by the library)."""
+    torch = _torch()
+    if x.dtype != torch.bfloat16:
+        raise ValueError("x must be bfloat16")
+    if y is None:
+        y = torch.empty_like(x)
+    ws = weights_struct(weights)
+    rs = routing.c_struct()
+    status = lib().moe_verify_layer_noalloc(_dev_ptr(x, "x"), C.byref(ws), C.byref(rs), _dev_ptr(y, "y"), _stream(x))
+    if status == MOE_ERR_WORKSPACE:
+        raise MoeError("moe_verify_layer_noalloc", status, lib().moe_last_error().decode())
+    _check("moe_verify_layer_noalloc", status)
     return y
 
 

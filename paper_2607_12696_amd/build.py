@@ -20,7 +20,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libecospec_moe.so")
 BUILD = os.path.join(ROOT, "_build")
 
-SOURCES = ["route_topk.hip", "expert_union.hip", "expert_ffn.hip", "pack.hip", "router.hip", "abi.cpp", "selector.cpp"]
+SOURCES = ["route_topk.hip", "expert_union.hip", "expert_ffn.hip", "pack.hip", "router.hip", "noalloc.hip", "abi.cpp", "selector.cpp"]
 ARCH = "gfx950"
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall", "-Wno-unused-function"]

@@ -67,6 +67,12 @@ moe_status_t check_weights(const moe_weights_t *w)
 
 }  // namespace
 
+namespace ecospec {
+
+void set_last_error(const char *msg) { snprintf(g_last_error, sizeof g_last_error, "%s", msg); }
+
+}  // namespace ecospec
+
 extern "C" {
 
 const char *moe_status_string(moe_status_t s)
@@ -175,8 +181,12 @@ moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, siz
     return MOE_OK;
 }
 
-static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
-                                void *workspace, size_t workspace_bytes, void *stream, void *const *events)
+}  // extern "C"
+
+namespace ecospec {
+
+moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y, void *workspace,
+                         size_t workspace_bytes, void *stream, void *const *events)
 {
     moe_status_t st = check_weights(w);
     if (st != MOE_OK) return st;
@@ -240,16 +250,20 @@ static moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe
     return from_hip(ecospec::launch_verify(a, workspace, ws, (hipStream_t)stream, events ? ev : nullptr));
 }
 
+}  // namespace ecospec
+
+extern "C" {
+
 moe_status_t moe_verify_layer(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
                               void *workspace, size_t workspace_bytes, void *stream)
 {
-    return verify_impl(x, w, r, y, workspace, workspace_bytes, stream, nullptr);
+    return ecospec::verify_impl(x, w, r, y, workspace, workspace_bytes, stream, nullptr);
 }
 
 moe_status_t moe_verify_layer_timed(const void *x, const moe_weights_t *w, const moe_routing_t *r, void *y,
                                     void *workspace, size_t workspace_bytes, void *stream, void *const *events)
 {
-    return verify_impl(x, w, r, y, workspace, workspace_bytes, stream, events);
+    return ecospec::verify_impl(x, w, r, y, workspace, workspace_bytes, stream, events);
 }
 
 static moe_status_t check_pack(int fmt, int E, int N, int K)
