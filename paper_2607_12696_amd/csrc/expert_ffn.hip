@@ -675,6 +675,11 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
 // MX activation mode: LDS geometry of one step's FP8 activation tile (64
 // tokens x 256 codes, rows padded by 16 bytes) followed by its scales (8 per
 // token: 4 blocks of each of the step's two 128-wide chunks).
+// Activation tiles in LDS for a prefetch depth: the ring slots and the tiles
+// then cycle together (two suffice for correctness: a wavefront at step i's
+// barrier has finished step i - 1's contraction).
+constexpr int kTiles(int PD) { return PD % 2 ? PD : 2; }
+
 constexpr int kRowQ = 256 + 16;
 constexpr int kScaleQ = kMB * 16 * kRowQ;
 
@@ -795,7 +800,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     constexpr int NV = Fmt<FMT>::kVecs, SB = Fmt<FMT>::kBlocks;
     constexpr int BROW = BTile<SB>::kRow, BBUF = BTile<SB>::kBuf;
     constexpr uint32_t BLK = 1024u * NV;  // bytes of one 16 x 128 block of a tile
-    __shared__ __attribute__((aligned(16))) uint8_t lds[2 * BBUF];
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kTiles(PD) * BBUF];
     const VerifyArgs &a = P.a;
     // Workgroups are dispatched round-robin over the 8 XCDs; taking the ranges
     // XCD-major gives each XCD one contiguous eighth of the units, so the
@@ -907,10 +912,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
         for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    auto body = [&](int slot, int par, long i) {
+    // One step: the loads of the unit PD - 1 places ahead, then unit i's
+    // activation tile into LDS and its contraction.  Only this part depends
+    // on the ring slot, so only it is replicated per unrolled step.
+    auto step = [&](int slot, int par, long i) {
         issue((slot + PD - 1) % PD, i + PD - 1);
         if (i >= n) return;  // the last round of the unrolled loop runs past the range
-        const long u = unit_of(i);
         const int nmb = (cd.M + 15) / 16;
         uint8_t *buf = lds + par * BBUF;
         // After the previous step's barrier no wavefront still reads this buffer.
@@ -945,9 +952,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             default: contract<FMT, 4>(wf[slot], buf, acc); break;
             }
         }
-        // End of a piece (an item boundary, the range's end or the end of the
-        // sequence): finish the item, or park its partial sums if it is cut at
-        // either end of the range, and move on to the next piece.
+    };
+
+    // End of a piece (an item boundary, the range's end or the end of the
+    // sequence): finish the item, or park its partial sums if it is cut at
+    // either end of the range, and move on to the next piece.  It runs a few
+    // times per range: every copy of it is cold in the instruction cache, so
+    // the loop keeps as few copies as it can (one per unrolled step).
+    auto end_of_piece = [&](long i) {
+        const long u = unit_of(i);
+        const int nmb = (cd.M + 15) / 16;
         const long un = i + 1 < n ? unit_of(i + 1) : -1;
         if (u + 1 == cib + nsteps || un != u + 1) {
             if (cib >= x0 && cib + nsteps <= x1) {
@@ -976,10 +990,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 
 #pragma unroll
     for (int j = 0; j < PD - 1; ++j) issue(j, j);
-    constexpr int UN = PD % 2 ? 2 * PD : PD;  // ring slots and LDS parity repeat together
+    // One activation tile per ring slot for odd PD (kTiles), so the loop
+    // unrolls PD steps, not 2 * PD: half the code, half the cold copies.
+    constexpr int UN = kTiles(PD);
     for (long i0 = 0; i0 < n; i0 += UN) {
 #pragma unroll
-        for (int j = 0; j < UN; ++j) body(j % PD, j & 1, i0 + j);
+        for (int j = 0; j < UN; ++j) {
+            step(j % PD, j, i0 + j);  // the last round may run past the range: loads of zeros only
+            if (i0 + j < n) end_of_piece(i0 + j);
+        }
     }
     if (DOWN) record_cuts(P, pl, sp, x0, x1);
 }
@@ -1209,11 +1228,13 @@ __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
             const int slot = t * a.k + min(j0 + q, a.k - 1);
             // A slot whose expert lies outside [0, E) was never placed: it adds nothing and its
             // (unwritten) map entries are not read.
+            // (All four loads are issued together; only the map entries' use waits on the expert.)
             const int e = a.topk_idx[slot];
-            ok[q] = j0 + q < a.k && (unsigned)e < (unsigned)a.E;
-            pj[q] = ok[q] ? a.inv[slot] : 0;
-            gj[q] = ok[q] ? a.gidx[slot] : 0;
+            const int pv = a.inv[slot], gv = a.gidx[slot];
             wj[q] = a.topk_w[slot];
+            ok[q] = j0 + q < a.k && (unsigned)e < (unsigned)a.E;
+            pj[q] = ok[q] ? pv : 0;
+            gj[q] = ok[q] ? gv : 0;
             bj[q] = a.b_down && ok[q] ? *reinterpret_cast<const f32x4 *>(a.b_down + (size_t)e * a.d + c)
                                       : f32x4{0.f, 0.f, 0.f, 0.f};
         }
