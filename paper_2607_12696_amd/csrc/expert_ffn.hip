@@ -596,28 +596,24 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
         src.q1 = arow_ok ? (uint32_t)(row1 / 16) * ((nblocks + 3) / 4) * 256u + lane * 4u : kOff;
     }
 
-    // Activation rows: in pass i this wavefront stages rows i*kBRowsPerPass +
-    // 4*wave + q, q = lane / 16.  Their source rows (token of a grouped
-    // position for gate/up, the grouped position itself for down) are read
-    // through the scalar unit.
+    // Activation rows: in pass i, lane l of this wavefront stages row
+    // i*kBRowsPerPass + 4*wave + l/16 of the item's tokens (16 lanes per row).
+    // Its source row (the token of a grouped position for gate/up, the grouped
+    // position itself for down) is read by each lane for itself: no wave-wide
+    // round trips.
     // MX activations: rows of nblocks * 128 e4m3fn codes and nblocks * 4 scales.
     const uint32_t brow_bytes = MXA ? (uint32_t)nblocks * kMacroK : (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
     const int q = lane >> 4;
 #pragma unroll
     for (int i = 0; i < kBPass; ++i) {
+        const int r = i * kBRowsPerPass + 4 * wave + q;
         int row = -1;
-#pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-            const int r = i * kBRowsPerPass + 4 * wave + qq;
-            int v = -1;
-            if (r < d.M) {
-                const int p = d.p0 + r;
-                v = DOWN ? p
-                    : d.shared ? p - a.T * a.k
-                    : a.T * a.k <= kMaxTokLds ? __builtin_amdgcn_readfirstlane(sp.tok[p])
-                                              : (int)((uint32_t)ld_s(a.perm + p) / (uint32_t)a.k);
-            }
-            row = q == qq ? v : row;
+        if (r < d.M) {
+            const int p = d.p0 + r;
+            row = DOWN ? p
+                : d.shared ? p - a.T * a.k
+                : a.T * a.k <= kMaxTokLds ? sp.tok[p]
+                                          : (int)((uint32_t)a.perm[p] / (uint32_t)a.k);
         }
         src.boff[i] = row >= 0 ? (uint32_t)row * brow_bytes + (uint32_t)bc * 16u : kOff;
         src.soff[i] = row >= 0 ? (uint32_t)row * (uint32_t)nblocks * 4u + (uint32_t)(bc & 1) * 4u : kOff;
