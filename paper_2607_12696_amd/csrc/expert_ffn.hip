@@ -986,13 +986,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 
 #pragma unroll
     for (int j = 0; j < PD - 1; ++j) issue(j, j);
-    // One activation tile per ring slot for odd PD (kTiles), so the loop
-    // unrolls PD steps, not 2 * PD: half the code, half the cold copies.
-    constexpr int UN = kTiles(PD);
-    for (long i0 = 0; i0 < n; i0 += UN) {
+    // The loop unrolls PD steps (ring slot j); with kTiles(PD) activation
+    // tiles (PD of them for odd PD, else 2) the tile cycles with the slot, so
+    // PD steps suffice, not 2 * PD: half the code, half the cold copies.
+    for (long i0 = 0; i0 < n; i0 += PD) {
 #pragma unroll
-        for (int j = 0; j < UN; ++j) {
-            step(j % PD, j, i0 + j);  // the last round may run past the range: loads of zeros only
+        for (int j = 0; j < PD; ++j) {
+            step(j, j % kTiles(PD), i0 + j);  // the last round may run past the range: loads of zeros only
             if (i0 + j < n) end_of_piece(i0 + j);
         }
     }
