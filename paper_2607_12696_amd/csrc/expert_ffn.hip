@@ -223,6 +223,8 @@ struct FfnParams {
     int band_rows;        // rows per item: 16 * kWG (gate/up) or 32 * kWG (down)
     int nbands;           // bands per expert: ceil(N / band_rows)
     int workers;          // workgroups of the main kernel's grid
+    size_t mat_bytes;     // bytes of one packed matrix (W_gate, W_up or W_down) of an expert
+    size_t sc_bytes;      // bytes of its scales (0 for bf16)
     float *partials;      // [workers][2][slot_floats]
     int slot_floats;      // floats per partial-sum slot: partial_floats(T)
     long long *ranges;    // [workers][2]: unit range [x0, x1) of each workgroup, written by the expert kernel
@@ -297,25 +299,57 @@ struct Split {
     int wave_tot[kWG];
 };
 
-// Fills sp.cw and the groups' metadata for the launch (whole workgroup).
+// Fills sp.cw and the groups' metadata for the launch (whole workgroup) and
+// returns the plan.  Without a token-group plan (one group per union member,
+// then the shared expert) the union's offsets and ids are read for every
+// possible member in the same round trip as the union size and the slots'
+// tokens: the schedule waits for global memory once, not twice.
 template <int FMT, bool MXA>
-__device__ __forceinline__ void build_costs(const FfnParams &P, const Plan &pl, Split &sp)
+__device__ __forceinline__ Plan build_costs(const FfnParams &P, Split &sp)
 {
+    constexpr int kPre = 2;  // groups per thread read ahead (E <= kPre * kThreads covers every union)
     const VerifyArgs &a = P.a;
     const int S = a.T * a.k;
+    const int tid = threadIdx.x;
+    int o0[kPre], o1[kPre], id[kPre];
+#pragma unroll
+    for (int j = 0; j < kPre; ++j) {
+        const int g = j * kThreads + tid;
+        const bool ok = P.plan == nullptr && g < a.E;
+        o0[j] = ok ? a.offsets[g] : 0;
+        o1[j] = ok ? a.offsets[g + 1] : 0;
+        id[j] = ok ? a.union_ids[g] : 0;
+    }
+    const Plan pl = load_plan(P);
     if (S <= kMaxTokLds)
-        for (int p = threadIdx.x; p < S; p += kThreads) sp.tok[p] = a.perm[p] / a.k;
+        for (int p = tid; p < S; p += kThreads) sp.tok[p] = a.perm[p] / a.k;
     int run = 0;
-    for (int base = 0; base < pl.n_groups; base += kThreads) {
-        const int g = base + (int)threadIdx.x;
+    for (int base = 0, j = 0; base < pl.n_groups; base += kThreads, ++j) {
+        const int g = base + tid;
         int c = 0;
         if (g < pl.n_groups) {
             const int u = P.plan ? P.plan[8 + 2 * g] : g, tg = P.plan ? P.plan[8 + 2 * g + 1] : 0;
             const bool shared = u >= pl.U;
-            const int Mu = shared ? a.T : a.offsets[u + 1] - a.offsets[u];
+            int lo = 0, hi = 0, e = -1;
+            if (!shared) {
+                if (P.plan == nullptr && j < kPre) {
+#pragma unroll
+                    for (int q = 0; q < kPre; ++q)
+                        if (q == j) {
+                            lo = o0[q];
+                            hi = o1[q];
+                            e = id[q];
+                        }
+                } else {
+                    lo = a.offsets[u];
+                    hi = a.offsets[u + 1];
+                    e = a.union_ids[u];
+                }
+            }
+            const int Mu = shared ? a.T : hi - lo;
             sp.gM[g] = min(kTokGroup, Mu - tg * kTokGroup);
-            sp.gp0[g] = (shared ? S : a.offsets[u]) + tg * kTokGroup;
-            sp.ge[g] = shared ? -1 : a.union_ids[u];
+            sp.gp0[g] = (shared ? S : lo) + tg * kTokGroup;
+            sp.ge[g] = e;
             c = group_cost<FMT, MXA>(sp.gM[g]);
         }
         int tot = 0;
@@ -325,6 +359,7 @@ __device__ __forceinline__ void build_costs(const FfnParams &P, const Plan &pl, 
     }
     if (threadIdx.x == 0) sp.cw[pl.n_groups] = run;
     __syncthreads();
+    return pl;
 }
 
 // First unit x with P_x * W >= target (0 <= target <= C * W), by binary
@@ -340,13 +375,6 @@ __device__ __forceinline__ void build_bounds(Split &sp, int n_groups, long K, in
     const long long C = (long long)sp.cw[n_groups] * K;
     for (int v = threadIdx.x; v <= W; v += kThreads) sp.bound[v] = first_unit(sp, n_groups, K, W, C * v);
     __syncthreads();
-}
-
-// Unit range [x0, x1) of workgroup w (after build_bounds).
-__device__ __forceinline__ void worker_range(const Split &sp, int w, long &x0, long &x1)
-{
-    x0 = (long)sp.bound[w];
-    x1 = (long)sp.bound[w + 1];
 }
 
 // Workgroup whose range holds unit x.
@@ -374,11 +402,7 @@ __device__ __forceinline__ ItemDesc describe_lds(const FfnParams &P, const Split
 {
     const VerifyArgs &a = P.a;
     const int gi = item / P.nbands, band = item - gi * P.nbands;
-    const int fmt = a.fmt;
-    const size_t kp = (size_t)P.nblocks * kMacroK;
-    const size_t mat = (size_t)P.N * kp * (fmt == FMT_BF16 ? 2 : 1) / (fmt == FMT_MXFP4 ? 2 : 1);
-    const size_t sc = fmt == FMT_FP8 ? (size_t)(P.N / 128) * (P.K / 128) * 4
-                      : fmt == FMT_MXFP4 ? (size_t)P.N * ((P.nblocks + 3) / 4) * 16 : 0;
+    const size_t mat = P.mat_bytes, sc = P.sc_bytes;
     ItemDesc d;
     const int e0 = __builtin_amdgcn_readfirstlane(sp.ge[gi]);
     d.shared = e0 < 0;
@@ -541,7 +565,7 @@ struct Source {
     uint32_t q0, q1;            // scale offsets at step 0
     uint32_t boff[kBPass];      // lane offsets of this thread's activation rows at step 0 (kOff: no token)
     uint32_t soff[kBPass];      // MX activations: offsets of the rows' block scales at step 0
-    long ib, ie;                // the item's units [ib, ie)
+    int ib, ie;                 // the item's units [ib, ie)
     int item;
 };
 
@@ -556,12 +580,11 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
     const int K = P.K, nsteps = P.nsteps;
     const ItemDesc d = describe_lds<DOWN>(P, sp, item);
     src.item = item;
-    src.ib = (long)item * nsteps;
+    src.ib = item * nsteps;
     src.ie = src.ib + nsteps;
 
     const int nblocks = P.nblocks;
-    const uint32_t mat_bytes =
-        (uint32_t)((size_t)P.N * nblocks * kMacroK * (FMT == FMT_BF16 ? 2 : 1) / (FMT == FMT_MXFP4 ? 2 : 1));
+    const uint32_t mat_bytes = (uint32_t)P.mat_bytes;  // < 2^31 (checked at the boundary)
     const int row0 = tile_row<DOWN>(d, wave, 0), row1 = tile_row<DOWN>(d, wave, 1);
     const bool arow_ok = row0 < P.N;
     if (DOWN && d.pair) {
@@ -583,8 +606,7 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
         src.a0 = arow_ok ? (uint32_t)(row0 / 16) * nblocks * BLK + lane * 16u : kOff;
         src.a1 = arow_ok ? (uint32_t)(row1 / 16) * nblocks * BLK + lane * 16u : kOff;
     }
-    const uint32_t sc_bytes = FMT == FMT_FP8 ? (uint32_t)((P.N / 128) * (K / 128) * 4)
-                                             : (uint32_t)((size_t)P.N * ((nblocks + 3) / 4) * 16);
+    const uint32_t sc_bytes = (uint32_t)P.sc_bytes;
     src.rs0 = make_rsrc(FMT == FMT_BF16 ? d.wa : d.sa, FMT == FMT_BF16 ? 0u : sc_bytes);
     src.rs1 = make_rsrc(FMT == FMT_BF16 ? d.wb : d.sb, FMT == FMT_BF16 ? 0u : sc_bytes);
     src.q0 = src.q1 = 0;
@@ -806,19 +828,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
     const int tid = threadIdx.x, br = tid >> 4, bc = tid & 15;
-    const Plan pl = load_plan(P);
     const int nsteps = P.nsteps, K = P.K;
     __shared__ Split sp;
-    build_costs<FMT, MXA>(P, pl, sp);
+    const Plan pl = build_costs<FMT, MXA>(P, sp);
     build_bounds(sp, pl.n_groups, (long)P.nbands * nsteps, P.workers);
-    long x0, x1;
-    worker_range(sp, w, x0, x1);
-    if (threadIdx.x == 0) {  // for the fix-up (gate/up) and combine (down) kernels
-        P.ranges[2 * w] = x0;
-        P.ranges[2 * w + 1] = x1;
-        if (!DOWN) write_fix_record(P, pl, sp, w, x0, x1);
+    // Unit indices fit in 32 bits (fewer than 2^30 units: every matrix is below 2^31 bytes and a
+    // launch has at most 4096 token groups), so the unit arithmetic below is 32-bit.
+    const int x0 = (int)sp.bound[w], x1 = (int)sp.bound[w + 1];
+    // For the fix-up (gate/up) and combine (down) kernels, written when the
+    // range is done: the range, and the cut gate/up item it finishes.
+    auto write_records = [&]() {
+        if (threadIdx.x == 0) {
+            P.ranges[2 * w] = x0;
+            P.ranges[2 * w + 1] = x1;
+            if (!DOWN) write_fix_record(P, pl, sp, w, x0, x1);
+        }
+    };
+    if (x0 >= x1) {  // no units, no item
+        write_records();
+        return;
     }
-    if (x0 >= x1) return;
     const uint32_t rows = (uint32_t)(DOWN ? a.T * a.k + (a.sh_gate ? a.T : 0) : a.T);
     // Activation rows: bf16 x or H, or (MX) e4m3fn codes of K padded to nblocks * 128 and their block scales.
     const uint32_t brow_bytes = MXA ? (uint32_t)P.nblocks * kMacroK : (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
@@ -832,12 +861,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // ranges at scattered K offsets (measured: gate/up -2% at 32 experts,
     // -1.2% at 128).  Each piece is still summed in K order, so the results do
     // not change.
-    const long n = x1 - x0;
-    const long rot = (x0 + nsteps - 1) / nsteps * nsteps < x1 ? (x0 + nsteps - 1) / nsteps * nsteps - x0 : 0;
-    auto unit_of = [&](long i) { return i < n - rot ? x0 + rot + i : x0 + i - (n - rot); };
+    const uint32_t uns = (uint32_t)nsteps;
+    auto item_of = [&](int u) { return (int)((uint32_t)u / uns); };
+    const int n = x1 - x0;
+    const int b0 = (int)(((uint32_t)x0 + uns - 1u) / uns * uns);  // first item boundary at or after x0
+    const int rot = b0 < x1 ? b0 - x0 : 0;
+    auto unit_of = [&](int i) { return i < n - rot ? x0 + rot + i : x0 + i - (n - rot); };
 
     Source src;
-    set_source<FMT, DOWN, MXA>(src, P, sp, (int)(unit_of(0) / nsteps));
+    set_source<FMT, DOWN, MXA>(src, P, sp, item_of(unit_of(0)));
 
     WFrag<FMT> wf[PD][2];
     u32x4 bst[PD][kBPass][SB];
@@ -845,10 +877,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // Loads of the i-th unit of the sequence into ring slot `slot`; past the
     // range the loads read zeros (offsets beyond every buffer), so every path
     // issues the same loads and the compiler's wait counts stay exact.
-    auto issue = [&](int slot, long i) {
+    auto issue = [&](int slot, int i) {
         const bool ok = i < n;
-        const long v = ok ? unit_of(i) : src.ib;
-        if (ok && (v < src.ib || v >= src.ie)) set_source<FMT, DOWN, MXA>(src, P, sp, (int)(v / nsteps));
+        const int v = ok ? unit_of(i) : src.ib;
+        if (ok && (v < src.ib || v >= src.ie)) set_source<FMT, DOWN, MXA>(src, P, sp, item_of(v));
         const uint32_t step = (uint32_t)(v - src.ib);
 #pragma unroll
         for (int b = 0; b < SB; ++b) {
@@ -898,10 +930,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     };
 
     // The item being contracted.
-    int citem = (int)(unit_of(0) / nsteps);
+    int citem = item_of(unit_of(0));
     ItemDesc cd = describe_lds<DOWN>(P, sp, citem);
     ItemBias cbias = load_bias<DOWN>(P, cd, wave);
-    long cib = (long)citem * nsteps;
+    int cib = citem * nsteps;
     f32x4 acc[2][kMB];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -911,7 +943,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // One step: the loads of the unit PD - 1 places ahead, then unit i's
     // activation tile into LDS and its contraction.  Only this part depends
     // on the ring slot, so only it is replicated per unrolled step.
-    auto step = [&](int slot, int par, long i) {
+    auto step = [&](int slot, int par, int i) {
         issue((slot + PD - 1) % PD, i + PD - 1);
         if (i >= n) return;  // the last round of the unrolled loop runs past the range
         const int nmb = (cd.M + 15) / 16;
@@ -955,10 +987,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // either end of the range, and move on to the next piece.  It runs a few
     // times per range: every copy of it is cold in the instruction cache, so
     // the loop keeps as few copies as it can (one per unrolled step).
-    auto end_of_piece = [&](long i) {
-        const long u = unit_of(i);
+    auto end_of_piece = [&](int i) {
+        const int u = unit_of(i);
         const int nmb = (cd.M + 15) / 16;
-        const long un = i + 1 < n ? unit_of(i + 1) : -1;
+        const int un = i + 1 < n ? unit_of(i + 1) : -1;
         if (u + 1 == cib + nsteps || un != u + 1) {
             if (cib >= x0 && cib + nsteps <= x1) {
                 finish_item<DOWN, MXA>(P, cd, wave, acc, cbias);
@@ -976,8 +1008,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
                 for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
             if (un >= 0) {
-                citem = (int)(un / nsteps);
-                cib = (long)citem * nsteps;
+                citem = item_of(un);
+                cib = citem * nsteps;
                 cd = describe_lds<DOWN>(P, sp, citem);
                 cbias = load_bias<DOWN>(P, cd, wave);
             }
@@ -989,13 +1021,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // The loop unrolls PD steps (ring slot j); with kTiles(PD) activation
     // tiles (PD of them for odd PD, else 2) the tile cycles with the slot, so
     // PD steps suffice, not 2 * PD: half the code, half the cold copies.
-    for (long i0 = 0; i0 < n; i0 += PD) {
+    for (int i0 = 0; i0 < n; i0 += PD) {
 #pragma unroll
         for (int j = 0; j < PD; ++j) {
             step(j, j % kTiles(PD), i0 + j);  // the last round may run past the range: loads of zeros only
             if (i0 + j < n) end_of_piece(i0 + j);
         }
     }
+    write_records();
     if (DOWN) record_cuts(P, pl, sp, x0, x1);
 }
 
@@ -1170,31 +1203,57 @@ __global__ __launch_bounds__(256) void plan_kernel(VerifyArgs a, int32_t *plan)
 // Where expert output O[p][c .. c+3] (row r of a token group, item `item` of
 // the down launch) comes from: the down kernel's O row if the item was whole,
 // else the partial sums of its contributors added in workgroup order (what a
-// fix-up would have stored).  `cut` is the item's record_cuts entry.
-__device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, long item, int p, int r, int c)
+// fix-up would have stored).  `cut` is the item's record_cuts entry.  Items cut
+// over more than three ranges take expert_out_walk; here they read nothing and
+// give zeros.
+__device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, int p, int r, int c)
 {
+    if (cut >= 0 && !split::packed_contributors(cut)) return f32x4{0.f, 0.f, 0.f, 0.f};
+    // A whole item's O row, or up to three parked partial sums: all loads issued at once
+    // (absent ones read zeros) and added in workgroup order.
     const int off = r * D.band_rows + c % D.band_rows;  // partial_offset<true>
-    if (cut < 0 || split::packed_contributors(cut)) {
-        // A whole item's O row, or up to three parked partial sums: all loads issued at once
-        // (absent ones read zeros) and added in workgroup order.
-        const int cnt = cut < 0 ? 0 : split::packed_count(cut);
-        const rsrc_t ro = make_rsrc(D.a.o, (uint32_t)((size_t)(D.a.T * D.a.k + (D.a.sh_gate ? D.a.T : 0)) * D.a.d * 4));
-        const rsrc_t rp = make_rsrc(D.partials, (uint32_t)((size_t)D.workers * 2 * D.slot_floats * 4));
-        const f32x4 v0 = __builtin_bit_cast(
-            f32x4, cut < 0 ? load16<0>(ro, (uint32_t)((size_t)p * D.a.d + c) * 4u)
-                           : load16<0>(rp, (uint32_t)(split::packed_slot(cut, 0) * D.slot_floats + off) * 4u));
-        const f32x4 v1 = __builtin_bit_cast(
-            f32x4, load16<0>(rp, cnt > 1 ? (uint32_t)(split::packed_slot(cut, 1) * D.slot_floats + off) * 4u : kOff));
-        const f32x4 v2 = __builtin_bit_cast(
-            f32x4, load16<0>(rp, cnt > 2 ? (uint32_t)(split::packed_slot(cut, 2) * D.slot_floats + off) * 4u : kOff));
-        return cnt > 2 ? v0 + v1 + v2 : cnt > 1 ? v0 + v1 : v0;
-    }
+    const int cnt = cut < 0 ? 0 : split::packed_count(cut);
+    const rsrc_t ro = make_rsrc(D.a.o, (uint32_t)((size_t)(D.a.T * D.a.k + (D.a.sh_gate ? D.a.T : 0)) * D.a.d * 4));
+    const rsrc_t rp = make_rsrc(D.partials, (uint32_t)((size_t)D.workers * 2 * D.slot_floats * 4));
+    const f32x4 v0 = __builtin_bit_cast(
+        f32x4, cut < 0 ? load16<0>(ro, (uint32_t)((size_t)p * D.a.d + c) * 4u)
+                       : load16<0>(rp, (uint32_t)(split::packed_slot(cut, 0) * D.slot_floats + off) * 4u));
+    const f32x4 v1 = __builtin_bit_cast(
+        f32x4, load16<0>(rp, cnt > 1 ? (uint32_t)(split::packed_slot(cut, 1) * D.slot_floats + off) * 4u : kOff));
+    const f32x4 v2 = __builtin_bit_cast(
+        f32x4, load16<0>(rp, cnt > 2 ? (uint32_t)(split::packed_slot(cut, 2) * D.slot_floats + off) * 4u : kOff));
+    return cnt > 2 ? v0 + v1 + v2 : cnt > 1 ? v0 + v1 : v0;
+}
+
+// The same for an item cut over more than three ranges: each contributor's slot
+// follows from its range.  Four contributors at a time: their ranges in one
+// round trip, then their sums in one.
+__device__ __forceinline__ f32x4 expert_out_walk(const FfnParams &D, long long cut, long item, int r, int c)
+{
+    constexpr int CW = 4;
+    const int off = r * D.band_rows + c % D.band_rows;
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-    // More than three contributors: each one's slot follows from its range.
     const long ib = item * D.nsteps, ie = ib + D.nsteps;
-    for (int v = split::first_worker(cut), w1 = split::last_worker(cut); v <= w1; ++v) {
-        const int slot = split::piece_slot(v, (long)D.ranges[2 * v], (long)D.ranges[2 * v + 1], ib, ie);
-        if (slot >= 0) s += *reinterpret_cast<const f32x4 *>(D.partials + (size_t)slot * D.slot_floats + off);
+    const int w1 = split::last_worker(cut);
+    for (int v0 = split::first_worker(cut); v0 <= w1; v0 += CW) {
+        long long rg[CW][2];
+#pragma unroll
+        for (int q = 0; q < CW; ++q) {
+            const int v = min(v0 + q, w1);
+            rg[q][0] = D.ranges[2 * v];
+            rg[q][1] = D.ranges[2 * v + 1];
+        }
+        int slot[CW];
+        f32x4 pv[CW];
+#pragma unroll
+        for (int q = 0; q < CW; ++q) {
+            slot[q] = v0 + q <= w1 ? split::piece_slot(v0 + q, (long)rg[q][0], (long)rg[q][1], ib, ie) : -1;
+            pv[q] = slot[q] >= 0 ? *reinterpret_cast<const f32x4 *>(D.partials + (size_t)slot[q] * D.slot_floats + off)
+                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int q = 0; q < CW; ++q)
+            if (slot[q] >= 0) s += pv[q];
     }
     return s;
 }
@@ -1202,7 +1261,11 @@ __device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, l
 // y[t] = sum_j w[t][j] * (O[slot t*k + j] + b_down[expert of the slot]) (+ shared) -> bf16, summed in the
 // order j = 0..k-1, then the shared expert; 4 columns per thread.  D is the
 // down launch's geometry.  The k slots are handled 8 at a time, each stage's
-// loads issued together.
+// loads issued together; the shared expert's chain (its item, cut entry and
+// output) goes with the first stage's, so the kernel waits on global memory
+// three times whatever the slots.  Items cut over more than three ranges
+// (small batches spread thin over the workgroups) are walked afterwards, one
+// at a time, so that the common path stays short.
 __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
 {
     constexpr int CH = 8;
@@ -1212,8 +1275,13 @@ __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
     if (i >= a.T * per_row) return;
     const int t = i / per_row, c = (i - t * per_row) * 4;
     const int band = c / D.band_rows;
-    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+    // The shared expert's token groups are the last ceil(T / 64).
+    const bool sh = a.sh_gate != nullptr;
+    const int n_groups = sh ? (D.plan ? D.plan[0] : *a.n_unique + 1) : 0;
+    const long sitem = (long)(n_groups - (a.T + kTokGroup - 1) / kTokGroup + t / kTokGroup) * D.nbands + band;
+    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f}, vsh = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int j0 = 0; j0 < a.k; j0 += CH) {
+        const bool with_sh = sh && j0 == 0;
         int pj[CH], gj[CH];
         float wj[CH];
         long long cj[CH];
@@ -1236,19 +1304,47 @@ __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
         }
 #pragma unroll
         for (int q = 0; q < CH; ++q) cj[q] = ok[q] ? D.cut[(long)(gj[q] >> 6) * D.nbands + band] : -1;
+        const long long csh = with_sh ? D.cut[sitem] : -1;
+        // vj[q] = O + b_down of slot q.  A slot whose item needs the walk holds b_down for now
+        // (its walk sum w is added as w + b below, the same operation as O + b).
+        uint32_t walk = 0;  // bit q: slot q's item needs the walk; bit CH: the shared expert's
+        int wcode[CH];      // first and last contributor of such an item (w0 << 16 | w1)
 #pragma unroll
-        for (int q = 0; q < CH; ++q) vj[q] = expert_out(D, cj[q], (long)(gj[q] >> 6) * D.nbands + band, pj[q], gj[q] & 63, c);
+        for (int q = 0; q < CH; ++q) {
+            const bool wk = cj[q] >= 0 && !split::packed_contributors(cj[q]);
+            const f32x4 v = expert_out(D, cj[q], pj[q], gj[q] & 63, c);
+            vj[q] = a.b_down ? (wk ? bj[q] : v + bj[q]) : v;
+            wcode[q] = (int)cj[q];
+            if (wk) walk |= 1u << q;
+        }
+        if (with_sh) {
+            vsh = expert_out(D, csh, a.T * a.k + t, t % kTokGroup, c);
+            if (csh >= 0 && !split::packed_contributors(csh)) walk |= 1u << CH;
+        }
+        while (walk) {
+            const int q = __builtin_ctz(walk);
+            walk &= walk - 1;
+            long long cq = csh;
+            long iq = sitem;
+            int rq = t % kTokGroup;
+#pragma unroll
+            for (int qq = 0; qq < CH; ++qq)
+                if (qq == q) {
+                    cq = wcode[qq];
+                    iq = (long)(gj[qq] >> 6) * D.nbands + band;
+                    rq = gj[qq] & 63;
+                }
+            const f32x4 v = expert_out_walk(D, cq, iq, rq, c);
+#pragma unroll
+            for (int qq = 0; qq < CH; ++qq)
+                if (qq == q) vj[qq] = a.b_down ? v + vj[qq] : v;
+            if (q == CH) vsh = v;
+        }
 #pragma unroll
         for (int q = 0; q < CH; ++q)
-            if (ok[q]) s += wj[q] * (a.b_down ? vj[q] + bj[q] : vj[q]);
+            if (ok[q]) s += wj[q] * vj[q];
     }
-    if (a.sh_gate) {
-        // The shared expert's token groups are the last ceil(T / 64).
-        const int n_groups = D.plan ? D.plan[0] : *a.n_unique + 1;
-        const int g = n_groups - (a.T + kTokGroup - 1) / kTokGroup + t / kTokGroup;
-        const long item = (long)g * D.nbands + band;
-        s += expert_out(D, D.cut[item], item, a.T * a.k + t, t % kTokGroup, c);
-    }
+    if (sh) s += vsh;
     *reinterpret_cast<u32x2 *>(a.y + (size_t)t * a.d + c) = u32x2{pack_bf16x2(s[0], s[1]), pack_bf16x2(s[2], s[3])};
 }
 
@@ -1361,6 +1457,8 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     g.band_rows = 16 * kWG;
     g.nbands = (a.d_ff + g.band_rows - 1) / g.band_rows;
     g.workers = G;
+    g.mat_bytes = packed_matrix_bytes(FMT, a.d_ff, a.d);
+    g.sc_bytes = packed_scale_bytes(FMT, a.d_ff, a.d);
     g.partials = partials;
     g.slot_floats = ws.slot_floats;
     g.ranges = reinterpret_cast<long long *>(partials + (size_t)G * 2 * ws.slot_floats);
@@ -1381,6 +1479,8 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     dn.nsteps = (dn.nblocks + SB - 1) / SB;
     dn.band_rows = 32 * kWG;
     dn.nbands = (a.d + dn.band_rows - 1) / dn.band_rows;
+    dn.mat_bytes = packed_matrix_bytes(FMT, a.d, a.d_ff);
+    dn.sc_bytes = packed_scale_bytes(FMT, a.d, a.d_ff);
     if ((err = mark(events, 2, stream)) != hipSuccess) return err;
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD, MXA>), dim3(G), dim3(kThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;

@@ -22,6 +22,19 @@
 namespace ecospec {
 namespace split {
 
+// floor(a / b) for 0 <= a < 2^53 and 0 < b < 2^53: the double quotient is
+// within one of it (its relative error is below 2^-53 and a / b < 2^53), so
+// one correction makes it exact.  Cheaper on the GPU than a 64-bit division.
+constexpr long long div_floor(long long a, long long b)
+{
+    long long q = (long long)((double)a / (double)b);
+    if (q * b > a)
+        --q;
+    else if ((q + 1) * b <= a)
+        ++q;
+    return q;
+}
+
 // First unit x with P_x * W >= target (0 <= target <= C*K*W); n_groups*K if none.
 constexpr long first_unit(const int *cw, int n_groups, long K, long W, long long target)
 {
@@ -34,7 +47,7 @@ constexpr long first_unit(const int *cw, int n_groups, long K, long W, long long
         if ((long long)cw[mid] * K * W < target) lo = mid; else hi = mid - 1;
     }
     const long long base = (long long)cw[lo] * K * W, cg = cw[lo + 1] - cw[lo];
-    const long long r = (target - base + cg * W - 1) / (cg * W);
+    const long long r = div_floor(target - base + cg * W - 1, cg * W);
     return r >= K ? (long)(lo + 1) * K : (long)lo * K + (long)r;
 }
 
@@ -44,7 +57,7 @@ constexpr int owner_of(const int *cw, int n_groups, long K, int W, long x)
     const int g = (int)(x / K);
     const long long cg = cw[g + 1] - cw[g];
     const long long px = (long long)cw[g] * K + (x - (long long)g * K) * cg;
-    return (int)(px * W / ((long long)cw[n_groups] * K));
+    return (int)div_floor(px * W, (long long)cw[n_groups] * K);
 }
 
 // Partial-sum slot of range [v0, v1) for the item of units [ib, ie), or -1 if

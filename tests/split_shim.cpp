@@ -16,4 +16,5 @@ long long split_contributors(const int *cw, const long long *bound, int n_groups
 }
 int split_piece_slot(int v, long v0, long v1, long ib, long ie) { return piece_slot(v, v0, v1, ib, ie); }
 long split_finished_item(long x0, long x1, long ns) { return finished_item(x0, x1, ns); }
+long long split_div_floor(long long a, long long b) { return div_floor(a, b); }
 }

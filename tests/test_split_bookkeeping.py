@@ -48,6 +48,8 @@ def lib(tmp_path_factory):
     L.split_piece_slot.restype = i
     L.split_finished_item.argtypes = [l, l, l]
     L.split_finished_item.restype = l
+    L.split_div_floor.argtypes = [ll, ll]
+    L.split_div_floor.restype = ll
     return L
 
 
@@ -177,3 +179,46 @@ def test_random_costs_and_grids(lib):
         W = int(rng.choice([1, 2, 3, 7, 64, 256, 512]))
         wide += run_case(lib, costs, nbands, nsteps, W)
     assert wide > 0
+
+
+def test_div_floor_is_exact(lib):
+    # The split's divisions go through a double quotient corrected by one step; its operands stay
+    # below 2^45 (cost total x units per group x workgroups).  Exact against Python integers,
+    # including quotients that sit on or next to an integer, where the double rounds either way.
+    rng = np.random.default_rng(11)
+    cases = [(0, 1), (1, 1), (2**45, 1), (2**45 - 1, 3), (2**52, 2**52 - 1), (2**52 - 1, 2**52)]
+    for _ in range(3000):
+        b = int(rng.integers(1, 2**int(rng.integers(1, 45))))
+        q = int(rng.integers(0, 2**45 // b + 1))
+        for a in (q * b - 1, q * b, q * b + 1, q * b + b - 1):
+            if 0 <= a < 2**52:
+                cases.append((a, b))
+    for a, b in cases:
+        assert lib.split_div_floor(a, b) == a // b, (a, b)
+
+
+def test_first_unit_at_large_magnitudes(lib):
+    # Targets near the largest the kernels produce (4096 groups, 2^17 units per group, 512
+    # workgroups): first_unit against the definition in exact integers.
+    rng = np.random.default_rng(5)
+    for _ in range(40):
+        n = int(rng.integers(1, 4097))
+        costs = rng.integers(8, 42, n)
+        cw = np.concatenate([[0], np.cumsum(costs)]).astype(np.int32)
+        K = int(rng.integers(1, 2**17))
+        W = int(rng.choice([256, 512]))
+        C_tot = int(cw[-1]) * K
+        for w in rng.integers(0, W + 1, 16).tolist():
+            target = C_tot * int(w)
+            # smallest unit x = g*K + r with (cw[g]*K + r*c_g) * W >= target
+            if target <= 0:
+                want = 0
+            elif target >= C_tot * W:
+                want = n * K
+            else:
+                g = int(np.searchsorted(cw[:-1].astype(np.int64) * K * W, target, side="left")) - 1
+                base, cg = int(cw[g]) * K * W, int(costs[g])
+                r = -(-(target - base) // (cg * W))
+                want = (g + 1) * K if r >= K else g * K + r
+            got = lib.split_first_unit(cw.ctypes.data, n, K, W, target)
+            assert got == want, (n, K, W, w)
