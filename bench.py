@@ -17,7 +17,7 @@ Prints ONE JSON line on stdout; progress goes to stderr.
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--no-sweep] [--no-cpu] [--no-stack]
     python bench.py --profile [--shape ds|gpt]       # short run for rocprofv3 (+ a copy kernel for counter calibration)
-    python bench.py --summarize-kstats DIR OUT       # rocprofv3 --kernel-trace --stats output -> profiles/ summary
+    python bench.py --summarize-kstats DIR OUT [--shape ds|gpt]  # rocprofv3 --kernel-trace --stats output -> profiles/ summary
     python bench.py --summarize-pmc FETCH WRITE OUT [--shape ds|gpt]  # rocprofv3 --pmc output -> profiles/ summary
 """
 from __future__ import annotations
@@ -40,6 +40,8 @@ METRIC = "MoE verify-layer µs and HBM GB/s vs unique experts (V3.1 shape, FP8)"
 PEAK_HBM_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 KSTATS_SUMMARY = os.path.join(PROFILES, "verify_ds_fp8_T64_U32.kernel_stats.txt")
+KSTATS_FILES = {"ds": "profiles/verify_ds_fp8_T64_U32.kernel_stats.txt",
+                "gpt": "profiles/verify_gpt_mxfp4_T64_U32.kernel_stats.txt"}
 PMC_SUMMARY = {"ds": os.path.join(PROFILES, "expert_ffn_ds_fp8_T64_U32.pmc.txt"),
                "gpt": os.path.join(PROFILES, "expert_ffn_gpt_mxfp4_T64_U32.pmc.txt")}
 FFN_SOURCE = os.path.join(ROOT, "paper_2607_12696_amd", "csrc", "expert_ffn.hip")
@@ -611,19 +613,20 @@ class Stack:
 
 # --------------------------------------------------------------------------- profiler summaries
 
-def summarize_kstats(kt_dir, out_path):
+def summarize_kstats(kt_dir, out_path, shape="ds"):
     """The library's kernels of a `rocprofv3 --kernel-trace --stats` run of `bench.py --profile`."""
     paths = glob.glob(os.path.join(kt_dir, "**", "*kernel_stats.csv"), recursive=True)
     if not paths:
         raise SystemExit(f"no kernel_stats.csv under {kt_dir}")
     rows = [r for r in csv.DictReader(open(paths[0])) if "ecospec" in r["Name"] and "pack" not in r["Name"]]
     rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    name = {"ds": "DeepSeek-V3.1-shaped FP8 layer, T=64 draft tokens routed to U=32 of 256 experts + 1 shared",
+            "gpt": "GPT-OSS-120B-shaped MXFP4 layer, T=64 draft tokens routed to U=32 of 128 experts"}[shape]
     with open(out_path, "w") as f:
-        f.write("# rocprofv3 kernel-trace statistics of the verification pass: DeepSeek-V3.1-shaped FP8 layer,\n")
-        f.write("# T=64 draft tokens routed to U=32 of 256 experts + 1 shared (55 steps: 5 warm-up + 50, as bench.py\n")
-        f.write("# times them).\n# commands (repository root, TMPDIR=/tmp):\n")
-        f.write("#   rocprofv3 --kernel-trace --stats -d KT_DIR --output-format csv -- python3 bench.py --profile\n")
-        f.write("#   python3 bench.py --summarize-kstats KT_DIR profiles/verify_ds_fp8_T64_U32.kernel_stats.txt\n")
+        f.write(f"# rocprofv3 kernel-trace statistics of the verification pass: {name}\n")
+        f.write("# (55 steps: 5 warm-up + 50, as bench.py times them).\n# commands (repository root, TMPDIR=/tmp):\n")
+        f.write(f"#   rocprofv3 --kernel-trace --stats -d KT_DIR --output-format csv -- python3 bench.py --profile --shape {shape}\n")
+        f.write(f"#   python3 bench.py --summarize-kstats KT_DIR {KSTATS_FILES[shape]} --shape {shape}\n")
         f.write("# rows: this library's kernels of the steps (weight packing and input generation omitted)\n")
         f.write(f"kernel_source_sha: {source_sha()}\n")
         f.write("# kernel | calls | average us | min us | max us\n")
@@ -662,7 +665,7 @@ def summarize_pmc(fetch_dir, write_dir, out_path, shape):
         f.write("# commands (repository root, TMPDIR=/tmp):\n")
         f.write(f"#   rocprofv3 --pmc FETCH_SIZE -d FETCH_DIR --output-format csv -- python3 bench.py --profile --shape {shape}\n")
         f.write(f"#   rocprofv3 --pmc WRITE_SIZE -d WRITE_DIR --output-format csv -- python3 bench.py --profile --shape {shape}\n")
-        f.write(f"#   python3 bench.py --summarize-pmc FETCH_DIR WRITE_DIR {os.path.relpath(out_path, ROOT)} --shape {shape}\n")
+        f.write(f"#   python3 bench.py --summarize-pmc FETCH_DIR WRITE_DIR {os.path.relpath(PMC_SUMMARY[shape], ROOT)} --shape {shape}\n")
         f.write("# counters are KiB per dispatch; each is scaled by COPY_BYTES / (its reading for the calibration\n")
         f.write("# kernel, torch.bitwise_not over 1 GiB of int32, which reads and writes 1 GiB each)\n")
         f.write(f"kernel_source_sha: {source_sha()}\n")
@@ -715,7 +718,7 @@ def main():
     args = ap.parse_args()
 
     if args.summarize_kstats:
-        summarize_kstats(*args.summarize_kstats)
+        summarize_kstats(*args.summarize_kstats, args.shape)
         return 0
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.shape)

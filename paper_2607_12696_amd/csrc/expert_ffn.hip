@@ -274,6 +274,9 @@ __device__ __forceinline__ Plan load_plan(const FfnParams &P)
 #ifndef ECOSPEC_COST_FP4_MX
 #define ECOSPEC_COST_FP4_MX 16
 #endif
+#ifndef ECOSPEC_COST_BLOCK
+#define ECOSPEC_COST_BLOCK 3  // per 16-token block
+#endif
 template <int FMT, bool MXA>
 __device__ __forceinline__ int group_cost(int M)
 {
@@ -281,7 +284,7 @@ __device__ __forceinline__ int group_cost(int M)
                     : FMT == FMT_FP8  ? ECOSPEC_COST_FP8
                     : MXA             ? ECOSPEC_COST_FP4_MX
                                       : ECOSPEC_COST_FP4;
-    return A + 3 * ((M + 15) / 16);
+    return A + ECOSPEC_COST_BLOCK * ((M + 15) / 16);
 }
 
 constexpr int kMaxTokLds = 4096;  // routed slots whose token rows are staged in LDS
@@ -460,16 +463,25 @@ __device__ __forceinline__ ItemBias load_bias(const FfnParams &P, const ItemDesc
     return b;
 }
 
+// g * sigmoid(s * g) with the hardware exp2 and reciprocal (about 2 ulp in
+// fp32, far below the bf16 rounding of H): g / (1 + e^(-s g)).  Large -s g
+// gives 1 + inf, whose reciprocal is 0, and NaN stays NaN, as in the
+// division form.
+__device__ __forceinline__ float gated(float g, float s)
+{
+    return g * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-s * g * 1.44269504088896341f));
+}
+
 // h from the gate and up values of one row (biases already added):
 // act 0 silu(g) * u; act 1 (GPT-OSS) with g capped at limit and u clamped to
 // [-limit, limit], g * sigmoid(alpha * g) * (u + 1).  The comparisons keep NaN.
 __device__ __forceinline__ float activate(const VerifyArgs &a, float g, float u)
 {
-    if (a.act == 0) return g / (1.f + expf(-g)) * u;
+    if (a.act == 0) return gated(g, 1.f) * u;
     if (g > a.limit) g = a.limit;
     if (u > a.limit) u = a.limit;
     if (u < -a.limit) u = -a.limit;
-    return g / (1.f + expf(-a.alpha * g)) * (u + 1.f);
+    return gated(g, a.alpha) * (u + 1.f);
 }
 
 // Finishes a wavefront's (tile 0, tile 1) accumulators of an item: gate/up ->
@@ -533,7 +545,7 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
                     const float g0 = g[2 * i], g1 = g[2 * i + 1];
-                    h2[i] = pack_bf16x2(g0 / (1.f + expf(-g0)) * v[2 * i], g1 / (1.f + expf(-g1)) * v[2 * i + 1]);
+                    h2[i] = pack_bf16x2(gated(g0, 1.f) * v[2 * i], gated(g1, 1.f) * v[2 * i + 1]);
                 }
             } else {
                 g += bias.g;
