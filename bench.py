@@ -210,14 +210,16 @@ class Runner:
         self.ws = torch.empty(moe.moe_verify_workspace_size(self.wds[0], T, sh.k), dtype=torch.uint8, device=dev)
 
     def step(self, lg, i, events=None):
-        """One pass of the hot path; events = optional 6 marks: before route, then the 5 marks of the
-        timed verify entry point (before and after the gate/up expert kernel, before and after the down
-        expert kernel, after combine)."""
+        """One pass of the hot path: the router top-k, then the verification, which builds the expert
+        union and grouping itself (in the gate/up kernel; T > 64: a union kernel and the token-group plan
+        first).  events = optional 6 marks: before the top-k, then the 5 marks of the timed verify entry
+        point (before and after the gate/up expert kernel, before and after the down expert kernel, after
+        combine)."""
         moe, sh = self.moe, self.sh
         wd = self.wds[i % len(self.wds)]
         if events is not None:
             events[0].record()
-        moe.moe_route_union(lg, sh.k, sh.score, out=self.r)
+        moe.moe_route_topk(lg, sh.k, sh.score, topk_idx=self.r.topk_idx, topk_w=self.r.topk_w)
         if events is None:
             moe.moe_verify_layer(self.x, wd, self.r, y=self.y, workspace=self.ws)
         else:
@@ -274,7 +276,7 @@ class Runner:
         for i in range(steps):
             self.step(pool[(warmup + i) % len(pool)], warmup + i, evs[i])
         torch.cuda.synchronize()
-        spans = {"step": (0, 5), "route_union": (0, 1), "verify": (1, 5), "gateup": (1, 2), "gateup_fixup": (2, 3),
+        spans = {"step": (0, 5), "route": (0, 1), "verify": (1, 5), "gateup": (1, 2), "gateup_fixup": (2, 3),
                  "down": (3, 4), "combine": (4, 5)}
         return {k: [e[a].elapsed_time(e[b]) for e in evs] for k, (a, b) in spans.items()}
 
@@ -532,7 +534,8 @@ class Stack:
         """The 8-layer pass for one selection; returns the layer outputs."""
         moe, sh = self.moe, self.sh
         for l in range(self.L):
-            moe.moe_route_union(logits[l], sh.k, sh.score, out=self.routs[l])
+            r = self.routs[l]
+            moe.moe_route_topk(logits[l], sh.k, sh.score, topk_idx=r.topk_idx, topk_w=r.topk_w)
             moe.moe_verify_layer(self.xs[l], self.layers[l], self.routs[l], y=self.ys[l], workspace=self.ws)
         return self.ys
 

@@ -134,17 +134,21 @@ typedef struct {
     int down_paired;
 } moe_weights_t;
 
-/* Routing of T tokens as produced by moe_route_topk + moe_expert_union
- * (device pointers).  Slot s = t*k + j is the j-th expert of token t. */
+/* Routing of T tokens (device pointers).  Slot s = t*k + j is the j-th
+ * expert of token t.  topk_idx and topk_w are moe_route_topk's output; the
+ * union and grouping arrays are moe_expert_union's output for that topk_idx.
+ * moe_verify_layer reads topk_idx and topk_w and writes the union and
+ * grouping arrays itself (the same values moe_expert_union gives), so they
+ * need not be filled before the call. */
 typedef struct {
     int T, k, E;
     const int32_t *topk_idx; /* [T][k] */
     const float *topk_w;     /* [T][k] */
-    const int32_t *counts;   /* [E]    */
-    const int32_t *union_ids;/* [E]    */
-    const int32_t *n_unique; /* [1]    */
-    const int32_t *offsets;  /* [E+1]  */
-    const int32_t *perm;     /* [T*k]  */
+    int32_t *counts;         /* [E]    */
+    int32_t *union_ids;      /* [E]    */
+    int32_t *n_unique;       /* [1]    */
+    int32_t *offsets;        /* [E+1]  */
+    int32_t *perm;           /* [T*k]  */
 } moe_routing_t;
 
 /*
@@ -298,7 +302,10 @@ moe_status_t moe_verify_workspace_size(const moe_weights_t *w, int T, int k, siz
  * Each distinct routed expert (and the shared one) is streamed from HBM once
  * per call for up to 64 of its tokens (once per 64 tokens beyond that).
  *   x  [T][d] bf16 in, y [T][d] bf16 out (may not alias x), device.
- *   r  routing from moe_route_topk + moe_expert_union for the same T, k, E.
+ *   r  routing for the same T, k, E: topk_idx and topk_w in (moe_route_topk);
+ *      counts, union_ids, n_unique, offsets and perm out, the union of the
+ *      routed experts and the grouping of the slots by expert (Eq. 1), as
+ *      moe_expert_union computes them (their contents on entry do not matter).
  *   workspace: device buffer of at least moe_verify_workspace_size bytes,
  *   256-byte aligned; its contents on entry do not matter.
  * Arithmetic: weights decoded exactly to bf16, bf16 matrix cores with fp32

@@ -205,7 +205,8 @@ def moe_route_topk_hidden(x, w_router, k: int, score: int, logits=None, workspac
 
 @dataclass
 class Routing:
-    """Device routing of T tokens: the outputs of moe_route_topk and moe_expert_union."""
+    """Device routing of T tokens: the outputs of moe_route_topk and moe_expert_union.  moe_verify_layer
+    reads topk_idx / topk_w and writes the union and grouping arrays itself."""
     T: int
     k: int
     E: int
@@ -239,6 +240,16 @@ def moe_expert_union(topk_idx, E: int, topk_w=None, out: Routing | None = None) 
         _dev_ptr(out.n_unique, "n_unique"), _dev_ptr(out.offsets, "offsets"), _dev_ptr(out.perm, "perm"),
         _stream(topk_idx)))
     return out
+
+
+def routing_for(topk_idx, topk_w, E: int) -> Routing:
+    """A Routing around a top-k (moe_route_topk's output) with empty union and grouping arrays, which
+    moe_verify_layer fills."""
+    torch = _torch()
+    T, k = topk_idx.shape
+    i32 = dict(dtype=torch.int32, device=topk_idx.device)
+    return Routing(T, k, E, topk_idx, topk_w, torch.empty(E, **i32), torch.empty(E, **i32), torch.empty(1, **i32),
+                   torch.empty(E + 1, **i32), torch.empty(T * k, **i32))
 
 
 def moe_route_union(logits, k: int, score: int, out: Routing | None = None) -> Routing:
@@ -432,8 +443,10 @@ def moe_verify_layer_timed(x, weights: dict, routing: Routing, y, workspace, eve
 
 
 def moe_verify_step(x, logits, weights: dict, k: int, score: int, workspace=None, y=None):
-    """Route, union and verify one layer: the whole hot path on the device."""
-    r = moe_route_union(logits, k, score)
+    """Route (top-k), then verify one layer, which builds the union and grouping itself: the whole hot
+    path on the device.  Returns y and the routing, its union arrays filled by the verification."""
+    idx, w = moe_route_topk(logits, k, score)
+    r = routing_for(idx, w, logits.shape[1])
     return moe_verify_layer(x, weights, r, y=y, workspace=workspace), r
 
 

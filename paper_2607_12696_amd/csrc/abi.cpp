@@ -194,7 +194,7 @@ moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe_routin
     if (!aligned(x, 16) || !aligned(y, 16) || !aligned(workspace, 256)) return MOE_ERR_INVALID_ARG;
     if (r->T < 1 || r->k < 1 || r->k > kMaxK || r->k > w->E || r->E != w->E || (long)r->T * r->k > kMaxSlots)
         return MOE_ERR_INVALID_ARG;
-    if (!r->topk_idx || !r->topk_w || !r->union_ids || !r->n_unique || !r->offsets || !r->perm)
+    if (!r->topk_idx || !r->topk_w || !r->counts || !r->union_ids || !r->n_unique || !r->offsets || !r->perm)
         return MOE_ERR_INVALID_ARG;
     const bool shared = w->sh_gate != nullptr;
     const ecospec::VerifyWorkspace ws =
@@ -238,6 +238,7 @@ moe_status_t verify_impl(const void *x, const moe_weights_t *w, const moe_routin
     a.b_up = w->b_up;
     a.b_down = w->b_down;
     a.act_fmt = w->act_fmt;
+    a.counts = r->counts;
     a.union_ids = r->union_ids;
     a.n_unique = r->n_unique;
     a.offsets = r->offsets;

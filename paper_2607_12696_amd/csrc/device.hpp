@@ -119,4 +119,20 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *wave_tot, int *t
     return before + incl - v;
 }
 
+// Rank of this lane's expert e among the lower lanes holding e, and whether
+// this lane is the highest lane holding e (ok: the lane holds a valid expert).
+__device__ __forceinline__ void wave_match(int e, bool ok, int nbits, int &rank, bool &top, int &count)
+{
+    const int lane = lane_id();
+    uint64_t peers = __ballot(ok);
+    for (int b = 0; b < nbits; ++b) {
+        const bool bit = ok && ((e >> b) & 1);
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    rank = __popcll(peers & ((1ull << lane) - 1ull));
+    count = __popcll(peers);
+    top = ok && lane == 63 - __clzll(peers);
+}
+
 }  // namespace ecospec

@@ -365,6 +365,130 @@ __device__ __forceinline__ Plan build_costs(const FfnParams &P, Split &sp)
     return pl;
 }
 
+// Gate/up launch without a token-group plan (T <= 64: every expert's tokens
+// form one group).  The union of the routed experts and the grouping of the
+// slots by expert (Eq. 1, the stable counting sort moe_expert_union computes)
+// are built by each workgroup in LDS straight from topk_idx, with the groups'
+// costs; workgroup 0 also writes them to the routing arrays for the later
+// launches and the caller.  Per pass of 512 slots: wavefront matches by ballot
+// (rank among equal experts, count per wavefront), per-expert counts in
+// wcnt[kWG][E] (scratch in the activation tiles, unused this early); one scan
+// over the experts in id order (= union order) gives each member its union
+// position and first grouped position, a second one the cost prefix; a second
+// sweep places every slot.
+template <int FMT, bool MXA>
+__device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, int *wcnt)
+{
+    constexpr int kPass = 8;  // slots: T * k <= 64 * 64 = kPass * kThreads
+    constexpr int EPT = 2;    // experts per thread: E <= 1024
+    const VerifyArgs &a = P.a;
+    const int S = a.T * a.k, E = a.E, tid = threadIdx.x, wave = tid / kWave;
+    const bool out = blockIdx.x == 0;
+    int nbits = 0;
+    while ((1 << nbits) < E) ++nbits;
+    const int passes = (S + kThreads - 1) / kThreads;
+    int ex[kPass], rank[kPass], cnt[kPass];
+    bool top[kPass];
+#pragma unroll
+    for (int ps = 0; ps < kPass; ++ps) {
+        const int sl = ps * kThreads + tid;
+        ex[ps] = ps < passes && sl < S ? a.topk_idx[sl] : -1;
+        rank[ps] = cnt[ps] = 0;
+        top[ps] = false;
+    }
+    // Counts per expert over the passes.
+    int tot[EPT] = {0, 0};
+#pragma unroll
+    for (int ps = 0; ps < kPass; ++ps) {
+        if (ps >= passes) break;
+        for (int i = tid; i < kWG * E; i += kThreads) wcnt[i] = 0;
+        __syncthreads();
+        wave_match(ex[ps], (unsigned)ex[ps] < (unsigned)E, nbits, rank[ps], top[ps], cnt[ps]);
+        if (top[ps]) wcnt[wave * E + ex[ps]] = cnt[ps];
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < EPT; ++j) {
+            const int e = j * kThreads + tid;
+            if (e < E)
+                for (int w = 0; w < kWG; ++w) tot[j] += wcnt[w * E + e];
+        }
+        __syncthreads();
+    }
+    // Union positions, first grouped positions and the cost prefix.  A group
+    // keeps at most 64 tokens (more only with repeated experts within a token).
+    int run_u = 0, run_p = 0, run_c = 0, start[EPT];
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) {
+        const int e = j * kThreads + tid;
+        const int c = e < E ? tot[j] : 0;
+        const int M = min(kTokGroup, c);
+        int tup = 0, tcost = 0;
+        const int up = block_exclusive_scan((c << 11) | (c > 0 ? 1 : 0), sp.wave_tot, &tup);
+        const int cp = block_exclusive_scan(c > 0 ? group_cost<FMT, MXA>(M) : 0, sp.wave_tot, &tcost);
+        const int pos = run_u + (up & 2047);
+        start[j] = run_p + (up >> 11);
+        if (c > 0) {
+            sp.ge[pos] = e;
+            sp.gp0[pos] = start[j];
+            sp.gM[pos] = M;
+            sp.cw[pos] = run_c + cp;
+        }
+        if (out && e < E) a.counts[e] = c;
+        run_u += tup & 2047;
+        run_p += tup >> 11;
+        run_c += tcost;
+    }
+    Plan pl;
+    pl.U = run_u;
+    pl.n_groups = run_u + (a.sh_gate ? 1 : 0);
+    if (tid == 0) {
+        int total = run_c;
+        if (a.sh_gate) {  // the shared expert: all T tokens, after every routed slot
+            sp.ge[run_u] = -1;
+            sp.gp0[run_u] = S;
+            sp.gM[run_u] = min(kTokGroup, a.T);
+            sp.cw[run_u] = run_c;
+            total += group_cost<FMT, MXA>(min(kTokGroup, a.T));
+        }
+        sp.cw[pl.n_groups] = total;
+    }
+    // Placement: first position of the expert + slots of earlier passes and wavefronts + rank.
+    int run[EPT] = {start[0], start[1]};
+#pragma unroll
+    for (int ps = 0; ps < kPass; ++ps) {
+        if (ps >= passes) break;
+        for (int i = tid; i < kWG * E; i += kThreads) wcnt[i] = 0;
+        __syncthreads();
+        if (top[ps]) wcnt[wave * E + ex[ps]] = cnt[ps];
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < EPT; ++j) {
+            const int e = j * kThreads + tid;
+            if (e < E)
+                for (int w = 0; w < kWG; ++w) {
+                    const int nw = wcnt[w * E + e];
+                    wcnt[w * E + e] = run[j];
+                    run[j] += nw;
+                }
+        }
+        __syncthreads();
+        if ((unsigned)ex[ps] < (unsigned)E) {
+            const int pos = wcnt[wave * E + ex[ps]] + rank[ps], sl = ps * kThreads + tid;
+            sp.tok[pos] = sl / a.k;
+            if (out) a.perm[pos] = sl;
+        }
+        __syncthreads();
+    }
+    if (out) {
+        for (int u = tid; u <= E; u += kThreads) {
+            if (u < E) a.union_ids[u] = u < run_u ? sp.ge[u] : -1;
+            a.offsets[u] = u < run_u ? sp.gp0[u] : run_p;
+        }
+        if (tid == 0) *a.n_unique = run_u;
+    }
+    return pl;
+}
+
 // First unit x with P_x * W >= target (0 <= target <= C * W), by binary
 // search over the groups' cost prefix.
 __device__ __forceinline__ long first_unit(const Split &sp, int n_groups, long K, long W, long long target)
@@ -842,7 +966,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int tid = threadIdx.x, br = tid >> 4, bc = tid & 15;
     const int nsteps = P.nsteps, K = P.K;
     __shared__ Split sp;
-    const Plan pl = build_costs<FMT, MXA>(P, sp);
+    static_assert(kTiles(PD) * BBUF >= kWG * 1024 * 4, "the union's scratch fits the activation tiles");
+    const Plan pl = !DOWN && P.plan == nullptr ? union_and_costs<FMT, MXA>(P, sp, reinterpret_cast<int *>(lds))
+                                               : build_costs<FMT, MXA>(P, sp);
     build_bounds(sp, pl.n_groups, (long)P.nbands * nsteps, P.workers);
     // Unit indices fit in 32 bits (fewer than 2^30 units: every matrix is below 2^31 bytes and a
     // launch has at most 4096 token groups), so the unit arithmetic below is 32-bit.
@@ -1442,6 +1568,10 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     hipError_t err;
 
     if (grouped) {
+        // The token-group plan needs the union first; without it the gate/up kernel builds the union itself.
+        if ((err = launch_expert_union(a.topk_idx, a.T, a.k, a.E, a.counts, a.union_ids, a.n_unique, a.offsets,
+                                       a.perm, stream)) != hipSuccess)
+            return err;
         hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(256), 0, stream, a, plan);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }

@@ -26,22 +26,6 @@ namespace ecospec {
 constexpr int kUnionThreads = 1024;
 constexpr int kUnionWaves = kUnionThreads / kWave;
 
-// Rank of this lane's expert e among the lower lanes holding e, and whether
-// this lane is the highest lane holding e (ok: the lane holds a valid expert).
-__device__ __forceinline__ void wave_match(int e, bool ok, int nbits, int &rank, bool &top, int &count)
-{
-    const int lane = lane_id();
-    uint64_t peers = __ballot(ok);
-    for (int b = 0; b < nbits; ++b) {
-        const bool bit = ok && ((e >> b) & 1);
-        const uint64_t m = __ballot(bit);
-        peers &= bit ? m : ~m;
-    }
-    rank = __popcll(peers & ((1ull << lane) - 1ull));
-    count = __popcll(peers);
-    top = ok && lane == 63 - __clzll(peers);
-}
-
 // The union, scans and grouping of S routed slots idx[0 .. S) (global or LDS),
 // by the whole 1024-thread workgroup.
 __device__ __forceinline__ void union_block(const int32_t *idx, int S, int E, int32_t *__restrict__ counts,

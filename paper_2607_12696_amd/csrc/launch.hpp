@@ -39,7 +39,9 @@ struct VerifyArgs {
     int act;             // 0: SwiGLU, 1: GPT-OSS clamped SwiGLU
     float alpha, limit;
     const float *b_gate, *b_up, *b_down;  // routed experts' biases or null
-    const int32_t *union_ids, *n_unique, *offsets, *perm;
+    // The union and grouping of the slots (Eq. 1): written by the call itself (by the gate/up kernel, or by
+    // the union kernel when T > 64), read by its later kernels.
+    int32_t *counts, *union_ids, *n_unique, *offsets, *perm;
     const uint16_t *x;  // [T][d] bf16
     uint16_t *y;        // [T][d] bf16
     uint16_t *h;        // workspace: [T*k (+T)][d_ff] bf16 SwiGLU rows at grouped positions

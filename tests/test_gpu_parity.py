@@ -623,6 +623,54 @@ def test_workspace_contents_do_not_matter():
     assert torch.equal(y1, y2)
 
 
+UNION_SHAPES = {
+    **{n: SMALL[n] for n in ("toy", "fp8", "mxfp4", "bf16_tail")},
+    # 1024 experts, top-16: two experts per thread and, at T = 64, two passes of 512 slots in the gate/up
+    # kernel's own union.
+    "many_e": synth.Shape("many_e", 64, 64, 1024, 16, synth.FMT_BF16, 0, False),
+}
+_union_layers = {}
+
+
+@pytest.mark.parametrize("name", list(UNION_SHAPES))
+@pytest.mark.parametrize("T", [1, 8, 64, 130])
+@pytest.mark.parametrize("bad", [False, True])
+def test_verify_builds_the_union_itself(name, T, bad):
+    # The verification writes the union and grouping of Eq. 1 itself (in the gate/up kernel for T <= 64, by
+    # the union kernel beyond): from a bare top-k, with garbage in the union arrays, it gives the oracle's
+    # union and grouping bit for bit and the same y as from moe_expert_union's routing.  bad: some slots
+    # name an expert outside [0, E); they are never placed and add nothing.
+    sh = UNION_SHAPES[name]
+    note(f"verify builds the union shape={name} T={T} bad={bad}")
+    if name not in _union_layers:
+        _union_layers[name] = synth.layer_weights(sh, seed=29)
+    dl = to_dev(_union_layers[name])
+    x = synth.activations(T, sh.d, seed=3 * T).to(DEV)
+    lg = synth.logits_scattered(T, sh.E, seed=3 * T + 1).to(DEV)
+    idx, w = moe.moe_route_topk(lg, sh.k, sh.score)
+    if bad:
+        idx = idx.clone()
+        idx.view(-1)[:: 7] = sh.E + 3
+    r1 = moe.moe_expert_union(idx, sh.E, topk_w=w)
+    y1 = moe.moe_verify_layer(x, dl, r1)
+    r2 = moe.routing_for(idx, w, sh.E)
+    for t in (r2.counts, r2.union_ids, r2.n_unique, r2.offsets, r2.perm):
+        t.fill_(-7)
+    y2 = moe.moe_verify_layer(x, dl, r2)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    if bad:  # the oracle refuses such slots: compare with moe_expert_union, which skips them too
+        u = {n: getattr(r1, n).cpu().numpy() for n in ("counts", "union_ids", "offsets", "perm")}
+        u["n_unique"] = int(r1.n_unique.item())
+    else:
+        u = oracle.union(idx.cpu().numpy(), sh.E)
+    placed = int(u["offsets"][-1])
+    assert int(r2.n_unique.item()) == u["n_unique"]
+    for n in ("counts", "union_ids", "offsets"):
+        assert np.array_equal(getattr(r2, n).cpu().numpy(), u[n]), n
+    assert np.array_equal(r2.perm.cpu().numpy()[:placed], u["perm"][:placed])
+
+
 # ----------------------------------------------------------------------------- MX activation mode
 
 # MXFP4 weights with MX FP8 activations on the scaled FP4 x FP8 matrix-core instruction, against the
