@@ -119,6 +119,49 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *wave_tot, int *t
     return before + incl - v;
 }
 
+// Two block-wide exclusive scans in one pass (three barriers for both).
+// wave_tot: 2 * (blockDim.x / kWave) ints of LDS.
+__device__ __forceinline__ void block_exclusive_scan2(int v0, int v1, int *wave_tot, int &ex0, int &ex1, int &tot0,
+                                                      int &tot1)
+{
+    const int lane = lane_id(), wave = threadIdx.x / kWave, nwaves = blockDim.x / kWave;
+    int a = v0, b = v1;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int na = __shfl_up(a, o, kWave), nb = __shfl_up(b, o, kWave);
+        if (lane >= o) {
+            a += na;
+            b += nb;
+        }
+    }
+    if (lane == kWave - 1) {
+        wave_tot[wave] = a;
+        wave_tot[nwaves + wave] = b;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        int wa = lane < nwaves ? wave_tot[lane] : 0, wb = lane < nwaves ? wave_tot[nwaves + lane] : 0;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int na = __shfl_up(wa, o, kWave), nb = __shfl_up(wb, o, kWave);
+            if (lane >= o) {
+                wa += na;
+                wb += nb;
+            }
+        }
+        if (lane < nwaves) {
+            wave_tot[lane] = wa;  // inclusive wave prefixes
+            wave_tot[nwaves + lane] = wb;
+        }
+    }
+    __syncthreads();
+    ex0 = (wave > 0 ? wave_tot[wave - 1] : 0) + a - v0;
+    ex1 = (wave > 0 ? wave_tot[nwaves + wave - 1] : 0) + b - v1;
+    tot0 = wave_tot[nwaves - 1];
+    tot1 = wave_tot[2 * nwaves - 1];
+    __syncthreads();  // wave_tot is reused by the next scan
+}
+
 // Rank of this lane's expert e among the lower lanes holding e, and whether
 // this lane is the highest lane holding e (ok: the lane holds a valid expert).
 __device__ __forceinline__ void wave_match(int e, bool ok, int nbits, int &rank, bool &top, int &count)

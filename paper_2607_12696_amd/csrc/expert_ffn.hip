@@ -299,7 +299,7 @@ struct Split {
     int gM[kMaxGroups];                 // tokens in each group (<= 64)
     int ge[kMaxGroups];                 // expert id of each group (-1: the shared expert)
     int tok[kMaxTokLds];                // token of each grouped position (if T*k <= kMaxTokLds)
-    int wave_tot[kWG];
+    int wave_tot[2 * kWG];
 };
 
 // Fills sp.cw and the groups' metadata for the launch (whole workgroup) and
@@ -412,7 +412,7 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
             if (e < E)
                 for (int w = 0; w < kWG; ++w) tot[j] += wcnt[w * E + e];
         }
-        __syncthreads();
+        if (ps + 1 < passes) __syncthreads();  // one pass: its counts stay in wcnt for the placement
     }
     // Union positions, first grouped positions and the cost prefix.  A group
     // keeps at most 64 tokens (more only with repeated experts within a token).
@@ -422,9 +422,9 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
         const int e = j * kThreads + tid;
         const int c = e < E ? tot[j] : 0;
         const int M = min(kTokGroup, c);
-        int tup = 0, tcost = 0;
-        const int up = block_exclusive_scan((c << 11) | (c > 0 ? 1 : 0), sp.wave_tot, &tup);
-        const int cp = block_exclusive_scan(c > 0 ? group_cost<FMT, MXA>(M) : 0, sp.wave_tot, &tcost);
+        int up, cp, tup, tcost;
+        block_exclusive_scan2((c << 11) | (c > 0 ? 1 : 0), c > 0 ? group_cost<FMT, MXA>(M) : 0, sp.wave_tot, up, cp,
+                              tup, tcost);
         const int pos = run_u + (up & 2047);
         start[j] = run_p + (up >> 11);
         if (c > 0) {
@@ -457,10 +457,12 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
 #pragma unroll
     for (int ps = 0; ps < kPass; ++ps) {
         if (ps >= passes) break;
-        for (int i = tid; i < kWG * E; i += kThreads) wcnt[i] = 0;
-        __syncthreads();
-        if (top[ps]) wcnt[wave * E + ex[ps]] = cnt[ps];
-        __syncthreads();
+        if (passes > 1) {
+            for (int i = tid; i < kWG * E; i += kThreads) wcnt[i] = 0;
+            __syncthreads();
+            if (top[ps]) wcnt[wave * E + ex[ps]] = cnt[ps];
+            __syncthreads();
+        }
 #pragma unroll
         for (int j = 0; j < EPT; ++j) {
             const int e = j * kThreads + tid;
@@ -477,7 +479,7 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
             sp.tok[pos] = sl / a.k;
             if (out) a.perm[pos] = sl;
         }
-        __syncthreads();
+        if (ps + 1 < passes) __syncthreads();
     }
     if (out) {
         for (int u = tid; u <= E; u += kThreads) {
