@@ -387,6 +387,7 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
     int nbits = 0;
     while ((1 << nbits) < E) ++nbits;
     const int passes = (S + kThreads - 1) / kThreads;
+    const int nj = E > kThreads ? 2 : 1;  // expert rounds actually needed (the code runs cold: skip the second)
     int ex[kPass], rank[kPass], cnt[kPass];
     bool top[kPass];
 #pragma unroll
@@ -408,6 +409,7 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < EPT; ++j) {
+            if (j >= nj) break;
             const int e = j * kThreads + tid;
             if (e < E)
                 for (int w = 0; w < kWG; ++w) tot[j] += wcnt[w * E + e];
@@ -416,9 +418,10 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
     }
     // Union positions, first grouped positions and the cost prefix.  A group
     // keeps at most 64 tokens (more only with repeated experts within a token).
-    int run_u = 0, run_p = 0, run_c = 0, start[EPT];
+    int run_u = 0, run_p = 0, run_c = 0, start[EPT] = {0, 0};
 #pragma unroll
     for (int j = 0; j < EPT; ++j) {
+        if (j >= nj) break;
         const int e = j * kThreads + tid;
         const int c = e < E ? tot[j] : 0;
         const int M = min(kTokGroup, c);
@@ -465,13 +468,18 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
         }
 #pragma unroll
         for (int j = 0; j < EPT; ++j) {
+            if (j >= nj) break;
             const int e = j * kThreads + tid;
-            if (e < E)
+            if (e < E) {
+                int nw[kWG];
+#pragma unroll
+                for (int w = 0; w < kWG; ++w) nw[w] = wcnt[w * E + e];
+#pragma unroll
                 for (int w = 0; w < kWG; ++w) {
-                    const int nw = wcnt[w * E + e];
                     wcnt[w * E + e] = run[j];
-                    run[j] += nw;
+                    run[j] += nw[w];
                 }
+            }
         }
         __syncthreads();
         if ((unsigned)ex[ps] < (unsigned)E) {
