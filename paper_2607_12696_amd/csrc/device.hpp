@@ -39,6 +39,36 @@ __device__ __forceinline__ u32x4 load16(rsrc_t r, uint32_t off)
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, AUX));
 }
 
+// The descriptor of make_rsrc as its four dwords (base, stride 0, range,
+// format word), for the direct-to-LDS load below.
+__device__ __forceinline__ u32x4 rsrc_words(const void *p, uint32_t bytes)
+{
+    const uint64_t v = reinterpret_cast<uintptr_t>(p);
+    return u32x4{(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) & 0xffffu,
+                 (uint32_t)__builtin_amdgcn_readfirstlane(bytes), 0x00020000u};
+}
+
+// LDS address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const void *p)
+{
+    return (uint32_t)reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void *)p);
+}
+
+// 16 bytes per lane from a raw buffer straight into LDS: lane l's bytes land
+// at lds + 16 l (lds wave-uniform, passed to the hardware in M0, which needs
+// one wait state before the load reads it); offsets beyond the buffer's range
+// write zeros.  The load counts in vmcnt like any other; it is written as
+// assembly because the compiler, seeing an LDS write it cannot place, would
+// make every later LDS read wait for all outstanding loads.  Callers
+// therefore wait for it themselves (s_waitcnt vmcnt); the compiler's own waits
+// for other loads only grow stricter from loads it does not know about.
+__device__ __forceinline__ void load16_lds(const u32x4 &rsrc, uint32_t off, uint32_t lds)
+{
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds" ::"v"(off), "s"(lds), "s"(rsrc)
+                 : "memory", "m0");
+}
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
 // Butterfly reductions over the 64 lanes of a wavefront; every lane gets the result.

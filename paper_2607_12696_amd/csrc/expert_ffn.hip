@@ -11,8 +11,9 @@
 // 128 rows of W_up (16 + 16 per wavefront), down bands are 256 rows of W_down
 // (32 per wavefront).  All eight walk the reduction dimension together in
 // macro steps of 128 elements, so the activation tile of a step (the item's
-// tokens x 128 elements) is fetched from L2 once, by coalesced 16-byte loads,
-// parked in LDS and read by every wavefront.  A single workgroup per CU keeps
+// tokens x 128 elements) is fetched from L2 once, by 16-byte loads that go
+// straight into LDS (no registers, no LDS store instructions), and read there
+// by every wavefront.  A single workgroup per CU keeps
 // the CU's waves in lockstep: two workgroups sharing a CU drift apart (the
 // older one wins instruction issue), which leaves the younger one's share of
 // an equal split running alone at the end of the launch.
@@ -26,12 +27,13 @@
 // codes are decoded exactly to bf16 in registers (v_cvt_scalef32_pk_bf16_fp8
 // with unit scale; v_cvt_scalef32_pk_bf16_fp4 with the e8m0 power of two); FP8
 // 128x128 block scales multiply the fp32 partial sum of each macro step (one
-// step lies inside one scale block).  A step's weight, scale and activation
-// loads are issued together, PD-1 steps ahead of its use: the vector-memory
-// counter retires loads in issue order, so consuming them in issue order is
-// what keeps PD-1 steps in flight.  Loads outside a buffer's range (padding
-// tokens, K tails, rows past N) return zeros; the loop has no branches
-// around loads.
+// step lies inside one scale block).  A step's weight and scale loads are
+// issued PD-1 steps ahead of its use, its activation loads right after the
+// barrier of the step PD-1 before it: the vector-memory counter retires loads
+// in issue order, so consuming them in issue order is what keeps PD-1 steps
+// in flight, and the barrier wait counts the loads still allowed in flight.
+// Loads outside a buffer's range (padding tokens, K tails, rows past N)
+// return zeros (into LDS too); the loop has no branches around loads.
 //
 // Work split ("stream-K").  All (item, step) units of a launch are laid end
 // to end and cut into contiguous ranges of equal modelled cost (a step's
@@ -120,11 +122,16 @@ template <> struct Fmt<FMT_BF16>  { static constexpr int kVecs = 4, kBlocks = 1;
 template <> struct Fmt<FMT_FP8>   { static constexpr int kVecs = 2, kBlocks = 1; };
 template <> struct Fmt<FMT_MXFP4> { static constexpr int kVecs = 1, kBlocks = 2; };
 
-// LDS geometry of one step's activation tile (64 tokens x 128 * SB elements,
-// rows padded by 16 bytes against bank conflicts).
+// LDS geometry of one step's activation tile: 64 tokens x 128 * SB bf16
+// elements, block-major.  Block b of token row r is 256 bytes at
+// b * kBlk + r * 256, its 16-byte chunk c stored in position c ^ (r % 16): the
+// tile is written by direct global-to-LDS loads, which put a wavefront's 64
+// lanes on 1 KiB of consecutive LDS (no room for row padding), and the
+// swizzle keeps the matrix-core operand reads free of bank conflicts (16
+// consecutive token rows, same chunk: 16 different positions).
 template <int SB> struct BTile {
-    static constexpr int kRow = 256 * SB + 16;  // LDS bytes per activation row
-    static constexpr int kBuf = kMB * 16 * kRow;
+    static constexpr int kBlk = kMB * 16 * 256;  // one 128-wide block of all 64 token rows
+    static constexpr int kBuf = SB * kBlk;
 };
 
 // One lane's weights of one macro step of one tile (+ their scales).  The
@@ -709,8 +716,9 @@ struct Source {
     uint32_t a0, a1;            // lane offsets of the two tiles at step 0 (kOff: rows past N)
     uint32_t kstride;           // bytes from one 128-wide block of a tile to the next
     uint32_t q0, q1;            // scale offsets at step 0
-    uint32_t boff[kBPass];      // lane offsets of this thread's activation rows at step 0 (kOff: no token)
+    uint32_t boff[kBPass];      // lane offsets of this thread's activation chunks at step 0 (kOff: no token)
     uint32_t soff[kBPass];      // MX activations: offsets of the rows' block scales at step 0
+    int kc;                     // first element (within a 128-wide block) of the thread's activation chunk
     int ib, ie;                 // the item's units [ib, ie)
     int item;
 };
@@ -765,13 +773,17 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
     }
 
     // Activation rows: in pass i, lane l of this wavefront stages row
-    // i*kBRowsPerPass + 4*wave + l/16 of the item's tokens (16 lanes per row).
+    // i*kBRowsPerPass + 4*wave + l/16 of the item's tokens (16 lanes per row)
+    // into chunk position l % 16, i.e. the row's chunk (l % 16) ^ (row % 16)
+    // (the tile's swizzle; MX activations: chunk l % 16).
     // Its source row (the token of a grouped position for gate/up, the grouped
     // position itself for down) is read by each lane for itself: no wave-wide
     // round trips.
     // MX activations: rows of nblocks * 128 e4m3fn codes and nblocks * 4 scales.
     const uint32_t brow_bytes = MXA ? (uint32_t)nblocks * kMacroK : (uint32_t)(DOWN ? a.d_ff : a.d) * 2u;
     const int q = lane >> 4;
+    const int cq = MXA ? bc : bc ^ ((4 * wave + q) & 15);
+    src.kc = cq * 8;
 #pragma unroll
     for (int i = 0; i < kBPass; ++i) {
         const int r = i * kBRowsPerPass + 4 * wave + q;
@@ -783,7 +795,7 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
                 : a.T * a.k <= kMaxTokLds ? sp.tok[p]
                                           : (int)((uint32_t)a.perm[p] / (uint32_t)a.k);
         }
-        src.boff[i] = row >= 0 ? (uint32_t)row * brow_bytes + (uint32_t)bc * 16u : kOff;
+        src.boff[i] = row >= 0 ? (uint32_t)row * brow_bytes + (uint32_t)cq * 16u : kOff;
         src.soff[i] = row >= 0 ? (uint32_t)row * (uint32_t)nblocks * 4u + (uint32_t)(bc & 1) * 4u : kOff;
     }
 }
@@ -794,15 +806,17 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
 template <int FMT, int NMB>
 __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_t *buf, f32x4 (&acc)[2][kMB])
 {
-    constexpr int SB = Fmt<FMT>::kBlocks, ROW = BTile<SB>::kRow, NS = 4 * SB;
+    constexpr int SB = Fmt<FMT>::kBlocks, NS = 4 * SB;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
-    const uint8_t *bp = buf + col * ROW + grp * 64;
-    // Sub-step s reads block s / 4 of the row (256 bytes each), 16 bytes per sub-step within it.
-    auto boff = [](int s) { return (s >> 2) * 256 + (s & 3) * 16; };
+    // Sub-step s takes chunk 4 * grp + s % 4 of block s / 4 of token row 16 * mb + col, stored
+    // at chunk position (4 * grp + s % 4) ^ col (the row's low four bits are col).
+    const uint8_t *bp = buf + col * 256;
+    const int xg = ((4 * grp) ^ col) * 16;
+    auto boff = [&](int s) { return (s >> 2) * BTile<SB>::kBlk + (xg ^ ((s & 3) * 16)); };
     bf16x8 b[2][NMB];
 #pragma unroll
     for (int mb = 0; mb < NMB; ++mb)
-        b[0][mb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * ROW));
+        b[0][mb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * 256 + boff(0)));
     // FP8 accumulates the step in `part` and adds scale * part at the end.
     f32x4 part[2][NMB];
 #pragma unroll
@@ -815,7 +829,7 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
 #pragma unroll
             for (int mb = 0; mb < NMB; ++mb)
                 b[(s + 1) & 1][mb] =
-                    __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * ROW + boff(s + 1)));
+                    __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * 256 + boff(s + 1)));
         }
         const bf16x8 av0 = decode_a<FMT>(wv[0], s), av1 = decode_a<FMT>(wv[1], s);
 #pragma unroll
@@ -839,10 +853,12 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
 // MX activation mode: LDS geometry of one step's FP8 activation tile (64
 // tokens x 256 codes, rows padded by 16 bytes) followed by its scales (8 per
 // token: 4 blocks of each of the step's two 128-wide chunks).
-// Activation tiles in LDS for a prefetch depth: the ring slots and the tiles
-// then cycle together (two suffice for correctness: a wavefront at step i's
-// barrier has finished step i - 1's contraction).
-constexpr int kTiles(int PD) { return PD % 2 ? PD : 2; }
+// Activation tiles in LDS for a prefetch depth.  Direct loads: one per ring
+// slot, the tile of step i + PD - 1 being loaded once every wavefront has
+// passed step i's barrier, i.e. finished step i - 1, the tile's last reader.
+// MX activations (staged through registers, written before the barrier): the
+// slots and tiles cycle together, two tiles sufficing for correctness.
+constexpr int kTiles(int PD, bool MXA) { return !MXA ? PD : PD % 2 ? PD : 2; }
 
 constexpr int kRowQ = 256 + 16;
 constexpr int kScaleQ = kMB * 16 * kRowQ;
@@ -962,9 +978,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     static_assert(!MXA || FMT == FMT_MXFP4, "MX activations take MXFP4 weights");
     static_assert(!MXA || 2 * (kScaleQ + kMB * 16 * 8) <= 2 * BTile<Fmt<FMT>::kBlocks>::kBuf, "MX tile fits the LDS");
     constexpr int NV = Fmt<FMT>::kVecs, SB = Fmt<FMT>::kBlocks;
-    constexpr int BROW = BTile<SB>::kRow, BBUF = BTile<SB>::kBuf;
+    constexpr int BBUF = BTile<SB>::kBuf, NT = kTiles(PD, MXA);
     constexpr uint32_t BLK = 1024u * NV;  // bytes of one 16 x 128 block of a tile
-    __shared__ __attribute__((aligned(16))) uint8_t lds[kTiles(PD) * BBUF];
+    __shared__ __attribute__((aligned(16))) uint8_t lds[NT * BBUF];
     const VerifyArgs &a = P.a;
     // Workgroups are dispatched round-robin over the 8 XCDs; taking the ranges
     // XCD-major gives each XCD one contiguous eighth of the units, so the
@@ -976,7 +992,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int tid = threadIdx.x, br = tid >> 4, bc = tid & 15;
     const int nsteps = P.nsteps, K = P.K;
     __shared__ Split sp;
-    static_assert(kTiles(PD) * BBUF >= kWG * 1024 * 4, "the union's scratch fits the activation tiles");
+    static_assert(NT * BBUF >= kWG * 1024 * 4, "the union's scratch fits the activation tiles");
     const Plan pl = !DOWN && P.plan == nullptr ? union_and_costs<FMT, MXA>(P, sp, reinterpret_cast<int *>(lds))
                                                : build_costs<FMT, MXA>(P, sp);
     build_bounds(sp, pl.n_groups, (long)P.nbands * nsteps, P.workers);
@@ -1002,6 +1018,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const rsrc_t rb = make_rsrc(MXA ? static_cast<const void *>(DOWN ? a.hq : a.xq)
                                     : static_cast<const void *>(DOWN ? a.h : a.x), rows * brow_bytes);
     const rsrc_t rsa = make_rsrc(DOWN ? a.hs : a.xs, MXA ? rows * (uint32_t)P.nblocks * 4u : 0u);
+    const u32x4 rbw = rsrc_words(DOWN ? static_cast<const void *>(a.h) : static_cast<const void *>(a.x), rows * brow_bytes);
 
     // Processing order: from the range's first item boundary to its end, then
     // the head piece before that boundary.  All workgroups thus start their
@@ -1020,12 +1037,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     set_source<FMT, DOWN, MXA>(src, P, sp, item_of(unit_of(0)));
 
     WFrag<FMT> wf[PD][2];
-    u32x4 bst[PD][kBPass][SB];
-    uint32_t sst[PD][kBPass];  // MX: the rows' block scales of a step (threads bc < 2)
-    // Loads of the i-th unit of the sequence into ring slot `slot`; past the
-    // range the loads read zeros (offsets beyond every buffer), so every path
-    // issues the same loads and the compiler's wait counts stay exact.
-    auto issue = [&](int slot, int i) {
+    u32x4 bst[MXA ? PD : 1][kBPass][SB];      // MX: the activation codes of a step
+    uint32_t sst[MXA ? PD : 1][kBPass];       // MX: the rows' block scales of a step (threads bc < 2)
+    // Vector-memory instructions per unit: weight side (weights and scales, plus MX activations)
+    // and direct activation loads.  Every unit issues exactly these, past the range too (loads
+    // of zeros: offsets beyond every buffer), so that the counted wait below is exact.
+    constexpr int kLdW = 2 * NV * SB + (FMT == FMT_FP8 ? 2 * SB : FMT == FMT_MXFP4 ? 2 : 0) + (MXA ? 2 * kBPass : 0);
+    constexpr int kLdA = MXA ? 0 : kBPass * SB;
+    // Weight-side loads of the i-th unit of the sequence into ring slot `slot`.
+    auto issue_w = [&](int slot, int i) {
         const bool ok = i < n;
         const int v = ok ? unit_of(i) : src.ib;
         if (ok && (v < src.ib || v >= src.ie)) set_source<FMT, DOWN, MXA>(src, P, sp, item_of(v));
@@ -1056,12 +1076,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                     wf[slot][0].shift = wf[slot][1].shift = (int)(kb & 3u) * 8;
                 }
             }
-            if constexpr (!MXA) {
-                const bool kok = ok && (int)kb * kMacroK + bc * 8 < K;
-#pragma unroll
-                for (int i = 0; i < kBPass; ++i)
-                    bst[slot][i][b] = load16<0>(rb, (kok && src.boff[i] != kOff) ? src.boff[i] + kb * 256u : kOff);
-            }
         }
         if constexpr (MXA) {
             // A step's 2 x 128 codes of a row are 256 contiguous bytes (16 per thread),
@@ -1073,6 +1087,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                 bst[slot][i][0] = load16<0>(rb, (aok && src.boff[i] != kOff) ? src.boff[i] + step * 256u : kOff);
                 sst[slot][i] = __builtin_amdgcn_raw_buffer_load_b32(
                     rsa, (int)((sok && src.soff[i] != kOff) ? src.soff[i] + step * 8u : kOff), 0, 0);
+            }
+        }
+    };
+    // Activation tile of the i-th unit straight into LDS tile i % PD (bf16 activations): pass p,
+    // block b of this wavefront covers token rows 32p + 4 wave .. + 3, 1 KiB of the tile.  Rows
+    // past the item's tokens and elements past K read zeros.  Uses the sources issue_w(i) set.
+    auto issue_a = [&](int i) {
+        if constexpr (!MXA) {
+            const bool ok = i < n;
+            const int v = ok ? unit_of(i) : src.ib;
+            const uint32_t step = (uint32_t)(v - src.ib);
+            const uint32_t tile = lds_addr(lds) + (uint32_t)((i % PD) * BBUF + 4 * wave * 256);
+#pragma unroll
+            for (int b = 0; b < SB; ++b) {
+                const uint32_t kb = step * SB + b;
+                const bool kok = ok && (SB == 1 || (int)kb < P.nblocks) && (int)kb * kMacroK + src.kc < K;
+#pragma unroll
+                for (int p = 0; p < kBPass; ++p)
+                    load16_lds(rbw, (kok && src.boff[p] != kOff) ? src.boff[p] + kb * 256u : kOff,
+                               tile + (uint32_t)(b * BTile<SB>::kBlk + p * kBRowsPerPass * 256));
             }
         }
     };
@@ -1088,31 +1122,34 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
         for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // One step: the loads of the unit PD - 1 places ahead, then unit i's
-    // activation tile into LDS and its contraction.  Only this part depends
-    // on the ring slot, so only it is replicated per unrolled step.
+    // One step: the weight loads of the unit PD - 1 places ahead, the wait
+    // for unit i's activation tile and the barrier, the direct activation
+    // loads of the unit PD - 1 places ahead (into the tile unit i - 1 used),
+    // then unit i's contraction.  Only this part depends on the ring slot, so
+    // only it is replicated per unrolled step.  MX activations are staged
+    // through registers and stored to LDS before the barrier instead.
     auto step = [&](int slot, int par, int i) {
-        issue((slot + PD - 1) % PD, i + PD - 1);
+        issue_w((slot + PD - 1) % PD, i + PD - 1);
         if (i >= n) return;  // the last round of the unrolled loop runs past the range
         const int nmb = (cd.M + 15) / 16;
         uint8_t *buf = lds + par * BBUF;
-        // After the previous step's barrier no wavefront still reads this buffer.
         if constexpr (MXA) {
+            // After the previous step's barrier no wavefront still reads this buffer.
 #pragma unroll
             for (int i = 0; i < kBPass; ++i) {
                 *reinterpret_cast<u32x4 *>(buf + (i * kBRowsPerPass + br) * kRowQ + bc * 16) = bst[slot][i][0];
                 if (bc < 2)
                     *reinterpret_cast<uint32_t *>(buf + kScaleQ + (i * kBRowsPerPass + br) * 8 + bc * 4) = sst[slot][i];
             }
+            __syncthreads();
         } else {
-#pragma unroll
-            for (int i = 0; i < kBPass; ++i)
-#pragma unroll
-                for (int b = 0; b < SB; ++b)
-                    *reinterpret_cast<u32x4 *>(buf + (i * kBRowsPerPass + br) * BROW + b * 256 + bc * 16) =
-                        bst[slot][i][b];
+            // This wavefront's direct loads of unit i have landed once at most the loads issued
+            // after them are outstanding: PD - 2 whole units and the weight side of unit
+            // i + PD - 1.  (A workgroup barrier with a fence would wait for every direct load,
+            // the prefetched ones too.)  The barrier then publishes all wavefronts' parts.
+            asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((PD - 2) * (kLdW + kLdA) + kLdW) : "memory");
+            issue_a(i + PD - 1);
         }
-        __syncthreads();
         if constexpr (MXA) {
             switch (nmb) {
             case 1: contract_mx<1>(wf[slot], buf, acc); break;
@@ -1165,17 +1202,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     };
 
 #pragma unroll
-    for (int j = 0; j < PD - 1; ++j) issue(j, j);
-    // The loop unrolls PD steps (ring slot j); with kTiles(PD) activation
-    // tiles (PD of them for odd PD, else 2) the tile cycles with the slot, so
-    // PD steps suffice, not 2 * PD: half the code, half the cold copies.
+    for (int j = 0; j < PD - 1; ++j) {
+        issue_w(j, j);
+        issue_a(j);
+    }
+    // The loop unrolls PD steps (ring slot j); the NT activation tiles (PD,
+    // or 2 for MX activations at even PD) cycle with the slot, so PD steps
+    // suffice, not 2 * PD: half the code, half the cold copies.
     for (int i0 = 0; i0 < n; i0 += PD) {
 #pragma unroll
         for (int j = 0; j < PD; ++j) {
-            step(j, j % kTiles(PD), i0 + j);  // the last round may run past the range: loads of zeros only
+            step(j, j % NT, i0 + j);  // the last round may run past the range: loads of zeros only
             if (i0 + j < n) end_of_piece(i0 + j);
         }
     }
+    // No direct load may still be writing this workgroup's LDS when it ends.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     write_records();
     if (DOWN) record_cuts(P, pl, sp, x0, x1);
 }
