@@ -236,7 +236,6 @@ struct FfnParams {
     int slot_floats;      // floats per partial-sum slot: partial_floats(T)
     long long *ranges;    // [workers][2]: unit range [x0, x1) of each workgroup, written by the expert kernel
     long long *fix;       // gate/up only: [workers][4] fix-up record of each workgroup (see write_fix_record)
-    long long *cut;       // down only: [groups * nbands] how combine reads each item (see record_cuts)
     const int32_t *plan;  // token groups when T > 64 (else null: one group per expert)
 };
 
@@ -305,7 +304,8 @@ struct Split {
     int gp0[kMaxGroups];                // grouped position of each group's first token
     int gM[kMaxGroups];                 // tokens in each group (<= 64)
     int ge[kMaxGroups];                 // expert id of each group (-1: the shared expert)
-    int tok[kMaxTokLds];                // token of each grouped position (if T*k <= kMaxTokLds)
+    int tok[kMaxTokLds];                // gate/up: token of each grouped position, down: its routed slot
+                                        // (if T*k <= kMaxTokLds)
     int wave_tot[2 * kWG];
 };
 
@@ -314,7 +314,7 @@ struct Split {
 // then the shared expert) the union's offsets and ids are read for every
 // possible member in the same round trip as the union size and the slots'
 // tokens: the schedule waits for global memory once, not twice.
-template <int FMT, bool MXA>
+template <int FMT, bool MXA, bool DOWN>
 __device__ __forceinline__ Plan build_costs(const FfnParams &P, Split &sp)
 {
     constexpr int kPre = 2;  // groups per thread read ahead (E <= kPre * kThreads covers every union)
@@ -332,7 +332,7 @@ __device__ __forceinline__ Plan build_costs(const FfnParams &P, Split &sp)
     }
     const Plan pl = load_plan(P);
     if (S <= kMaxTokLds)
-        for (int p = tid; p < S; p += kThreads) sp.tok[p] = a.perm[p] / a.k;
+        for (int p = tid; p < S; p += kThreads) sp.tok[p] = DOWN ? a.perm[p] : a.perm[p] / a.k;
     int run = 0;
     for (int base = 0, j = 0; base < pl.n_groups; base += kThreads, ++j) {
         const int g = base + tid;
@@ -913,23 +913,29 @@ __device__ __forceinline__ long long contributors(const FfnParams &P, const Plan
     return split::contributors(sp.cw, sp.bound, pl.n_groups, (long)P.nbands * P.nsteps, P.workers, ib, ie);
 }
 
-// Down launch: for the combine kernel, how each item this range touches is to
-// be read (every item is touched by some range, so the table is rewritten
-// whole on every launch): -1 if it is whole (its rows are in O), else its
-// contributors().
-__device__ __forceinline__ void record_cuts(const FfnParams &P, const Plan &pl, Split &sp, long x0, long x1)
+// Down launch: for the combine kernel, the output descriptor (split.hpp) of
+// every row of each item whose last unit lies in this range, so that every
+// row of every item is described by exactly one range on every launch.  A
+// whole item's row is its row of O; a cut item's row is the sum of its
+// contributors' parked partial sums, in workgroup order.  Descriptors are
+// indexed by the row's routed slot (the shared expert's rows by T*k + token).
+__device__ __forceinline__ void record_outputs(const FfnParams &P, const Plan &pl, const Split &sp, int x0, int x1)
 {
-    const long ns = P.nsteps;
-    const long i0 = x0 / ns, i1 = (x1 - 1) / ns;
-    for (long item = i0 + threadIdx.x; item <= i1; item += kThreads)
-        if (item * ns >= x0 && (item + 1) * ns <= x1) P.cut[item] = -1;
-    long it[2];
-    int n = 0;
-    if (i0 * ns < x0 || (i0 + 1) * ns > x1) it[n++] = i0;
-    if (i1 != i0 && (i1 + 1) * ns > x1) it[n++] = i1;
-    for (int i = 0; i < n; ++i) {
-        const long long c = contributors(P, pl, sp, it[i] * ns, (it[i] + 1) * ns);
-        if (threadIdx.x == 0) P.cut[it[i]] = c;
+    const VerifyArgs &a = P.a;
+    const int ns = P.nsteps, S = a.T * a.k;
+    const long K = (long)P.nbands * ns;
+    for (int item = x0 / ns; item * ns < x1; ++item) {
+        const int ib = item * ns, ie = ib + ns;
+        if (ie > x1) break;  // described by the range holding its last unit
+        const int gi = item / P.nbands, band = item - gi * P.nbands;
+        const int M = sp.gM[gi], p0 = sp.gp0[gi];
+        const bool whole = ib >= x0;
+        const uint64_t cut = whole ? 0ull : split::out_cut(sp.cw, sp.bound, pl.n_groups, K, P.workers, ib, ie);
+        for (int r = threadIdx.x; r < M; r += kThreads) {
+            const int p = p0 + r;
+            const int row = p >= S ? p : S <= kMaxTokLds ? sp.tok[p] : a.perm[p];
+            a.desc[(size_t)row * P.nbands + band] = whole ? split::out_whole((uint32_t)p) : split::out_with_row(cut, r);
+        }
     }
 }
 
@@ -994,7 +1000,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     __shared__ Split sp;
     static_assert(NT * BBUF >= kWG * 1024 * 4, "the union's scratch fits the activation tiles");
     const Plan pl = !DOWN && P.plan == nullptr ? union_and_costs<FMT, MXA>(P, sp, reinterpret_cast<int *>(lds))
-                                               : build_costs<FMT, MXA>(P, sp);
+                                               : build_costs<FMT, MXA, DOWN>(P, sp);
     build_bounds(sp, pl.n_groups, (long)P.nbands * nsteps, P.workers);
     // Unit indices fit in 32 bits (fewer than 2^30 units: every matrix is below 2^31 bytes and a
     // launch has at most 4096 token groups), so the unit arithmetic below is 32-bit.
@@ -1219,46 +1225,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // No direct load may still be writing this workgroup's LDS when it ends.
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     write_records();
-    if (DOWN) record_cuts(P, pl, sp, x0, x1);
+    if (DOWN) record_outputs(P, pl, sp, x0, x1);
 }
 
-// Finishes the gate/up items cut between workgroups.  Block w < workers
-// handles the record of workgroup w (an item whose last unit, but not its
-// first, lies in w's range): it adds the parked partial sums of the item's
-// contributors, in workgroup order, and finishes the item.  The blocks past
-// the workers write, for the combine kernel, each routed slot's grouped
-// position and (token group, row in the group), one grouped position per
-// thread.  The kernel boundary makes the expert kernel's records and partial
-// sums visible here.
+// Finishes the gate/up items cut between workgroups.  Block w handles the
+// record of workgroup w (an item whose last unit, but not its first, lies in
+// w's range): it adds the parked partial sums of the item's contributors, in
+// workgroup order, and finishes the item.  The kernel boundary makes the
+// expert kernel's records and partial sums visible here.
 template <bool DOWN, bool MXA>
 __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
 {
     const int lane = lane_id();
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int w = blockIdx.x;
-    if (w >= P.workers) {
-        __shared__ int off_s[1025];
-        const VerifyArgs &a = P.a;
-        const int p = (w - P.workers) * kThreads + (int)threadIdx.x;
-        const int S = a.T * a.k;
-        const int slot = p < S ? a.perm[p] : 0;  // in flight with the offsets
-        const int U = *a.n_unique;
-        for (int u = threadIdx.x; u <= U; u += kThreads) off_s[u] = a.offsets[u];
-        __syncthreads();
-        // Positions past the placed slots (slots whose expert lies outside [0, E) are never placed)
-        // hold no slot of this call.
-        if (p >= off_s[U] || (unsigned)slot >= (unsigned)S) return;
-        int lo = 0, hi = U - 1;  // the union member u with off_s[u] <= p < off_s[u + 1]
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (off_s[mid] <= p) lo = mid; else hi = mid - 1;
-        }
-        const int o0 = off_s[lo];
-        const int g0 = P.plan ? P.plan[8 + 2 * kMaxGroups + lo] : lo;  // first token group of u
-        a.inv[slot] = p;
-        a.gidx[slot] = ((g0 + (p - o0) / kTokGroup) << 6) | ((p - o0) % kTokGroup);
-        return;
-    }
     const long long *rec = P.fix + 4 * (size_t)w;
     const long long item = ld_s64(rec);
     if (item < 0) return;
@@ -1390,72 +1370,82 @@ __global__ __launch_bounds__(256) void plan_kernel(VerifyArgs a, int32_t *plan)
     if (threadIdx.x == 0) plan[0] = run;
 }
 
-// Where expert output O[p][c .. c+3] (row r of a token group, item `item` of
-// the down launch) comes from: the down kernel's O row if the item was whole,
-// else the partial sums of its contributors added in workgroup order (what a
-// fix-up would have stored).  `cut` is the item's record_cuts entry.  Items cut
-// over more than three ranges take expert_out_walk; here they read nothing and
-// give zeros.
-__device__ __forceinline__ f32x4 expert_out(const FfnParams &D, long long cut, int p, int r, int c)
+// Expert output O[c .. c+3] of one row of the down launch, from the row's
+// output descriptor: its row of O if its item was whole, else the partial
+// sums of its contributors added in workgroup order (what a fix-up would have
+// stored).  Rows of items cut over more than three ranges take
+// expert_out_walk; here they read nothing and give zeros.
+__device__ __forceinline__ f32x4 expert_out(const FfnParams &D, uint64_t ds, int c)
 {
-    if (cut >= 0 && !split::packed_contributors(cut)) return f32x4{0.f, 0.f, 0.f, 0.f};
-    // A whole item's O row, or up to three parked partial sums: all loads issued at once
-    // (absent ones read zeros) and added in workgroup order.
-    const int off = r * D.band_rows + c % D.band_rows;  // partial_offset<true>
-    const int cnt = cut < 0 ? 0 : split::packed_count(cut);
+    const int kind = split::out_kind(ds);
+    if (kind >= 2) return f32x4{0.f, 0.f, 0.f, 0.f};
+    // A whole item's O row, or up to three parked partial sums: all loads issued at once (absent
+    // ones read zeros) and added in workgroup order.
+    const int off = split::out_row(ds) * D.band_rows + c % D.band_rows;  // partial_offset<true>
+    const int cnt = kind == 0 ? 0 : split::out_count(ds);
     const rsrc_t ro = make_rsrc(D.a.o, (uint32_t)((size_t)(D.a.T * D.a.k + (D.a.sh_gate ? D.a.T : 0)) * D.a.d * 4));
     const rsrc_t rp = make_rsrc(D.partials, (uint32_t)((size_t)D.workers * 2 * D.slot_floats * 4));
+    const uint32_t sf = (uint32_t)D.slot_floats;
     const f32x4 v0 = __builtin_bit_cast(
-        f32x4, cut < 0 ? load16<0>(ro, (uint32_t)((size_t)p * D.a.d + c) * 4u)
-                       : load16<0>(rp, (uint32_t)(split::packed_slot(cut, 0) * D.slot_floats + off) * 4u));
+        f32x4, kind == 0 ? load16<0>(ro, (uint32_t)((size_t)split::out_pos(ds) * D.a.d + c) * 4u)
+                         : load16<0>(rp, ((uint32_t)split::out_slot(ds, 0) * sf + (uint32_t)off) * 4u));
     const f32x4 v1 = __builtin_bit_cast(
-        f32x4, load16<0>(rp, cnt > 1 ? (uint32_t)(split::packed_slot(cut, 1) * D.slot_floats + off) * 4u : kOff));
+        f32x4, load16<0>(rp, cnt > 1 ? ((uint32_t)split::out_slot(ds, 1) * sf + (uint32_t)off) * 4u : kOff));
     const f32x4 v2 = __builtin_bit_cast(
-        f32x4, load16<0>(rp, cnt > 2 ? (uint32_t)(split::packed_slot(cut, 2) * D.slot_floats + off) * 4u : kOff));
+        f32x4, load16<0>(rp, cnt > 2 ? ((uint32_t)split::out_slot(ds, 2) * sf + (uint32_t)off) * 4u : kOff));
     return cnt > 2 ? v0 + v1 + v2 : cnt > 1 ? v0 + v1 : v0;
 }
 
-// The same for an item cut over more than three ranges: each contributor's slot
-// follows from its range.  Four contributors at a time: their ranges in one
-// round trip, then their sums in one.
-__device__ __forceinline__ f32x4 expert_out_walk(const FfnParams &D, long long cut, long item, int r, int c)
+// The same for a row of an item cut over more than three ranges w0..w1, eight
+// contributors at a time: their partial sums in one round trip (kind 2: slot
+// 2*w0 + tail0, then each later range's head piece), or, if some range in
+// between is empty (kind 3), the ranges first to skip the empty ones.
+__device__ __forceinline__ f32x4 expert_out_walk(const FfnParams &D, uint64_t ds, int c)
 {
-    constexpr int CW = 4;
-    const int off = r * D.band_rows + c % D.band_rows;
+    constexpr int CW = 8;
+    const int off = split::out_row(ds) * D.band_rows + c % D.band_rows;
+    const int w0 = split::out_w0(ds), w1 = split::out_w1(ds);
+    const bool check = split::out_kind(ds) == 3;
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-    const long ib = item * D.nsteps, ie = ib + D.nsteps;
-    const int w1 = split::last_worker(cut);
-    for (int v0 = split::first_worker(cut); v0 <= w1; v0 += CW) {
-        long long rg[CW][2];
+    for (int v0 = w0; v0 <= w1; v0 += CW) {
+        bool live[CW];
 #pragma unroll
-        for (int q = 0; q < CW; ++q) {
-            const int v = min(v0 + q, w1);
-            rg[q][0] = D.ranges[2 * v];
-            rg[q][1] = D.ranges[2 * v + 1];
+        for (int q = 0; q < CW; ++q) live[q] = v0 + q <= w1;
+        if (check) {
+            long long rg[CW][2];
+#pragma unroll
+            for (int q = 0; q < CW; ++q) {
+                const int v = min(v0 + q, w1);
+                rg[q][0] = D.ranges[2 * v];
+                rg[q][1] = D.ranges[2 * v + 1];
+            }
+#pragma unroll
+            for (int q = 0; q < CW; ++q) live[q] = live[q] && rg[q][0] < rg[q][1];
         }
-        int slot[CW];
         f32x4 pv[CW];
 #pragma unroll
         for (int q = 0; q < CW; ++q) {
-            slot[q] = v0 + q <= w1 ? split::piece_slot(v0 + q, (long)rg[q][0], (long)rg[q][1], ib, ie) : -1;
-            pv[q] = slot[q] >= 0 ? *reinterpret_cast<const f32x4 *>(D.partials + (size_t)slot[q] * D.slot_floats + off)
-                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+            const int v = v0 + q;
+            const int slot = v == w0 ? 2 * w0 + split::out_tail0(ds) : 2 * v;
+            pv[q] = live[q] ? *reinterpret_cast<const f32x4 *>(D.partials + (size_t)slot * D.slot_floats + off)
+                            : f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
         for (int q = 0; q < CW; ++q)
-            if (slot[q] >= 0) s += pv[q];
+            if (live[q]) s += pv[q];
     }
     return s;
 }
 
 // y[t] = sum_j w[t][j] * (O[slot t*k + j] + b_down[expert of the slot]) (+ shared) -> bf16, summed in the
 // order j = 0..k-1, then the shared expert; 4 columns per thread.  D is the
-// down launch's geometry.  The k slots are handled 8 at a time, each stage's
-// loads issued together; the shared expert's chain (its item, cut entry and
-// output) goes with the first stage's, so the kernel waits on global memory
-// three times whatever the slots.  Items cut over more than three ranges
-// (small batches spread thin over the workgroups) are walked afterwards, one
-// at a time, so that the common path stays short.
+// down launch's geometry.  The k slots are handled 8 at a time: each stage
+// loads its slots' experts, gate weights and output descriptors together, the
+// shared expert's descriptor going with the first stage's, then every output
+// row the descriptors name, so the kernel waits on global memory twice per
+// stage.  Rows of items cut over more than three ranges (small batches spread
+// thin over the workgroups) are walked afterwards, one at a time, so that the
+// common path stays short.
 __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
 {
     constexpr int CH = 8;
@@ -1465,66 +1455,51 @@ __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
     if (i >= a.T * per_row) return;
     const int t = i / per_row, c = (i - t * per_row) * 4;
     const int band = c / D.band_rows;
-    // The shared expert's token groups are the last ceil(T / 64).
+    const int S = a.T * a.k;
     const bool sh = a.sh_gate != nullptr;
-    const int n_groups = sh ? (D.plan ? D.plan[0] : *a.n_unique + 1) : 0;
-    const long sitem = (long)(n_groups - (a.T + kTokGroup - 1) / kTokGroup + t / kTokGroup) * D.nbands + band;
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f}, vsh = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int j0 = 0; j0 < a.k; j0 += CH) {
         const bool with_sh = sh && j0 == 0;
-        int pj[CH], gj[CH];
+        int ej[CH];
         float wj[CH];
-        long long cj[CH];
-        f32x4 vj[CH], bj[CH];
+        uint64_t dj[CH];
+        f32x4 vj[CH];
         bool ok[CH];
 #pragma unroll
         for (int q = 0; q < CH; ++q) {
             const int slot = t * a.k + min(j0 + q, a.k - 1);
-            // A slot whose expert lies outside [0, E) was never placed: it adds nothing and its
-            // (unwritten) map entries are not read.
-            // (All four loads are issued together; only the map entries' use waits on the expert.)
-            const int e = a.topk_idx[slot];
-            const int pv = a.inv[slot], gv = a.gidx[slot];
+            ej[q] = a.topk_idx[slot];
             wj[q] = a.topk_w[slot];
-            ok[q] = j0 + q < a.k && (unsigned)e < (unsigned)a.E;
-            pj[q] = ok[q] ? pv : 0;
-            gj[q] = ok[q] ? gv : 0;
-            bj[q] = a.b_down && ok[q] ? *reinterpret_cast<const f32x4 *>(a.b_down + (size_t)e * a.d + c)
-                                      : f32x4{0.f, 0.f, 0.f, 0.f};
+            dj[q] = a.desc[(size_t)slot * D.nbands + band];
         }
-#pragma unroll
-        for (int q = 0; q < CH; ++q) cj[q] = ok[q] ? D.cut[(long)(gj[q] >> 6) * D.nbands + band] : -1;
-        const long long csh = with_sh ? D.cut[sitem] : -1;
-        // vj[q] = O + b_down of slot q.  A slot whose item needs the walk holds b_down for now
-        // (its walk sum w is added as w + b below, the same operation as O + b).
-        uint32_t walk = 0;  // bit q: slot q's item needs the walk; bit CH: the shared expert's
-        int wcode[CH];      // first and last contributor of such an item (w0 << 16 | w1)
+        const uint64_t dsh = with_sh ? a.desc[(size_t)(S + t) * D.nbands + band] : 0ull;
+        // vj[q] = O + b_down of slot q.  A slot whose expert lies outside [0, E) was never placed:
+        // it adds nothing and its (unwritten) descriptor is not used.  A slot whose item needs the
+        // walk holds b_down for now (its walk sum w is added as w + b below, the same operation as O + b).
+        uint32_t walk = 0;  // bit q: slot q's row needs the walk; bit CH: the shared expert's
 #pragma unroll
         for (int q = 0; q < CH; ++q) {
-            const bool wk = cj[q] >= 0 && !split::packed_contributors(cj[q]);
-            const f32x4 v = expert_out(D, cj[q], pj[q], gj[q] & 63, c);
-            vj[q] = a.b_down ? (wk ? bj[q] : v + bj[q]) : v;
-            wcode[q] = (int)cj[q];
+            ok[q] = j0 + q < a.k && (unsigned)ej[q] < (unsigned)a.E;
+            const uint64_t dq = ok[q] ? dj[q] : split::out_whole(0u);
+            const f32x4 b = a.b_down && ok[q] ? *reinterpret_cast<const f32x4 *>(a.b_down + (size_t)ej[q] * a.d + c)
+                                              : f32x4{0.f, 0.f, 0.f, 0.f};
+            const f32x4 v = expert_out(D, dq, c);
+            const bool wk = split::out_kind(dq) >= 2;
+            vj[q] = a.b_down ? (wk ? b : v + b) : v;
             if (wk) walk |= 1u << q;
         }
         if (with_sh) {
-            vsh = expert_out(D, csh, a.T * a.k + t, t % kTokGroup, c);
-            if (csh >= 0 && !split::packed_contributors(csh)) walk |= 1u << CH;
+            vsh = expert_out(D, dsh, c);
+            if (split::out_kind(dsh) >= 2) walk |= 1u << CH;
         }
         while (walk) {
             const int q = __builtin_ctz(walk);
             walk &= walk - 1;
-            long long cq = csh;
-            long iq = sitem;
-            int rq = t % kTokGroup;
+            uint64_t dq = dsh;
 #pragma unroll
             for (int qq = 0; qq < CH; ++qq)
-                if (qq == q) {
-                    cq = wcode[qq];
-                    iq = (long)(gj[qq] >> 6) * D.nbands + band;
-                    rq = gj[qq] & 63;
-                }
-            const f32x4 v = expert_out_walk(D, cq, iq, rq, c);
+                if (qq == q) dq = dj[qq];
+            const f32x4 v = expert_out_walk(D, dq, c);
 #pragma unroll
             for (int qq = 0; qq < CH; ++qq)
                 if (qq == q) vj[qq] = a.b_down ? v + vj[qq] : v;
@@ -1586,13 +1561,11 @@ VerifyWorkspace verify_workspace(int d, int d_ff, int T, int k, bool shared, boo
     w.plan_cap = plan_capacity(T, k, shared);
     w.plan_offset = w.p_offset + align(w.p_bytes);
     w.plan_bytes = (8 + 2 * (size_t)kMaxGroups + 1026) * 4;  // groups, then first group per expert
-    w.map_offset = w.plan_offset + align(w.plan_bytes);
-    w.map_bytes = (size_t)T * k * 4 * 2;  // grouped position, (group, row) per routed slot
-    w.cut_offset = w.map_offset + align(w.map_bytes);
-    w.cut_bytes = (size_t)w.plan_cap * ((d + 32 * kWG - 1) / (32 * kWG)) * 8;
+    w.desc_offset = w.plan_offset + align(w.plan_bytes);
+    w.desc_bytes = rows * ((d + 32 * kWG - 1) / (32 * kWG)) * 8;  // one output descriptor per row and down band
     // MX activations: x codes + scales, then H codes + scales (rows padded to multiples of 128).
     const size_t kpd = (size_t)(d + kMacroK - 1) / kMacroK * kMacroK, kpf = (size_t)(d_ff + kMacroK - 1) / kMacroK * kMacroK;
-    w.mx_offset = w.cut_offset + align(w.cut_bytes);
+    w.mx_offset = w.desc_offset + align(w.desc_bytes);
     w.mx_bytes = mx ? align((size_t)T * kpd) + align((size_t)T * kpd / 32) + align(rows * kpf) + align(rows * kpf / 32) : 0;
     w.total = w.mx_offset + align(w.mx_bytes);
     return w;
@@ -1613,8 +1586,7 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     VerifyArgs a = args;
     a.h = reinterpret_cast<uint16_t *>(ws_base + ws.h_offset);
     a.o = reinterpret_cast<float *>(ws_base + ws.o_offset);
-    a.inv = reinterpret_cast<int32_t *>(ws_base + ws.map_offset);
-    a.gidx = a.inv + (size_t)a.T * a.k;
+    a.desc = reinterpret_cast<uint64_t *>(ws_base + ws.desc_offset);
     float *partials = reinterpret_cast<float *>(ws_base + ws.p_offset);
     int32_t *plan = reinterpret_cast<int32_t *>(ws_base + ws.plan_offset);
     hipError_t err;
@@ -1657,13 +1629,11 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     g.slot_floats = ws.slot_floats;
     g.ranges = reinterpret_cast<long long *>(partials + (size_t)G * 2 * ws.slot_floats);
     g.fix = g.ranges + (size_t)G * 2;
-    g.cut = reinterpret_cast<long long *>(ws_base + ws.cut_offset);
     g.plan = grouped ? plan : nullptr;
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD, MXA>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = mark(events, 1, stream)) != hipSuccess) return err;
-    const int map_blocks = (a.T * a.k + kThreads - 1) / kThreads;
-    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false, MXA>), dim3(G + map_blocks), dim3(kThreads), 0, stream, g);
+    hipLaunchKernelGGL((expert_ffn_fixup_kernel<false, MXA>), dim3(G), dim3(kThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     FfnParams dn = g;

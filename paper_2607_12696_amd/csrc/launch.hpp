@@ -46,8 +46,10 @@ struct VerifyArgs {
     uint16_t *y;        // [T][d] bf16
     uint16_t *h;        // workspace: [T*k (+T)][d_ff] bf16 SwiGLU rows at grouped positions
     float *o;           // workspace: [T*k (+T)][d] fp32 expert outputs at grouped positions (shared: T*k + t)
-    int32_t *inv;       // workspace: [T*k] grouped position of each routed slot
-    int32_t *gidx;      // workspace: [T*k] (token group << 6 | row in the group) of each routed slot
+    // workspace: [T*k + T][bands of the down launch] where the combine kernel reads each row of the down
+    // launch's output (routed slot s at row s, the shared expert's row of token t at T*k + t): an output
+    // descriptor of split.hpp, written by the down launch.
+    uint64_t *desc;
     // MX activation mode (act_fmt 1, MXFP4 weights only): x and the SwiGLU rows
     // are the projections' inputs as OCP MX FP8 (one e8m0 code per 32
     // consecutive elements), rows padded to the next multiple of 128 elements
@@ -66,10 +68,10 @@ constexpr int kTimingMarks = 5;  // events recorded by the timed entry point
 // Workspace layout shared by the size query and the launcher: H (bf16 SwiGLU
 // rows) and O (fp32 expert outputs), both at grouped positions; partial sums
 // and unit ranges of work items cut between workgroups; the token-group plan;
-// per-slot maps for the combine kernel; the cut-item table of the down launch.
+// the down launch's output descriptors for the combine kernel.
 struct VerifyWorkspace {
-    size_t h_offset, h_bytes, o_offset, o_bytes, p_offset, p_bytes, plan_offset, plan_bytes, map_offset, map_bytes,
-        cut_offset, cut_bytes, mx_offset, mx_bytes;
+    size_t h_offset, h_bytes, o_offset, o_bytes, p_offset, p_bytes, plan_offset, plan_bytes, desc_offset, desc_bytes,
+        mx_offset, mx_bytes;
     int plan_cap;
     int workers;      // workgroups of the expert kernels' grid (one per compute unit)
     int slot_floats;  // floats per partial-sum slot (two slots per workgroup)

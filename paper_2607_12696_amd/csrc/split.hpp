@@ -96,6 +96,56 @@ constexpr long finished_item(long x0, long x1, long ns)
     return (ib < x0 && ie <= x1) ? item : -1;
 }
 
+// Where the combine kernel reads one row of a down item (an 8-byte output
+// descriptor, written by the range that holds the item's last unit):
+//   kind 0, whole item: bits 0-31 the row's grouped position p (its row of O);
+//   kind 1, cut over two or three ranges: their slots (10 bits each, bits 0-29,
+//     in workgroup order), their count (bits 30-31) and the row r of the group
+//     (bits 32-37), the row's place in each slot;
+//   kind 2, cut over more than three ranges, none of them empty: the first and
+//     last workgroup w0, w1 (bits 0-9, 10-19), bit 20 set if w0's piece is its
+//     tail piece (slot 2*w0 + 1, else 2*w0), and r; every later range v adds its
+//     head piece, slot 2*v;
+//   kind 3: as kind 2, but some range between w0 and w1 is empty, so the
+//     reader asks piece_slot() for each of them.
+// Workgroups are fewer than 1024 (10 bits).
+constexpr uint64_t kOutKindShift = 62;
+
+constexpr uint64_t out_whole(uint32_t p) { return (uint64_t)p; }
+
+// Descriptor of the rows of the cut item [ib, ie) without its row field.
+constexpr uint64_t out_cut(const int *cw, const long long *bound, int n_groups, long K, int W, long ib, long ie)
+{
+    const int w0 = owner_of(cw, n_groups, K, W, ib);
+    const int w1 = owner_of(cw, n_groups, K, W, ie - 1);
+    uint64_t packed = 0;
+    int cnt = 0;
+    bool empty = false;
+    for (int v = w0; v <= w1; ++v) {
+        const int s = piece_slot(v, (long)bound[v], (long)bound[v + 1], ib, ie);
+        if (s < 0) {
+            empty = true;
+            continue;
+        }
+        if (cnt < 3) packed |= (uint64_t)s << (10 * cnt);
+        ++cnt;
+    }
+    if (cnt <= 3) return (1ull << kOutKindShift) | ((uint64_t)cnt << 30) | packed;
+    const bool tail0 = bound[w0] < ib;  // w0's range starts before the item: its tail piece
+    return ((empty ? 3ull : 2ull) << kOutKindShift) | ((uint64_t)w1 << 10) | (uint64_t)w0 |
+           ((uint64_t)(tail0 ? 1 : 0) << 20);
+}
+
+constexpr uint64_t out_with_row(uint64_t code, int r) { return code | ((uint64_t)r << 32); }
+constexpr int out_kind(uint64_t code) { return (int)(code >> kOutKindShift); }
+constexpr uint32_t out_pos(uint64_t code) { return (uint32_t)code; }
+constexpr int out_row(uint64_t code) { return (int)(code >> 32) & 63; }
+constexpr int out_count(uint64_t code) { return (int)(code >> 30) & 3; }
+constexpr int out_slot(uint64_t code, int i) { return (int)(code >> (10 * i)) & 1023; }
+constexpr int out_w0(uint64_t code) { return (int)code & 1023; }
+constexpr int out_w1(uint64_t code) { return (int)(code >> 10) & 1023; }
+constexpr int out_tail0(uint64_t code) { return (int)(code >> 20) & 1; }
+
 constexpr bool packed_contributors(long long code) { return (code >> 62) != 0; }
 constexpr int packed_count(long long code) { return (int)((code >> 60) & 3); }
 constexpr int packed_slot(long long code, int i) { return (int)((code >> (20 * i)) & 0xfffff); }

@@ -14,7 +14,11 @@ of the split:
   * the contributors of an item are the ranges that hold its units, in
     workgroup order; up to three are packed, past three the first and last
     workgroup are stored and the finisher walks the ranges between;
-  * each cut item has exactly one finisher, the range that holds its last unit.
+  * each cut item has exactly one finisher, the range that holds its last unit;
+  * the down launch's output descriptor of a cut item's rows names the same
+    slots: packed up to three, else the first and last workgroup and whether
+    the first one's piece is its tail piece, every later non-empty range
+    adding its head piece (and a flag that some range between is empty).
 
 Cases span W in {256, 512} (one or two workgroups per compute unit) and small
 grids, group costs of the kernels' form (A + 3 * token blocks) and arbitrary,
@@ -50,7 +54,36 @@ def lib(tmp_path_factory):
     L.split_finished_item.restype = l
     L.split_div_floor.argtypes = [ll, ll]
     L.split_div_floor.restype = ll
+    u = C.c_ulonglong
+    L.split_out_cut.argtypes = [p, p, i, l, i, l, l]
+    L.split_out_cut.restype = u
+    L.split_out_whole.argtypes = [C.c_uint]
+    L.split_out_whole.restype = u
+    L.split_out_with_row.argtypes = [u, i]
+    L.split_out_with_row.restype = u
+    L.split_out_fields.argtypes = [u, p]
+    L.split_out_fields.restype = None
     return L
+
+
+def out_fields(lib, code):
+    f = np.zeros(10, np.int32)
+    lib.split_out_fields(code, f.ctypes.data)
+    return dict(zip(("kind", "pos", "row", "count", "s0", "s1", "s2", "w0", "w1", "tail0"), f.tolist()))
+
+
+def out_slots(lib, code, bound):
+    """The partial-sum slots a reader of the output descriptor adds, in order (what the combine kernel
+    does: kind 3 consults the ranges, the others do not)."""
+    f = out_fields(lib, code)
+    if f["kind"] == 1:
+        return [f["s0"], f["s1"], f["s2"]][:f["count"]]
+    assert f["kind"] in (2, 3), f
+    slots = [2 * f["w0"] + f["tail0"]]
+    for v in range(f["w0"] + 1, f["w1"] + 1):
+        if f["kind"] == 2 or bound[v] < bound[v + 1]:
+            slots.append(2 * v)
+    return slots
 
 
 def brute_owner(costs, K, W):
@@ -124,6 +157,15 @@ def run_case(lib, costs, nbands, nsteps, W):
                 if s >= 0:
                     got.append(s)
         assert got == want, (item, got, want)
+        # The down launch's output descriptor of the item's rows names the same slots, for every row.
+        desc = lib.split_out_cut(cwp, bptr, n, K, W, ib, ie)
+        assert out_slots(lib, desc, bound) == want, (item, hex(desc), want)
+        w0, w1 = int(owner[ib]), int(owner[ie - 1])
+        empty = any(bound[v] >= bound[v + 1] for v in range(w0, w1 + 1))
+        assert out_fields(lib, desc)["kind"] == (1 if len(want) <= 3 else 3 if empty else 2)
+        for r in (0, 1, 37, 63):
+            f = out_fields(lib, lib.split_out_with_row(desc, r))
+            assert f["row"] == r and out_slots(lib, lib.split_out_with_row(desc, r), bound) == want
     # Items nobody parked are whole in exactly one range, and no cut item lacks a finisher.
     assert set(finisher) == set(parked)
     return wide
@@ -179,6 +221,32 @@ def test_random_costs_and_grids(lib):
         W = int(rng.choice([1, 2, 3, 7, 64, 256, 512]))
         wide += run_case(lib, costs, nbands, nsteps, W)
     assert wide > 0
+
+
+def test_whole_item_descriptor(lib):
+    # A whole item's row: kind 0 and its grouped position, for positions up to the largest a call has.
+    for p in (0, 1, 4095, 2**24 + 2**18, 2**25 - 1):
+        f = out_fields(lib, lib.split_out_whole(p))
+        assert f["kind"] == 0 and f["pos"] == p
+
+
+def test_descriptor_walk_with_empty_ranges(lib):
+    # More workgroups than units: ranges between an item's first and last contributor are empty, and the
+    # descriptor must say so (kind 3) for the reader to skip them.
+    kinds = set()
+    for W in (64, 256, 512):
+        for costs, nb, ns in (([200, 1, 1], 1, 3), ([5], 2, 3), ([1, 90], 1, 7)):
+            run_case(lib, costs, nb, ns, W)
+            K = nb * ns
+            cw = np.concatenate([[0], np.cumsum(costs)]).astype(np.int32)
+            owner = brute_owner(costs, K, W)
+            bound = np.searchsorted(owner, np.arange(W + 1), side="left").astype(np.int64)
+            for item in range(len(costs) * nb):
+                ib, ie = item * ns, (item + 1) * ns
+                if owner[ib] != owner[ie - 1]:
+                    kinds.add(out_fields(lib, lib.split_out_cut(cw.ctypes.data, bound.ctypes.data, len(costs), K, W,
+                                                                ib, ie))["kind"])
+    assert 3 in kinds
 
 
 def test_div_floor_is_exact(lib):
