@@ -272,7 +272,7 @@ __device__ __forceinline__ Plan load_plan(const FfnParams &P)
 #define ECOSPEC_COST_BF16 29
 #endif
 #ifndef ECOSPEC_COST_FP8
-#define ECOSPEC_COST_FP8 13
+#define ECOSPEC_COST_FP8 12
 #endif
 #ifndef ECOSPEC_COST_FP4
 #define ECOSPEC_COST_FP4 8
@@ -281,7 +281,7 @@ __device__ __forceinline__ Plan load_plan(const FfnParams &P)
 #define ECOSPEC_COST_FP4_MX 16
 #endif
 #ifndef ECOSPEC_COST_BLOCK
-#define ECOSPEC_COST_BLOCK 3  // per 16-token block
+#define ECOSPEC_COST_BLOCK 2  // per 16-token block
 #endif
 template <int FMT, bool MXA>
 __device__ __forceinline__ int group_cost(int M)

@@ -21,7 +21,7 @@ of the split:
     adding its head piece (and a flag that some range between is empty).
 
 Cases span W in {256, 512} (one or two workgroups per compute unit) and small
-grids, group costs of the kernels' form (A + 3 * token blocks) and arbitrary,
+grids, group costs of the kernels' form (A + 2 * token blocks) and arbitrary,
 and shapes where one item is spread over many workgroups (the > 3 encoding).
 """
 import ctypes as C
@@ -171,11 +171,11 @@ def run_case(lib, costs, nbands, nsteps, W):
     return wide
 
 
-KERNEL_COST = {"bf16": 29, "fp8": 13, "fp4": 8, "fp4_mx": 16}
+KERNEL_COST = {"bf16": 29, "fp8": 12, "fp4": 8, "fp4_mx": 16}
 
 
 def kernel_costs(fmt, Ms):
-    return [KERNEL_COST[fmt] + 3 * ((m + 15) // 16) for m in Ms]
+    return [KERNEL_COST[fmt] + 2 * ((m + 15) // 16) for m in Ms]
 
 
 # (fmt, tokens per group, nbands, nsteps): the launches of the full shapes and of a small shape that spreads
