@@ -19,6 +19,7 @@ Prints ONE JSON line on stdout; progress goes to stderr.
     python bench.py --profile [--shape ds|gpt]       # short run for rocprofv3 (+ a copy kernel for counter calibration)
     python bench.py --summarize-kstats DIR OUT [--shape ds|gpt]  # rocprofv3 --kernel-trace --stats output -> profiles/ summary
     python bench.py --summarize-pmc FETCH WRITE OUT [--shape ds|gpt]  # rocprofv3 --pmc output -> profiles/ summary
+    python bench.py --summarize-sq SQ_A SQ_B OUT [--shape ds|gpt]     # two SQ counter passes -> profiles/ summary
 """
 from __future__ import annotations
 
@@ -705,6 +706,73 @@ def summarize_pmc(fetch_dir, write_dir, out_path, shape):
     print(open(out_path).read())
 
 
+SQ_PASSES = {
+    "A": "SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY SQ_ACTIVE_INST_VALU "
+         "SQ_VALU_MFMA_BUSY_CYCLES SQ_ACTIVE_INST_LDS",
+    "B": "SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_SALU SQ_INSTS_LDS SQ_INSTS_VMEM_RD SQ_WAIT_INST_LDS SQ_INSTS_VALU_CVT "
+         "SQ_ACTIVE_INST_VMEM",
+}
+SQ_SUMMARY = {"ds": "profiles/expert_ffn_ds_fp8_T64_U32.sq.txt", "gpt": "profiles/expert_ffn_gpt_mxfp4_T64_U32.sq.txt"}
+
+
+def summarize_sq(dir_a, dir_b, out_path, shape, last=50):
+    """Shader-sequencer counters of the two expert kernels of a `bench.py --profile` run (two counter passes),
+    per dispatch over the last `last` dispatches, with the derived fractions of wavefront time: issuing any
+    instruction, issuing VALU, waiting for an instruction's inputs (SQ_WAIT_INST_ANY), waiting for anything.
+    Cycle counters count quad-cycles per wavefront; instruction counts are per wavefront and step (a step is
+    one 128-wide block, two for MXFP4, of one item on each of the workgroup's wavefronts)."""
+    import synth
+    sh = synth.SHAPES[shape]
+    T, U, waves_per_wg = 64, 32, 8
+    rows = {}
+    for d in (dir_a, dir_b):
+        for p in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(p) as f:
+                for r in csv.DictReader(f):
+                    n = r["Kernel_Name"]
+                    if "expert_ffn_kernel" not in n:
+                        continue
+                    down = ", true" in n or "ELb1E" in n
+                    per = rows.setdefault((down, r["Counter_Name"]), {})
+                    disp = int(r.get("Dispatch_Id", 0) or 0)
+                    per[disp] = per.get(disp, 0.0) + float(r["Counter_Value"])
+    n_exp = U + (1 if sh.shared else 0)
+    with open(out_path, "w") as f:
+        name = {"ds": "DeepSeek-V3.1-shaped FP8", "gpt": "GPT-OSS-120B-shaped MXFP4"}[shape]
+        f.write(f"# rocprofv3 shader-sequencer counters: expert kernels, {name} layer, T=64, exact-U routing, U=32\n")
+        f.write("# commands (repository root, TMPDIR=/tmp):\n")
+        for tag, cs in SQ_PASSES.items():
+            f.write(f"#   rocprofv3 --pmc {cs} -d SQ_{tag} --output-format csv -- python3 bench.py --profile --shape {shape}\n")
+        f.write(f"#   python3 bench.py --summarize-sq SQ_A SQ_B {SQ_SUMMARY[shape]} --shape {shape}\n")
+        f.write(f"# per dispatch, mean over the last {last} dispatches of each kernel\n")
+        f.write(f"kernel_source_sha: {source_sha()}\n")
+        for down in (False, True):
+            k = "down" if down else "gateup"
+            blocks = -(-(sh.d_ff if down else sh.d) // 128)
+            steps = -(-blocks // (2 if sh.fmt == 2 else 1))
+            bands = -(-(sh.d if down else sh.d_ff) // (256 if down else 128))
+            wave_steps = n_exp * bands * steps * waves_per_wg
+            c = {}
+            for (dn, name_), per in rows.items():
+                if dn == down:
+                    ds_ = sorted(per)[-last:]
+                    c[name_] = sum(per[i] for i in ds_) / max(1, len(ds_))
+            for name_ in sorted(c):
+                f.write(f"{k}_{name_}: {c[name_]:.0f}\n")
+            wc = c.get("SQ_WAVE_CYCLES")
+            if wc:
+                for cn in ("SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU", "SQ_WAIT_INST_ANY", "SQ_WAIT_ANY",
+                           "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_VMEM"):
+                    if cn in c:
+                        f.write(f"{k}_frac_of_wave_time_{cn[3:].lower()}: {c[cn] / wc:.3f}\n")
+            f.write(f"{k}_wave_steps: {wave_steps}\n")
+            for cn in ("SQ_INSTS_VALU", "SQ_INSTS_VALU_CVT", "SQ_INSTS_MFMA", "SQ_INSTS_SALU", "SQ_INSTS_LDS",
+                       "SQ_INSTS_VMEM_RD"):
+                if cn in c:
+                    f.write(f"{k}_{cn[9:].lower() or 'valu'}_per_wave_step: {c[cn] / wave_steps:.1f}\n")
+    print(open(out_path).read())
+
+
 def pmc_traffic(shape, kernel="gateup"):
     kv = read_summary(PMC_SUMMARY[shape])
     if not kv:
@@ -736,6 +804,7 @@ def main():
     ap.add_argument("--shape", default="ds", choices=["ds", "gpt"], help="layer of --profile / --summarize-pmc")
     ap.add_argument("--summarize-kstats", nargs=2, metavar=("KT_DIR", "OUT"))
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"))
+    ap.add_argument("--summarize-sq", nargs=3, metavar=("SQ_A", "SQ_B", "OUT"))
     args = ap.parse_args()
 
     if args.summarize_kstats:
@@ -743,6 +812,9 @@ def main():
         return 0
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.shape)
+        return 0
+    if args.summarize_sq:
+        summarize_sq(*args.summarize_sq, args.shape)
         return 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
