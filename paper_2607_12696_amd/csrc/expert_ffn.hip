@@ -817,12 +817,15 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
 #pragma unroll
     for (int mb = 0; mb < NMB; ++mb)
         b[0][mb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * 256 + boff(0)));
-    // FP8 accumulates the step in `part` and adds scale * part at the end.
+    // FP8 accumulates the step in `part` and adds scale * part at the end; the other formats
+    // accumulate in place.
     f32x4 part[2][NMB];
+    if constexpr (FMT == FMT_FP8) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb) part[t][mb] = FMT == FMT_FP8 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[t][mb];
+            for (int mb = 0; mb < NMB; ++mb) part[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         if (s < NS - 1) {
@@ -834,18 +837,17 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
         const bf16x8 av0 = decode_a<FMT>(wv[0], s), av1 = decode_a<FMT>(wv[1], s);
 #pragma unroll
         for (int mb = 0; mb < NMB; ++mb) {
-            part[0][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av0, b[s & 1][mb], part[0][mb], 0, 0, 0);
-            part[1][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av1, b[s & 1][mb], part[1][mb], 0, 0, 0);
+            f32x4 &c0 = FMT == FMT_FP8 ? part[0][mb] : acc[0][mb];
+            f32x4 &c1 = FMT == FMT_FP8 ? part[1][mb] : acc[1][mb];
+            c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av0, b[s & 1][mb], c0, 0, 0, 0);
+            c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av1, b[s & 1][mb], c1, 0, 0, 0);
         }
     }
+    if constexpr (FMT == FMT_FP8) {
 #pragma unroll
-    for (int mb = 0; mb < NMB; ++mb) {
-        if constexpr (FMT == FMT_FP8) {
+        for (int mb = 0; mb < NMB; ++mb) {
             acc[0][mb] += wv[0].scale * part[0][mb];
             acc[1][mb] += wv[1].scale * part[1][mb];
-        } else {
-            acc[0][mb] = part[0][mb];
-            acc[1][mb] = part[1][mb];
         }
     }
 }
@@ -1090,9 +1092,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             const bool sok = ok && bc < 2 && (int)(step * SB + (bc & 1)) < P.nblocks;
 #pragma unroll
             for (int i = 0; i < kBPass; ++i) {
-                bst[slot][i][0] = load16<0>(rb, (aok && src.boff[i] != kOff) ? src.boff[i] + step * 256u : kOff);
-                sst[slot][i] = __builtin_amdgcn_raw_buffer_load_b32(
-                    rsa, (int)((sok && src.soff[i] != kOff) ? src.soff[i] + step * 8u : kOff), 0, 0);
+                // A row's kOff plus the in-range step offset stays beyond the buffer: zeros.
+                bst[slot][i][0] = load16<0>(rb, aok ? src.boff[i] + step * 256u : kOff);
+                sst[slot][i] = __builtin_amdgcn_raw_buffer_load_b32(rsa, (int)(sok ? src.soff[i] + step * 8u : kOff), 0, 0);
             }
         }
     };
@@ -1110,8 +1112,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
                 const uint32_t kb = step * SB + b;
                 const bool kok = ok && (SB == 1 || (int)kb < P.nblocks) && (int)kb * kMacroK + src.kc < K;
 #pragma unroll
-                for (int p = 0; p < kBPass; ++p)
-                    load16_lds(rbw, (kok && src.boff[p] != kOff) ? src.boff[p] + kb * 256u : kOff,
+                for (int p = 0; p < kBPass; ++p)  // a row's kOff plus kb * 256 stays beyond the buffer: zeros
+                    load16_lds(rbw, kok ? src.boff[p] + kb * 256u : kOff,
                                tile + (uint32_t)(b * BTile<SB>::kBlk + p * kBRowsPerPass * 256));
             }
         }
