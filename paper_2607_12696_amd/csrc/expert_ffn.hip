@@ -76,8 +76,8 @@
 #ifndef ECOSPEC_PD_FP4
 #define ECOSPEC_PD_FP4 2
 #endif
-#ifndef ECOSPEC_WG_WAVES
-#define ECOSPEC_WG_WAVES 8
+#ifndef ECOSPEC_PHYS_WAVES
+#define ECOSPEC_PHYS_WAVES 8  // wavefronts of an expert workgroup (8: two per SIMD; 4: one per SIMD, measured slower)
 #endif
 #ifndef ECOSPEC_WG_PER_CU
 #define ECOSPEC_WG_PER_CU 1
@@ -90,10 +90,20 @@ enum { FMT_BF16 = 0, FMT_FP8 = 1, FMT_MXFP4 = 2 };
 constexpr int kMacroK = 128;            // reduction elements per macro step
 constexpr int kMB = 4;                  // 16-token blocks per item
 constexpr int kTokGroup = 16 * kMB;     // tokens per item
-constexpr int kWG = ECOSPEC_WG_WAVES;   // wavefronts per workgroup
-constexpr int kThreads = kWG * kWave;
-constexpr int kBRowsPerPass = kThreads / 16;         // activation rows staged per pass (16 threads per row)
+// An item's rows are cut into kWG slots: 16 rows (gate/up, with the same
+// rows of the up matrix) or 32 rows (down) each.  Slots are the unit of the
+// partial-sum layout and of the fix-up kernel (one wavefront per slot); an
+// expert workgroup has kPW wavefronts of kVPW slots each, i.e. kNT weight
+// tiles of 16 rows per wavefront.
+constexpr int kWG = 8;                               // slots per item
+constexpr int kPW = ECOSPEC_PHYS_WAVES;              // wavefronts of an expert workgroup
+constexpr int kVPW = kWG / kPW;                      // slots per wavefront
+constexpr int kNT = 2 * kVPW;                        // 16-row weight tiles per wavefront
+constexpr int kThreads = kWG * kWave;                // fix-up kernel
+constexpr int kEThreads = kPW * kWave;               // expert kernels
+constexpr int kBRowsPerPass = kEThreads / 16;        // activation rows staged per pass (16 threads per row)
 constexpr int kBPass = kTokGroup / kBRowsPerPass;    // passes per step
+static_assert(kWG % kPW == 0, "whole slots per wavefront");
 constexpr int kAuxNT = 2;               // nontemporal: streamed weights should not displace activations
 // Floats of one partial-sum slot: a workgroup's accumulators of the live token
 // blocks (a token group holds at most min(T, 64) tokens).
@@ -317,14 +327,14 @@ struct Split {
 template <int FMT, bool MXA, bool DOWN>
 __device__ __forceinline__ Plan build_costs(const FfnParams &P, Split &sp)
 {
-    constexpr int kPre = 2;  // groups per thread read ahead (E <= kPre * kThreads covers every union)
+    constexpr int kPre = (1024 + kEThreads - 1) / kEThreads;  // groups per thread read ahead (E <= 1024: every union)
     const VerifyArgs &a = P.a;
     const int S = a.T * a.k;
     const int tid = threadIdx.x;
     int o0[kPre], o1[kPre], id[kPre];
 #pragma unroll
     for (int j = 0; j < kPre; ++j) {
-        const int g = j * kThreads + tid;
+        const int g = j * kEThreads + tid;
         const bool ok = P.plan == nullptr && g < a.E;
         o0[j] = ok ? a.offsets[g] : 0;
         o1[j] = ok ? a.offsets[g + 1] : 0;
@@ -332,9 +342,9 @@ __device__ __forceinline__ Plan build_costs(const FfnParams &P, Split &sp)
     }
     const Plan pl = load_plan(P);
     if (S <= kMaxTokLds)
-        for (int p = tid; p < S; p += kThreads) sp.tok[p] = DOWN ? a.perm[p] : a.perm[p] / a.k;
+        for (int p = tid; p < S; p += kEThreads) sp.tok[p] = DOWN ? a.perm[p] : a.perm[p] / a.k;
     int run = 0;
-    for (int base = 0, j = 0; base < pl.n_groups; base += kThreads, ++j) {
+    for (int base = 0, j = 0; base < pl.n_groups; base += kEThreads, ++j) {
         const int g = base + tid;
         int c = 0;
         if (g < pl.n_groups) {
@@ -377,39 +387,41 @@ __device__ __forceinline__ Plan build_costs(const FfnParams &P, Split &sp)
 // slots by expert (Eq. 1, the stable counting sort moe_expert_union computes)
 // are built by each workgroup in LDS straight from topk_idx, with the groups'
 // costs; workgroup 0 also writes them to the routing arrays for the later
-// launches and the caller.  Per pass of 512 slots: wavefront matches by ballot
-// (rank among equal experts, count per wavefront), per-expert counts in
-// wcnt[kWG][E] (scratch in the activation tiles, unused this early); one scan
+// launches and the caller.  Per pass of one slot per thread: wavefront matches
+// by ballot (rank among equal experts, count per wavefront), per-expert counts
+// in wcnt[kPW][E] (scratch in the activation tiles, unused this early); one scan
 // over the experts in id order (= union order) gives each member its union
 // position and first grouped position, a second one the cost prefix; a second
 // sweep places every slot.
 template <int FMT, bool MXA>
 __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, int *wcnt)
 {
-    constexpr int kPass = 8;  // slots: T * k <= 64 * 64 = kPass * kThreads
-    constexpr int EPT = 2;    // experts per thread: E <= 1024
+    constexpr int kPass = 4096 / kEThreads;               // slots: T * k <= 64 * 64 = kPass * kEThreads
+    constexpr int EPT = (1024 + kEThreads - 1) / kEThreads;  // experts per thread: E <= 1024
     const VerifyArgs &a = P.a;
     const int S = a.T * a.k, E = a.E, tid = threadIdx.x, wave = tid / kWave;
     const bool out = blockIdx.x == 0;
     int nbits = 0;
     while ((1 << nbits) < E) ++nbits;
-    const int passes = (S + kThreads - 1) / kThreads;
-    const int nj = E > kThreads ? 2 : 1;  // expert rounds actually needed (the code runs cold: skip the second)
+    const int passes = (S + kEThreads - 1) / kEThreads;
+    const int nj = (E + kEThreads - 1) / kEThreads;  // expert rounds actually needed (the code runs cold: skip the rest)
     int ex[kPass], rank[kPass], cnt[kPass];
     bool top[kPass];
 #pragma unroll
     for (int ps = 0; ps < kPass; ++ps) {
-        const int sl = ps * kThreads + tid;
+        const int sl = ps * kEThreads + tid;
         ex[ps] = ps < passes && sl < S ? a.topk_idx[sl] : -1;
         rank[ps] = cnt[ps] = 0;
         top[ps] = false;
     }
     // Counts per expert over the passes.
-    int tot[EPT] = {0, 0};
+    int tot[EPT];
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) tot[j] = 0;
 #pragma unroll
     for (int ps = 0; ps < kPass; ++ps) {
         if (ps >= passes) break;
-        for (int i = tid; i < kWG * E; i += kThreads) wcnt[i] = 0;
+        for (int i = tid; i < kPW * E; i += kEThreads) wcnt[i] = 0;
         __syncthreads();
         wave_match(ex[ps], (unsigned)ex[ps] < (unsigned)E, nbits, rank[ps], top[ps], cnt[ps]);
         if (top[ps]) wcnt[wave * E + ex[ps]] = cnt[ps];
@@ -417,19 +429,21 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
 #pragma unroll
         for (int j = 0; j < EPT; ++j) {
             if (j >= nj) break;
-            const int e = j * kThreads + tid;
+            const int e = j * kEThreads + tid;
             if (e < E)
-                for (int w = 0; w < kWG; ++w) tot[j] += wcnt[w * E + e];
+                for (int w = 0; w < kPW; ++w) tot[j] += wcnt[w * E + e];
         }
         if (ps + 1 < passes) __syncthreads();  // one pass: its counts stay in wcnt for the placement
     }
     // Union positions, first grouped positions and the cost prefix.  A group
     // keeps at most 64 tokens (more only with repeated experts within a token).
-    int run_u = 0, run_p = 0, run_c = 0, start[EPT] = {0, 0};
+    int run_u = 0, run_p = 0, run_c = 0, start[EPT];
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) start[j] = 0;
 #pragma unroll
     for (int j = 0; j < EPT; ++j) {
         if (j >= nj) break;
-        const int e = j * kThreads + tid;
+        const int e = j * kEThreads + tid;
         const int c = e < E ? tot[j] : 0;
         const int M = min(kTokGroup, c);
         int up, cp, tup, tcost;
@@ -463,12 +477,14 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
         sp.cw[pl.n_groups] = total;
     }
     // Placement: first position of the expert + slots of earlier passes and wavefronts + rank.
-    int run[EPT] = {start[0], start[1]};
+    int run[EPT];
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) run[j] = start[j];
 #pragma unroll
     for (int ps = 0; ps < kPass; ++ps) {
         if (ps >= passes) break;
         if (passes > 1) {
-            for (int i = tid; i < kWG * E; i += kThreads) wcnt[i] = 0;
+            for (int i = tid; i < kPW * E; i += kEThreads) wcnt[i] = 0;
             __syncthreads();
             if (top[ps]) wcnt[wave * E + ex[ps]] = cnt[ps];
             __syncthreads();
@@ -476,13 +492,13 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
 #pragma unroll
         for (int j = 0; j < EPT; ++j) {
             if (j >= nj) break;
-            const int e = j * kThreads + tid;
+            const int e = j * kEThreads + tid;
             if (e < E) {
-                int nw[kWG];
+                int nw[kPW];
 #pragma unroll
-                for (int w = 0; w < kWG; ++w) nw[w] = wcnt[w * E + e];
+                for (int w = 0; w < kPW; ++w) nw[w] = wcnt[w * E + e];
 #pragma unroll
-                for (int w = 0; w < kWG; ++w) {
+                for (int w = 0; w < kPW; ++w) {
                     wcnt[w * E + e] = run[j];
                     run[j] += nw[w];
                 }
@@ -490,14 +506,14 @@ __device__ __forceinline__ Plan union_and_costs(const FfnParams &P, Split &sp, i
         }
         __syncthreads();
         if ((unsigned)ex[ps] < (unsigned)E) {
-            const int pos = wcnt[wave * E + ex[ps]] + rank[ps], sl = ps * kThreads + tid;
+            const int pos = wcnt[wave * E + ex[ps]] + rank[ps], sl = ps * kEThreads + tid;
             sp.tok[pos] = sl / a.k;
             if (out) a.perm[pos] = sl;
         }
         if (ps + 1 < passes) __syncthreads();
     }
     if (out) {
-        for (int u = tid; u <= E; u += kThreads) {
+        for (int u = tid; u <= E; u += kEThreads) {
             if (u < E) a.union_ids[u] = u < run_u ? sp.ge[u] : -1;
             a.offsets[u] = u < run_u ? sp.gp0[u] : run_p;
         }
@@ -517,7 +533,7 @@ __device__ __forceinline__ long first_unit(const Split &sp, int n_groups, long K
 __device__ __forceinline__ void build_bounds(Split &sp, int n_groups, long K, int W)
 {
     const long long C = (long long)sp.cw[n_groups] * K;
-    for (int v = threadIdx.x; v <= W; v += kThreads) sp.bound[v] = first_unit(sp, n_groups, K, W, C * v);
+    for (int v = threadIdx.x; v <= W; v += kEThreads) sp.bound[v] = first_unit(sp, n_groups, K, W, C * v);
     __syncthreads();
 }
 
@@ -625,85 +641,99 @@ __device__ __forceinline__ float activate(const VerifyArgs &a, float g, float u)
     return gated(g, a.alpha) * (u + 1.f);
 }
 
-// Finishes a wavefront's (tile 0, tile 1) accumulators of an item: gate/up ->
-// bf16 SwiGLU rows of H, down -> fp32 rows of O, both at grouped positions.  Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for
-// token column col of each 16-token block.
+// Finishes the accumulators of an item held by wavefront pw, which owns slots
+// pw * VPW .. pw * VPW + VPW - 1 (tiles 2j, 2j + 1 of its slot j): gate/up ->
+// bf16 SwiGLU rows of H, down -> fp32 rows of O, both at grouped positions.
+// Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for token column col
+// of each 16-token block.
 //
 // MX activation mode, gate/up: the SwiGLU rows go to the down launch as MX
-// FP8.  A band (128 rows) is one 128-element chunk of an H row; wavefront w's
-// 16 rows are half of the 32-row block w / 2, the other half being wavefront
-// w ^ 1's, so the two exchange their per-token maxima through LDS (every
-// wavefront of the workgroup takes part, also those past the last row, which
-// write the zero padding the down launch reads).  Row 16w + j of the chunk is
-// stored at byte 32 (w % 4) + 16 (w / 4) + j, the FP8 operand's lane order.
-template <bool DOWN, bool MXA>
-__device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &d, int wave,
-                                            const f32x4 (&acc)[2][kMB], const ItemBias &bias)
+// FP8.  A band (128 rows) is one 128-element chunk of an H row; slot v's 16
+// rows are half of the 32-row block v / 2, the other half being slot v ^ 1's,
+// so the two exchange their per-token maxima through LDS (every wavefront of
+// the workgroup takes part, also those past the last row, which write the
+// zero padding the down launch reads).  Row 16v + j of the chunk is stored at
+// byte 32 (v % 4) + 16 (v / 4) + j, the FP8 operand's lane order.
+template <bool DOWN, bool MXA, int VPW>
+__device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &d, int pw,
+                                            const f32x4 (&acc)[2 * VPW][kMB], const ItemBias (&bias)[VPW])
 {
     const VerifyArgs &a = P.a;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
     if constexpr (!DOWN && MXA) {
         __shared__ float red[kWG][kMB][16];
-        const bool rows_ok = tile_row<false>(d, wave, 0) < P.N;  // N % 32 == 0: a tile is all in or all out
-        float h[kMB][4];
+        float h[VPW][kMB][4];
 #pragma unroll
-        for (int mb = 0; mb < kMB; ++mb) {
-            const f32x4 g = acc[0][mb] + bias.g, v = acc[1][mb] + bias.u;
-            const bool live = rows_ok && mb * 16 + col < d.M;
+        for (int j = 0; j < VPW; ++j) {
+            const int v = pw * VPW + j;
+            const bool rows_ok = tile_row<false>(d, v, 0) < P.N;  // N % 32 == 0: a tile is all in or all out
 #pragma unroll
-            for (int i = 0; i < 4; ++i) h[mb][i] = live ? activate(a, g[i], v[i]) : 0.f;
-            float m = fmaxf(fmaxf(fabsf(h[mb][0]), fabsf(h[mb][1])), fmaxf(fabsf(h[mb][2]), fabsf(h[mb][3])));
-            m = fmaxf(m, __shfl_xor(m, 16, kWave));
-            m = fmaxf(m, __shfl_xor(m, 32, kWave));
-            if (grp == 0) red[wave][mb][col] = m;
+            for (int mb = 0; mb < kMB; ++mb) {
+                const f32x4 g = acc[2 * j][mb] + bias[j].g, u = acc[2 * j + 1][mb] + bias[j].u;
+                const bool live = rows_ok && mb * 16 + col < d.M;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) h[j][mb][i] = live ? activate(a, g[i], u[i]) : 0.f;
+                float m = fmaxf(fmaxf(fabsf(h[j][mb][0]), fabsf(h[j][mb][1])), fmaxf(fabsf(h[j][mb][2]), fabsf(h[j][mb][3])));
+                m = fmaxf(m, __shfl_xor(m, 16, kWave));
+                m = fmaxf(m, __shfl_xor(m, 32, kWave));
+                if (grp == 0) red[v][mb][col] = m;
+            }
         }
         __syncthreads();
         const int kp = P.nbands * P.band_rows;  // padded d_ff
 #pragma unroll
-        for (int mb = 0; mb < kMB; ++mb) {
-            const int r = mb * 16 + col;
-            if (r >= d.M) continue;
-            const int E = mx_exponent(fmaxf(red[wave][mb][col], red[wave ^ 1][mb][col]));
-            const float inv = mx_inv_scale(E);
-            const uint32_t q = e4m3_code(h[mb][0] * inv) | (e4m3_code(h[mb][1] * inv) << 8) |
-                               (e4m3_code(h[mb][2] * inv) << 16) | (e4m3_code(h[mb][3] * inv) << 24);
-            const size_t p = (size_t)(d.p0 + r);
-            *reinterpret_cast<uint32_t *>(a.hq + p * kp + d.n0 + 32 * (wave & 3) + 16 * (wave >> 2) + 4 * grp) = q;
-            if ((wave & 1) == 0 && grp == 0) a.hs[p * (kp / 32) + d.n0 / 32 + wave / 2] = (uint8_t)(E + 127);
+        for (int j = 0; j < VPW; ++j) {
+            const int v = pw * VPW + j;
+#pragma unroll
+            for (int mb = 0; mb < kMB; ++mb) {
+                const int r = mb * 16 + col;
+                if (r >= d.M) continue;
+                const int E = mx_exponent(fmaxf(red[v][mb][col], red[v ^ 1][mb][col]));
+                const float inv = mx_inv_scale(E);
+                const uint32_t q = e4m3_code(h[j][mb][0] * inv) | (e4m3_code(h[j][mb][1] * inv) << 8) |
+                                   (e4m3_code(h[j][mb][2] * inv) << 16) | (e4m3_code(h[j][mb][3] * inv) << 24);
+                const size_t p = (size_t)(d.p0 + r);
+                *reinterpret_cast<uint32_t *>(a.hq + p * kp + d.n0 + 32 * (v & 3) + 16 * (v >> 2) + 4 * grp) = q;
+                if ((v & 1) == 0 && grp == 0) a.hs[p * (kp / 32) + d.n0 / 32 + v / 2] = (uint8_t)(E + 127);
+            }
         }
         return;
     }
-    if (tile_row<DOWN>(d, wave, 0) >= P.N) return;  // rows past the last band
 #pragma unroll
-    for (int mb = 0; mb < kMB; ++mb) {
-        const int r = mb * 16 + col;
-        if (r >= d.M) continue;
-        const int p = d.p0 + r;
-        if (!DOWN) {
-            f32x4 g = acc[0][mb], v = acc[1][mb];
-            uint32_t h2[2];
-            if (a.act == 0 && !a.b_gate && !a.b_up) {
+    for (int j = 0; j < VPW; ++j) {
+        const int v = pw * VPW + j;
+        if (tile_row<DOWN>(d, v, 0) >= P.N) continue;  // rows past the last band
 #pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const float g0 = g[2 * i], g1 = g[2 * i + 1];
-                    h2[i] = pack_bf16x2(gated(g0, 1.f) * v[2 * i], gated(g1, 1.f) * v[2 * i + 1]);
+        for (int mb = 0; mb < kMB; ++mb) {
+            const int r = mb * 16 + col;
+            if (r >= d.M) continue;
+            const int p = d.p0 + r;
+            if (!DOWN) {
+                f32x4 g = acc[2 * j][mb], u = acc[2 * j + 1][mb];
+                uint32_t h2[2];
+                if (a.act == 0 && !a.b_gate && !a.b_up) {
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) {
+                        const float g0 = g[2 * i], g1 = g[2 * i + 1];
+                        h2[i] = pack_bf16x2(gated(g0, 1.f) * u[2 * i], gated(g1, 1.f) * u[2 * i + 1]);
+                    }
+                } else {
+                    g += bias[j].g;
+                    u += bias[j].u;
+                    float h[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) h[i] = activate(a, g[i], u[i]);
+                    h2[0] = pack_bf16x2(h[0], h[1]);
+                    h2[1] = pack_bf16x2(h[2], h[3]);
                 }
+                *reinterpret_cast<u32x2 *>(a.h + (size_t)p * a.d_ff + tile_row<DOWN>(d, v, 0) + 4 * grp) =
+                    u32x2{h2[0], h2[1]};
             } else {
-                g += bias.g;
-                v += bias.u;
-                float h[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) h[i] = activate(a, g[i], v[i]);
-                h2[0] = pack_bf16x2(h[0], h[1]);
-                h2[1] = pack_bf16x2(h[2], h[3]);
+                for (int t = 0; t < 2; ++t)
+                    *reinterpret_cast<f32x4 *>(a.o + (size_t)p * a.d + tile_row<DOWN>(d, v, t) + 4 * grp) =
+                        acc[2 * j + t][mb];
             }
-            *reinterpret_cast<u32x2 *>(a.h + (size_t)p * a.d_ff + tile_row<DOWN>(d, wave, 0) + 4 * grp) =
-                u32x2{h2[0], h2[1]};
-        } else {
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-                *reinterpret_cast<f32x4 *>(a.o + (size_t)p * a.d + tile_row<DOWN>(d, wave, t) + 4 * grp) =
-                    acc[t][mb];
         }
     }
 }
@@ -712,10 +742,11 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
 
 // Where the loads of one item come from.  Wave-uniform except the lane offsets.
 struct Source {
-    rsrc_t ra0, ra1, rs0, rs1;  // weight tiles 0 / 1 and their scales
-    uint32_t a0, a1;            // lane offsets of the two tiles at step 0 (kOff: rows past N)
+    rsrc_t ra0, ra1, rs0, rs1;  // matrices of each slot's tiles 0 / 1 (gate / up, or its two row tiles) and their scales
+    uint32_t a[kNT];            // lane offsets of the wavefront's tiles at step 0 (tile 2j + t: slot j's tile t;
+                                // kOff: rows past N)
     uint32_t kstride;           // bytes from one 128-wide block of a tile to the next
-    uint32_t q0, q1;            // scale offsets at step 0
+    uint32_t q[kNT];            // scale offsets at step 0
     uint32_t boff[kBPass];      // lane offsets of this thread's activation chunks at step 0 (kOff: no token)
     uint32_t soff[kBPass];      // MX activations: offsets of the rows' block scales at step 0
     int kc;                     // first element (within a 128-wide block) of the thread's activation chunk
@@ -739,37 +770,34 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
 
     const int nblocks = P.nblocks;
     const uint32_t mat_bytes = (uint32_t)P.mat_bytes;  // < 2^31 (checked at the boundary)
-    const int row0 = tile_row<DOWN>(d, wave, 0), row1 = tile_row<DOWN>(d, wave, 1);
-    const bool arow_ok = row0 < P.N;
-    if (DOWN && d.pair) {
-        // Row tiles 2p and 2p + 1 interleaved block by block: one contiguous run per block.
-        src.ra0 = src.ra1 = make_rsrc(d.wa, mat_bytes);
+    // Paired layouts (pack.hip): a slot's two tiles of one block are one run (down: its two row tiles,
+    // gate/up: the gate and up tiles of its rows), tile t at t * BLK in the run.
+    if (d.pair) {
+        src.ra0 = src.ra1 = make_rsrc(d.wa, DOWN ? mat_bytes : 2u * mat_bytes);
         src.kstride = 2u * BLK;
-        src.a0 = arow_ok ? (uint32_t)(row0 / 32) * nblocks * 2u * BLK + lane * 16u : kOff;
-        src.a1 = arow_ok ? src.a0 + BLK : kOff;
-    } else if (d.pair) {
-        // Gate block then up block of the same rows: one contiguous run per block.
-        src.ra0 = src.ra1 = make_rsrc(d.wa, 2u * mat_bytes);
-        src.kstride = 2u * BLK;
-        src.a0 = arow_ok ? (uint32_t)(row0 / 16) * nblocks * 2u * BLK + lane * 16u : kOff;
-        src.a1 = arow_ok ? src.a0 + BLK : kOff;
     } else {
         src.ra0 = make_rsrc(d.wa, mat_bytes);
         src.ra1 = make_rsrc(d.wb, mat_bytes);
         src.kstride = BLK;
-        src.a0 = arow_ok ? (uint32_t)(row0 / 16) * nblocks * BLK + lane * 16u : kOff;
-        src.a1 = arow_ok ? (uint32_t)(row1 / 16) * nblocks * BLK + lane * 16u : kOff;
     }
     const uint32_t sc_bytes = (uint32_t)P.sc_bytes;
     src.rs0 = make_rsrc(FMT == FMT_BF16 ? d.wa : d.sa, FMT == FMT_BF16 ? 0u : sc_bytes);
     src.rs1 = make_rsrc(FMT == FMT_BF16 ? d.wb : d.sb, FMT == FMT_BF16 ? 0u : sc_bytes);
-    src.q0 = src.q1 = 0;
-    if constexpr (FMT == FMT_FP8) {
-        src.q0 = arow_ok ? (uint32_t)(row0 / 128) * (K / 128) * 4u : kOff;
-        src.q1 = arow_ok ? (uint32_t)(row1 / 128) * (K / 128) * 4u : kOff;
-    } else if constexpr (FMT == FMT_MXFP4) {
-        src.q0 = arow_ok ? (uint32_t)(row0 / 16) * ((nblocks + 3) / 4) * 256u + lane * 4u : kOff;
-        src.q1 = arow_ok ? (uint32_t)(row1 / 16) * ((nblocks + 3) / 4) * 256u + lane * 4u : kOff;
+#pragma unroll
+    for (int tt = 0; tt < kNT; ++tt) {
+        const int v = wave * kVPW + tt / 2, t = tt % 2;
+        const int row0 = tile_row<DOWN>(d, v, 0), row = tile_row<DOWN>(d, v, t);
+        const bool ok = row0 < P.N;  // a slot's rows are all in or all out
+        if (d.pair)  // the slot's run (unit: 32 rows for down, 16 for gate/up) at block 0
+            src.a[tt] = ok ? (uint32_t)(row0 / (DOWN ? 32 : 16)) * nblocks * 2u * BLK + (uint32_t)t * BLK + lane * 16u
+                           : kOff;
+        else
+            src.a[tt] = ok ? (uint32_t)(row / 16) * nblocks * BLK + lane * 16u : kOff;
+        src.q[tt] = 0;
+        if constexpr (FMT == FMT_FP8)
+            src.q[tt] = ok ? (uint32_t)(row / 128) * (K / 128) * 4u : kOff;
+        else if constexpr (FMT == FMT_MXFP4)
+            src.q[tt] = ok ? (uint32_t)(row / 16) * ((nblocks + 3) / 4) * 256u + lane * 4u : kOff;
     }
 
     // Activation rows: in pass i, lane l of this wavefront stages row
@@ -800,11 +828,12 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
     }
 }
 
-// One macro step of a wavefront: its two 16 x 128 weight tiles against the
-// NMB 16-token blocks of the activation tile in LDS.  The activation reads of
-// sub-step s + 1 are issued before the matrix-core work of sub-step s.
+// One macro step of a wavefront: its kNT 16 x 128 weight tiles against the
+// NMB 16-token blocks of the activation tile in LDS, each activation fragment
+// read once for all tiles.  The activation reads of sub-step s + 1 are issued
+// before the matrix-core work of sub-step s.
 template <int FMT, int NMB>
-__device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_t *buf, f32x4 (&acc)[2][kMB])
+__device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[kNT], const uint8_t *buf, f32x4 (&acc)[kNT][kMB])
 {
     constexpr int SB = Fmt<FMT>::kBlocks, NS = 4 * SB;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
@@ -819,10 +848,10 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
         b[0][mb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * 256 + boff(0)));
     // FP8 accumulates the step in `part` and adds scale * part at the end; the other formats
     // accumulate in place.
-    f32x4 part[2][NMB];
+    f32x4 part[kNT][NMB];
     if constexpr (FMT == FMT_FP8) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < kNT; ++t)
 #pragma unroll
             for (int mb = 0; mb < NMB; ++mb) part[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
@@ -834,21 +863,21 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[2], const uint8_
                 b[(s + 1) & 1][mb] =
                     __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * 256 + boff(s + 1)));
         }
-        const bf16x8 av0 = decode_a<FMT>(wv[0], s), av1 = decode_a<FMT>(wv[1], s);
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb) {
-            f32x4 &c0 = FMT == FMT_FP8 ? part[0][mb] : acc[0][mb];
-            f32x4 &c1 = FMT == FMT_FP8 ? part[1][mb] : acc[1][mb];
-            c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av0, b[s & 1][mb], c0, 0, 0, 0);
-            c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av1, b[s & 1][mb], c1, 0, 0, 0);
+        for (int t = 0; t < kNT; ++t) {
+            const bf16x8 av = decode_a<FMT>(wv[t], s);
+#pragma unroll
+            for (int mb = 0; mb < NMB; ++mb) {
+                f32x4 &c = FMT == FMT_FP8 ? part[t][mb] : acc[t][mb];
+                c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, b[s & 1][mb], c, 0, 0, 0);
+            }
         }
     }
     if constexpr (FMT == FMT_FP8) {
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb) {
-            acc[0][mb] += wv[0].scale * part[0][mb];
-            acc[1][mb] += wv[1].scale * part[1][mb];
-        }
+        for (int t = 0; t < kNT; ++t)
+#pragma unroll
+            for (int mb = 0; mb < NMB; ++mb) acc[t][mb] += wv[t].scale * part[t][mb];
     }
 }
 
@@ -874,8 +903,8 @@ typedef __attribute__((ext_vector_type(8))) int i32x8;
 // and 64+16grp..64+16grp+15 (stored contiguously) with the scale of block grp
 // (K 32grp..32grp+31), which the instruction applies to that K block.
 template <int NMB>
-__device__ __forceinline__ void contract_mx(const WFrag<FMT_MXFP4> (&wv)[2], const uint8_t *buf,
-                                            f32x4 (&acc)[2][kMB])
+__device__ __forceinline__ void contract_mx(const WFrag<FMT_MXFP4> (&wv)[kNT], const uint8_t *buf,
+                                            f32x4 (&acc)[kNT][kMB])
 {
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
     const uint8_t *bp = buf + col * kRowQ + grp * 32;
@@ -892,7 +921,7 @@ __device__ __forceinline__ void contract_mx(const WFrag<FMT_MXFP4> (&wv)[2], con
             sb[mb] = sp[mb * 16 * 8 + b * 4];
         }
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
+        for (int t = 0; t < kNT; ++t) {
             const u32x4 w = wv[t].v[b];
             const i32x8 av = i32x8{(int)w[0], (int)w[1], (int)w[2], (int)w[3], 0, 0, 0, 0};
             const int sa = (int)((wv[t].code >> (wv[t].shift + 8 * b)) & 0xffu);
@@ -933,7 +962,7 @@ __device__ __forceinline__ void record_outputs(const FfnParams &P, const Plan &p
         const int M = sp.gM[gi], p0 = sp.gp0[gi];
         const bool whole = ib >= x0;
         const uint64_t cut = whole ? 0ull : split::out_cut(sp.cw, sp.bound, pl.n_groups, K, P.workers, ib, ie);
-        for (int r = threadIdx.x; r < M; r += kThreads) {
+        for (int r = threadIdx.x; r < M; r += kEThreads) {
             const int p = p0 + r;
             const int row = p >= S ? p : S <= kMaxTokLds ? sp.tok[p] : a.perm[p];
             a.desc[(size_t)row * P.nbands + band] = whole ? split::out_whole((uint32_t)p) : split::out_with_row(cut, r);
@@ -981,7 +1010,8 @@ __device__ __forceinline__ int partial_offset(int wave, int t, int mb, int lane)
 // the unit PD - 1 places ahead are issued while a unit is contracted, across
 // item boundaries: one pipeline for the whole range, never drained in between.
 template <int FMT, bool DOWN, int PD, bool MXA>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void expert_ffn_kernel(FfnParams P)
+__global__ __launch_bounds__(kEThreads) __attribute__((amdgpu_waves_per_eu(kVPW == 1 ? 2 : 1, kVPW == 1 ? 2 : 1)))
+void expert_ffn_kernel(FfnParams P)
 {
     static_assert(!MXA || FMT == FMT_MXFP4, "MX activations take MXFP4 weights");
     static_assert(!MXA || 2 * (kScaleQ + kMB * 16 * 8) <= 2 * BTile<Fmt<FMT>::kBlocks>::kBuf, "MX tile fits the LDS");
@@ -1000,7 +1030,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int tid = threadIdx.x, br = tid >> 4, bc = tid & 15;
     const int nsteps = P.nsteps, K = P.K;
     __shared__ Split sp;
-    static_assert(NT * BBUF >= kWG * 1024 * 4, "the union's scratch fits the activation tiles");
+    static_assert(NT * BBUF >= kPW * 1024 * 4, "the union's scratch fits the activation tiles");
     const Plan pl = !DOWN && P.plan == nullptr ? union_and_costs<FMT, MXA>(P, sp, reinterpret_cast<int *>(lds))
                                                : build_costs<FMT, MXA, DOWN>(P, sp);
     build_bounds(sp, pl.n_groups, (long)P.nbands * nsteps, P.workers);
@@ -1044,13 +1074,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     Source src;
     set_source<FMT, DOWN, MXA>(src, P, sp, item_of(unit_of(0)));
 
-    WFrag<FMT> wf[PD][2];
+    WFrag<FMT> wf[PD][kNT];
     u32x4 bst[MXA ? PD : 1][kBPass][SB];      // MX: the activation codes of a step
     uint32_t sst[MXA ? PD : 1][kBPass];       // MX: the rows' block scales of a step (threads bc < 2)
     // Vector-memory instructions per unit: weight side (weights and scales, plus MX activations)
     // and direct activation loads.  Every unit issues exactly these, past the range too (loads
     // of zeros: offsets beyond every buffer), so that the counted wait below is exact.
-    constexpr int kLdW = 2 * NV * SB + (FMT == FMT_FP8 ? 2 * SB : FMT == FMT_MXFP4 ? 2 : 0) + (MXA ? 2 * kBPass : 0);
+    constexpr int kLdW = kNT * NV * SB + (FMT == FMT_FP8 ? kNT * SB : FMT == FMT_MXFP4 ? kNT : 0) + (MXA ? 2 * kBPass : 0);
     constexpr int kLdA = MXA ? 0 : kBPass * SB;
     // Weight-side loads of the i-th unit of the sequence into ring slot `slot`.
     auto issue_w = [&](int slot, int i) {
@@ -1065,23 +1095,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
             const bool okb = ok && (SB == 1 || (int)kb < P.nblocks);
             const uint32_t so = kb * src.kstride;
 #pragma unroll
-            for (int i = 0; i < NV; ++i) {
-                wf[slot][0].v[b * NV + i] = load16<kAuxNT>(src.ra0, okb ? src.a0 + so + 1024u * i : kOff);
-                wf[slot][1].v[b * NV + i] = load16<kAuxNT>(src.ra1, okb ? src.a1 + so + 1024u * i : kOff);
-            }
+            for (int tt = 0; tt < kNT; ++tt)
+#pragma unroll
+                for (int i = 0; i < NV; ++i)
+                    wf[slot][tt].v[b * NV + i] = load16<kAuxNT>(tt % 2 ? src.ra1 : src.ra0, okb ? src.a[tt] + so + 1024u * i : kOff);
             if constexpr (FMT == FMT_FP8) {
                 const uint32_t sso = kb * 4u;
-                wf[slot][0].scale = __builtin_bit_cast(
-                    float, __builtin_amdgcn_raw_buffer_load_b32(src.rs0, (int)(okb ? src.q0 + sso : kOff), 0, 0));
-                wf[slot][1].scale = __builtin_bit_cast(
-                    float, __builtin_amdgcn_raw_buffer_load_b32(src.rs1, (int)(okb ? src.q1 + sso : kOff), 0, 0));
+#pragma unroll
+                for (int tt = 0; tt < kNT; ++tt)
+                    wf[slot][tt].scale = __builtin_bit_cast(
+                        float, __builtin_amdgcn_raw_buffer_load_b32(tt % 2 ? src.rs1 : src.rs0, (int)(okb ? src.q[tt] + sso : kOff),
+                                                                    0, 0));
             } else if constexpr (FMT == FMT_MXFP4) {
                 // The quad holding the step's blocks (kb0 = step * SB is even, so both lie in it).
                 if (b == 0) {
                     const uint32_t sso = (kb >> 2) * 256u;
-                    wf[slot][0].code = __builtin_amdgcn_raw_buffer_load_b32(src.rs0, (int)(okb ? src.q0 + sso : kOff), 0, 0);
-                    wf[slot][1].code = __builtin_amdgcn_raw_buffer_load_b32(src.rs1, (int)(okb ? src.q1 + sso : kOff), 0, 0);
-                    wf[slot][0].shift = wf[slot][1].shift = (int)(kb & 3u) * 8;
+#pragma unroll
+                    for (int tt = 0; tt < kNT; ++tt) {
+                        wf[slot][tt].code = __builtin_amdgcn_raw_buffer_load_b32(tt % 2 ? src.rs1 : src.rs0,
+                                                                                 (int)(okb ? src.q[tt] + sso : kOff), 0, 0);
+                        wf[slot][tt].shift = (int)(kb & 3u) * 8;
+                    }
                 }
             }
         }
@@ -1099,7 +1133,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         }
     };
     // Activation tile of the i-th unit straight into LDS tile i % PD (bf16 activations): pass p,
-    // block b of this wavefront covers token rows 32p + 4 wave .. + 3, 1 KiB of the tile.  Rows
+    // block b of this wavefront covers token rows kBRowsPerPass p + 4 wave .. + 3, 1 KiB of the tile.  Rows
     // past the item's tokens and elements past K read zeros.  Uses the sources issue_w(i) set.
     auto issue_a = [&](int i) {
         if constexpr (!MXA) {
@@ -1122,11 +1156,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // The item being contracted.
     int citem = item_of(unit_of(0));
     ItemDesc cd = describe_lds<DOWN>(P, sp, citem);
-    ItemBias cbias = load_bias<DOWN>(P, cd, wave);
-    int cib = citem * nsteps;
-    f32x4 acc[2][kMB];
+    ItemBias cbias[kVPW];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int j = 0; j < kVPW; ++j) cbias[j] = load_bias<DOWN>(P, cd, wave * kVPW + j);
+    int cib = citem * nsteps;
+    f32x4 acc[kNT][kMB];
+#pragma unroll
+    for (int t = 0; t < kNT; ++t)
 #pragma unroll
         for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -1186,25 +1222,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         const int un = i + 1 < n ? unit_of(i + 1) : -1;
         if (u + 1 == cib + nsteps || un != u + 1) {
             if (cib >= x0 && cib + nsteps <= x1) {
-                finish_item<DOWN, MXA>(P, cd, wave, acc, cbias);
+                finish_item<DOWN, MXA, kVPW>(P, cd, wave, acc, cbias);
             } else {
                 float *dst = P.partials + ((size_t)w * 2 + (cib <= x0 ? 0 : 1)) * P.slot_floats;
 #pragma unroll
-                for (int t = 0; t < 2; ++t)
+                for (int tt = 0; tt < kNT; ++tt)
 #pragma unroll
                     for (int mb = 0; mb < kMB; ++mb)
                         if (mb < nmb)
-                            *reinterpret_cast<f32x4 *>(dst + partial_offset<DOWN>(wave, t, mb, lane)) = acc[t][mb];
+                            *reinterpret_cast<f32x4 *>(dst + partial_offset<DOWN>(wave * kVPW + tt / 2, tt % 2, mb, lane)) =
+                                acc[tt][mb];
             }
 #pragma unroll
-            for (int t = 0; t < 2; ++t)
+            for (int t = 0; t < kNT; ++t)
 #pragma unroll
                 for (int mb = 0; mb < kMB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
             if (un >= 0) {
                 citem = item_of(un);
                 cib = citem * nsteps;
                 cd = describe_lds<DOWN>(P, sp, citem);
-                cbias = load_bias<DOWN>(P, cd, wave);
+#pragma unroll
+                for (int j = 0; j < kVPW; ++j) cbias[j] = load_bias<DOWN>(P, cd, wave * kVPW + j);
             }
         }
     };
@@ -1253,7 +1291,7 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
     d.M = (int)ld_s64(rec + 3);
     d.n0 = (int)(item % P.nbands) * P.band_rows;
     const int nmb = (d.M + 15) / 16;  // only the live token blocks were parked
-    const ItemBias bias = load_bias<DOWN>(P, d, wave);  // in flight with the partial sums
+    const ItemBias bias[1] = {load_bias<DOWN>(P, d, wave)};  // in flight with the partial sums
     f32x4 acc[2][kMB];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -1300,7 +1338,7 @@ __global__ __launch_bounds__(kThreads) void expert_ffn_fixup_kernel(FfnParams P)
             if (slot >= 0) add(P.partials + (size_t)slot * P.slot_floats);
         }
     }
-    finish_item<DOWN, MXA>(P, d, wave, acc, bias);
+    finish_item<DOWN, MXA, 1>(P, d, wave, acc, bias);
 }
 
 // MX activation mode: x [T][K] bf16 -> e4m3fn codes [T][kp] in the FP8
@@ -1632,7 +1670,7 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     g.ranges = reinterpret_cast<long long *>(partials + (size_t)G * 2 * ws.slot_floats);
     g.fix = g.ranges + (size_t)G * 2;
     g.plan = grouped ? plan : nullptr;
-    hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD, MXA>), dim3(G), dim3(kThreads), 0, stream, g);
+    hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD, MXA>), dim3(G), dim3(kEThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = mark(events, 1, stream)) != hipSuccess) return err;
     hipLaunchKernelGGL((expert_ffn_fixup_kernel<false, MXA>), dim3(G), dim3(kThreads), 0, stream, g);
@@ -1648,7 +1686,7 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     dn.mat_bytes = packed_matrix_bytes(FMT, a.d, a.d_ff);
     dn.sc_bytes = packed_scale_bytes(FMT, a.d, a.d_ff);
     if ((err = mark(events, 2, stream)) != hipSuccess) return err;
-    hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD, MXA>), dim3(G), dim3(kThreads), 0, stream, dn);
+    hipLaunchKernelGGL((expert_ffn_kernel<FMT, true, PD, MXA>), dim3(G), dim3(kEThreads), 0, stream, dn);
     if ((err = hipGetLastError()) != hipSuccess) return err;
 
     // Combine also adds up the down items cut between workgroups.
