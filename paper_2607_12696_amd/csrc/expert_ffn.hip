@@ -154,17 +154,14 @@ template <int FMT> struct WFrag {
     int shift;                                     // MXFP4: bit offset of the step's first block in `code`
 };
 
-__device__ __forceinline__ float e8m0_to_f32(uint32_t code)
-{
-    // 2^(code-127); code 0 is the subnormal 2^-127, code 255 is NaN.  Written
-    // as two selects on the bits: as nested conditional expressions the
-    // compiler branched around them, splitting the contraction into many
-    // small blocks at every sub-step.
-    uint32_t b = code << 23;
-    b = code == 0u ? 0x00400000u : b;
-    b = code == 255u ? 0x7fc00000u : b;
-    return __uint_as_float(b);
-}
+// The scale operand of the scaled conversions (v_cvt_scalef32_*): the
+// instruction takes the operand's exponent field as an e8m0 code, so field 0
+// scales by 2^-127 and field 255 gives NaN, as the OCP MX definition of the
+// code does (checked on the device against the exact scale value for all 256
+// codes and all 256 FP4 code pairs: identical results).  The code shifted into
+// the exponent field is therefore the operand for every code, with no special
+// cases.
+__device__ __forceinline__ float e8m0_scale_operand(uint32_t code) { return __uint_as_float((code & 0xffu) << 23); }
 
 // MX FP8 activation quantisation.  A block's scale exponent from its largest
 // magnitude: E = floor(log2(amax)) - 8 (448, the largest e4m3fn value, is
@@ -220,7 +217,7 @@ __device__ __forceinline__ bf16x8 decode_a(const WFrag<FMT> &f, int s)
         return __builtin_bit_cast(bf16x8, o);
     } else {
         const uint32_t w = f.v[s >> 2][s & 3];
-        const float sc = e8m0_to_f32((f.code >> (f.shift + 8 * (s >> 2))) & 0xffu);
+        const float sc = e8m0_scale_operand(f.code >> (f.shift + 8 * (s >> 2)));
         u32x4 o;
         o[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 0));
         o[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 1));
@@ -829,11 +826,15 @@ __device__ __forceinline__ void set_source(Source &src, const FfnParams &P, cons
 }
 
 // One macro step of a wavefront: its kNT 16 x 128 weight tiles against the
-// NMB 16-token blocks of the activation tile in LDS, each activation fragment
-// read once for all tiles.  The activation reads of sub-step s + 1 are issued
-// before the matrix-core work of sub-step s.
-template <int FMT, int NMB>
-__device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[kNT], const uint8_t *buf, f32x4 (&acc)[kNT][kMB])
+// nmb live 16-token blocks of the activation tile in LDS.  The tiles are
+// decoded once for the step; then each token block reads its activation
+// fragments and runs its chains.  Every accumulator is updated in place or
+// skipped (a wave-uniform branch per token block), so the loop carries them in
+// fixed registers whatever nmb is (a switch over nmb gave each arm its own
+// registers and the loop copied the accumulators back every step).
+template <int FMT>
+__device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[kNT], const uint8_t *buf, f32x4 (&acc)[kNT][kMB],
+                                         int nmb)
 {
     constexpr int SB = Fmt<FMT>::kBlocks, NS = 4 * SB;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
@@ -842,42 +843,38 @@ __device__ __forceinline__ void contract(const WFrag<FMT> (&wv)[kNT], const uint
     const uint8_t *bp = buf + col * 256;
     const int xg = ((4 * grp) ^ col) * 16;
     auto boff = [&](int s) { return (s >> 2) * BTile<SB>::kBlk + (xg ^ ((s & 3) * 16)); };
-    bf16x8 b[2][NMB];
+    bf16x8 av[NS][kNT];
 #pragma unroll
-    for (int mb = 0; mb < NMB; ++mb)
-        b[0][mb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * 256 + boff(0)));
-    // FP8 accumulates the step in `part` and adds scale * part at the end; the other formats
-    // accumulate in place.
-    f32x4 part[kNT][NMB];
-    if constexpr (FMT == FMT_FP8) {
+    for (int s = 0; s < NS; ++s)
 #pragma unroll
-        for (int t = 0; t < kNT; ++t)
+        for (int t = 0; t < kNT; ++t) av[s][t] = decode_a<FMT>(wv[t], s);
 #pragma unroll
-            for (int mb = 0; mb < NMB; ++mb) part[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int mb = 0; mb < kMB; ++mb) {
+        if (mb > 0 && mb >= nmb) break;
+        bf16x8 b[NS];
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-        if (s < NS - 1) {
+        for (int s = 0; s < NS; ++s)
+            b[s] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * 256 + boff(s)));
+        // FP8 accumulates the step in `part` and adds scale * part at the end; the other formats
+        // accumulate in place.
+        f32x4 part[kNT];
+        if constexpr (FMT == FMT_FP8) {
 #pragma unroll
-            for (int mb = 0; mb < NMB; ++mb)
-                b[(s + 1) & 1][mb] =
-                    __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(bp + mb * 16 * 256 + boff(s + 1)));
+            for (int t = 0; t < kNT; ++t) part[t] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
-        for (int t = 0; t < kNT; ++t) {
-            const bf16x8 av = decode_a<FMT>(wv[t], s);
+        for (int s = 0; s < NS; ++s)
 #pragma unroll
-            for (int mb = 0; mb < NMB; ++mb) {
-                f32x4 &c = FMT == FMT_FP8 ? part[t][mb] : acc[t][mb];
-                c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, b[s & 1][mb], c, 0, 0, 0);
+            for (int t = 0; t < kNT; ++t) {
+                f32x4 &c = FMT == FMT_FP8 ? part[t] : acc[t][mb];
+                c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[s][t], b[s], c, 0, 0, 0);
             }
+        if constexpr (FMT == FMT_FP8) {
+#pragma unroll
+            for (int t = 0; t < kNT; ++t)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[t][mb][j] = __builtin_fmaf(wv[t].scale, part[t][j], acc[t][mb][j]);
         }
-    }
-    if constexpr (FMT == FMT_FP8) {
-#pragma unroll
-        for (int t = 0; t < kNT; ++t)
-#pragma unroll
-            for (int mb = 0; mb < NMB; ++mb) acc[t][mb] += wv[t].scale * part[t][mb];
     }
 }
 
@@ -902,33 +899,37 @@ typedef __attribute__((ext_vector_type(8))) int i32x8;
 // with its e8m0 code; the B operand is token col's codes of K 16grp..16grp+15
 // and 64+16grp..64+16grp+15 (stored contiguously) with the scale of block grp
 // (K 32grp..32grp+31), which the instruction applies to that K block.
-template <int NMB>
 __device__ __forceinline__ void contract_mx(const WFrag<FMT_MXFP4> (&wv)[kNT], const uint8_t *buf,
-                                            f32x4 (&acc)[kNT][kMB])
+                                            f32x4 (&acc)[kNT][kMB], int nmb)
 {
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
     const uint8_t *bp = buf + col * kRowQ + grp * 32;
     const uint8_t *sp = buf + kScaleQ + col * 8 + grp;
+    i32x8 av[2][kNT];
+    int sa[2][kNT];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-        i32x8 bv[NMB];
-        int sb[NMB];
-#pragma unroll
-        for (int mb = 0; mb < NMB; ++mb) {
-            const u32x4 lo = *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kRowQ + b * 128);
-            const u32x4 hi = *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kRowQ + b * 128 + 16);
-            bv[mb] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
-            sb[mb] = sp[mb * 16 * 8 + b * 4];
-        }
+    for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int t = 0; t < kNT; ++t) {
             const u32x4 w = wv[t].v[b];
-            const i32x8 av = i32x8{(int)w[0], (int)w[1], (int)w[2], (int)w[3], 0, 0, 0, 0};
-            const int sa = (int)((wv[t].code >> (wv[t].shift + 8 * b)) & 0xffu);
+            av[b][t] = i32x8{(int)w[0], (int)w[1], (int)w[2], (int)w[3], 0, 0, 0, 0};
+            sa[b][t] = (int)((wv[t].code >> (wv[t].shift + 8 * b)) & 0xffu);
+        }
+    // Token blocks past nmb are skipped with a wave-uniform branch; the accumulators stay in
+    // place (see contract()).
 #pragma unroll
-            for (int mb = 0; mb < NMB; ++mb)
-                acc[t][mb] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv[mb], acc[t][mb], 4, 0, 0, sa, 0,
-                                                                              sb[mb]);
+    for (int mb = 0; mb < kMB; ++mb) {
+        if (mb > 0 && mb >= nmb) break;
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const u32x4 lo = *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kRowQ + b * 128);
+            const u32x4 hi = *reinterpret_cast<const u32x4 *>(bp + mb * 16 * kRowQ + b * 128 + 16);
+            const i32x8 bv = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+            const int sb = sp[mb * 16 * 8 + b * 4];
+#pragma unroll
+            for (int t = 0; t < kNT; ++t)
+                acc[t][mb] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av[b][t], bv, acc[t][mb], 4, 0, 0,
+                                                                              sa[b][t], 0, sb);
         }
     }
 }
@@ -1195,19 +1196,9 @@ void expert_ffn_kernel(FfnParams P)
             issue_a(i + PD - 1);
         }
         if constexpr (MXA) {
-            switch (nmb) {
-            case 1: contract_mx<1>(wf[slot], buf, acc); break;
-            case 2: contract_mx<2>(wf[slot], buf, acc); break;
-            case 3: contract_mx<3>(wf[slot], buf, acc); break;
-            default: contract_mx<4>(wf[slot], buf, acc); break;
-            }
+            contract_mx(wf[slot], buf, acc, nmb);
         } else {
-            switch (nmb) {
-            case 1: contract<FMT, 1>(wf[slot], buf, acc); break;
-            case 2: contract<FMT, 2>(wf[slot], buf, acc); break;
-            case 3: contract<FMT, 3>(wf[slot], buf, acc); break;
-            default: contract<FMT, 4>(wf[slot], buf, acc); break;
-            }
+            contract<FMT>(wf[slot], buf, acc, nmb);
         }
     };
 
