@@ -640,7 +640,10 @@ __device__ __forceinline__ float activate(const VerifyArgs &a, float g, float u)
 
 // Finishes the accumulators of an item held by wavefront pw, which owns slots
 // pw * VPW .. pw * VPW + VPW - 1 (tiles 2j, 2j + 1 of its slot j): gate/up ->
-// bf16 SwiGLU rows of H, down -> fp32 rows of O, both at grouped positions.
+// bf16 SwiGLU rows of H at grouped positions, down -> fp32 rows of O at the
+// rows' routed slots t * k + j (the shared expert's at T * k + t), so that the
+// combine kernel finds a whole item's row without a lookup.  tok: the slot of
+// each grouped position (down, T * k <= kMaxTokLds; else a.perm is read).
 // Lane (col, grp) holds rows 4*grp .. 4*grp+3 of a tile for token column col
 // of each 16-token block.
 //
@@ -653,7 +656,8 @@ __device__ __forceinline__ float activate(const VerifyArgs &a, float g, float u)
 // byte 32 (v % 4) + 16 (v / 4) + j, the FP8 operand's lane order.
 template <bool DOWN, bool MXA, int VPW>
 __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &d, int pw,
-                                            const f32x4 (&acc)[2 * VPW][kMB], const ItemBias (&bias)[VPW])
+                                            const f32x4 (&acc)[2 * VPW][kMB], const ItemBias (&bias)[VPW],
+                                            const int *tok = nullptr)
 {
     const VerifyArgs &a = P.a;
     const int lane = lane_id(), col = lane & 15, grp = lane >> 4;
@@ -726,9 +730,11 @@ __device__ __forceinline__ void finish_item(const FfnParams &P, const ItemDesc &
                 *reinterpret_cast<u32x2 *>(a.h + (size_t)p * a.d_ff + tile_row<DOWN>(d, v, 0) + 4 * grp) =
                     u32x2{h2[0], h2[1]};
             } else {
+                const int S = a.T * a.k;
+                const int row = p >= S ? p : S <= kMaxTokLds ? tok[p] : a.perm[p];
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
-                    *reinterpret_cast<f32x4 *>(a.o + (size_t)p * a.d + tile_row<DOWN>(d, v, t) + 4 * grp) =
+                    *reinterpret_cast<f32x4 *>(a.o + (size_t)row * a.d + tile_row<DOWN>(d, v, t) + 4 * grp) =
                         acc[2 * j + t][mb];
             }
         }
@@ -948,7 +954,7 @@ __device__ __forceinline__ long long contributors(const FfnParams &P, const Plan
 // Down launch: for the combine kernel, the output descriptor (split.hpp) of
 // every row of each item whose last unit lies in this range, so that every
 // row of every item is described by exactly one range on every launch.  A
-// whole item's row is its row of O; a cut item's row is the sum of its
+// whole item's row is its row of O (the row's slot); a cut item's row is the sum of its
 // contributors' parked partial sums, in workgroup order.  Descriptors are
 // indexed by the row's routed slot (the shared expert's rows by T*k + token).
 __device__ __forceinline__ void record_outputs(const FfnParams &P, const Plan &pl, const Split &sp, int x0, int x1)
@@ -966,7 +972,7 @@ __device__ __forceinline__ void record_outputs(const FfnParams &P, const Plan &p
         for (int r = threadIdx.x; r < M; r += kEThreads) {
             const int p = p0 + r;
             const int row = p >= S ? p : S <= kMaxTokLds ? sp.tok[p] : a.perm[p];
-            a.desc[(size_t)row * P.nbands + band] = whole ? split::out_whole((uint32_t)p) : split::out_with_row(cut, r);
+            a.desc[(size_t)row * P.nbands + band] = whole ? split::out_whole((uint32_t)row) : split::out_with_row(cut, r);
         }
     }
 }
@@ -1213,7 +1219,7 @@ void expert_ffn_kernel(FfnParams P)
         const int un = i + 1 < n ? unit_of(i + 1) : -1;
         if (u + 1 == cib + nsteps || un != u + 1) {
             if (cib >= x0 && cib + nsteps <= x1) {
-                finish_item<DOWN, MXA, kVPW>(P, cd, wave, acc, cbias);
+                finish_item<DOWN, MXA, kVPW>(P, cd, wave, acc, cbias, sp.tok);
             } else {
                 float *dst = P.partials + ((size_t)w * 2 + (cib <= x0 ? 0 : 1)) * P.slot_floats;
 #pragma unroll
@@ -1401,25 +1407,16 @@ __global__ __launch_bounds__(256) void plan_kernel(VerifyArgs a, int32_t *plan)
     if (threadIdx.x == 0) plan[0] = run;
 }
 
-// Expert output O[c .. c+3] of one row of the down launch, from the row's
-// output descriptor: its row of O if its item was whole, else the partial
-// sums of its contributors added in workgroup order (what a fix-up would have
-// stored).  Rows of items cut over more than three ranges take
-// expert_out_walk; here they read nothing and give zeros.
-__device__ __forceinline__ f32x4 expert_out(const FfnParams &D, uint64_t ds, int c)
+// A row of a down item cut over two or three ranges (descriptor kind 1): its
+// parked partial sums, all loads issued at once (absent ones read zeros) and
+// added in workgroup order.
+__device__ __forceinline__ f32x4 parked_sum(const FfnParams &D, uint64_t ds, int c)
 {
-    const int kind = split::out_kind(ds);
-    if (kind >= 2) return f32x4{0.f, 0.f, 0.f, 0.f};
-    // A whole item's O row, or up to three parked partial sums: all loads issued at once (absent
-    // ones read zeros) and added in workgroup order.
     const int off = split::out_row(ds) * D.band_rows + c % D.band_rows;  // partial_offset<true>
-    const int cnt = kind == 0 ? 0 : split::out_count(ds);
-    const rsrc_t ro = make_rsrc(D.a.o, (uint32_t)((size_t)(D.a.T * D.a.k + (D.a.sh_gate ? D.a.T : 0)) * D.a.d * 4));
+    const int cnt = split::out_count(ds);
     const rsrc_t rp = make_rsrc(D.partials, (uint32_t)((size_t)D.workers * 2 * D.slot_floats * 4));
     const uint32_t sf = (uint32_t)D.slot_floats;
-    const f32x4 v0 = __builtin_bit_cast(
-        f32x4, kind == 0 ? load16<0>(ro, (uint32_t)((size_t)split::out_pos(ds) * D.a.d + c) * 4u)
-                         : load16<0>(rp, ((uint32_t)split::out_slot(ds, 0) * sf + (uint32_t)off) * 4u));
+    const f32x4 v0 = __builtin_bit_cast(f32x4, load16<0>(rp, ((uint32_t)split::out_slot(ds, 0) * sf + (uint32_t)off) * 4u));
     const f32x4 v1 = __builtin_bit_cast(
         f32x4, load16<0>(rp, cnt > 1 ? ((uint32_t)split::out_slot(ds, 1) * sf + (uint32_t)off) * 4u : kOff));
     const f32x4 v2 = __builtin_bit_cast(
@@ -1488,40 +1485,48 @@ __global__ __launch_bounds__(256) void combine_kernel(FfnParams D)
     const int band = c / D.band_rows;
     const int S = a.T * a.k;
     const bool sh = a.sh_gate != nullptr;
+    const rsrc_t ro = make_rsrc(a.o, (uint32_t)((size_t)(S + (sh ? a.T : 0)) * a.d * 4));
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f}, vsh = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int j0 = 0; j0 < a.k; j0 += CH) {
         const bool with_sh = sh && j0 == 0;
         int ej[CH];
         float wj[CH];
         uint64_t dj[CH];
-        f32x4 vj[CH];
+        f32x4 oj[CH], vj[CH];
         bool ok[CH];
+        // One round trip: the slots' experts, gate weights and descriptors, and their rows of O
+        // (a whole item's output; unused for a cut item's row).
 #pragma unroll
         for (int q = 0; q < CH; ++q) {
             const int slot = t * a.k + min(j0 + q, a.k - 1);
             ej[q] = a.topk_idx[slot];
             wj[q] = a.topk_w[slot];
             dj[q] = a.desc[(size_t)slot * D.nbands + band];
+            oj[q] = __builtin_bit_cast(f32x4, load16<0>(ro, (uint32_t)((size_t)slot * a.d + c) * 4u));
         }
         const uint64_t dsh = with_sh ? a.desc[(size_t)(S + t) * D.nbands + band] : 0ull;
+        const f32x4 osh = with_sh ? __builtin_bit_cast(f32x4, load16<0>(ro, (uint32_t)((size_t)(S + t) * a.d + c) * 4u))
+                                  : f32x4{0.f, 0.f, 0.f, 0.f};
         // vj[q] = O + b_down of slot q.  A slot whose expert lies outside [0, E) was never placed:
-        // it adds nothing and its (unwritten) descriptor is not used.  A slot whose item needs the
-        // walk holds b_down for now (its walk sum w is added as w + b below, the same operation as O + b).
+        // it adds nothing and its (unwritten) descriptor is not used.  A cut item's row is the sum
+        // of its parked partial sums (kind 1), or needs the walk (kinds 2, 3): it holds b_down for
+        // now (its walk sum w is added as w + b below, the same operation as O + b).
         uint32_t walk = 0;  // bit q: slot q's row needs the walk; bit CH: the shared expert's
 #pragma unroll
         for (int q = 0; q < CH; ++q) {
             ok[q] = j0 + q < a.k && (unsigned)ej[q] < (unsigned)a.E;
-            const uint64_t dq = ok[q] ? dj[q] : split::out_whole(0u);
+            const int kind = ok[q] ? split::out_kind(dj[q]) : 0;
             const f32x4 b = a.b_down && ok[q] ? *reinterpret_cast<const f32x4 *>(a.b_down + (size_t)ej[q] * a.d + c)
                                               : f32x4{0.f, 0.f, 0.f, 0.f};
-            const f32x4 v = expert_out(D, dq, c);
-            const bool wk = split::out_kind(dq) >= 2;
+            const f32x4 v = kind == 0 ? oj[q] : kind == 1 ? parked_sum(D, dj[q], c) : f32x4{0.f, 0.f, 0.f, 0.f};
+            const bool wk = kind >= 2;
             vj[q] = a.b_down ? (wk ? b : v + b) : v;
             if (wk) walk |= 1u << q;
         }
         if (with_sh) {
-            vsh = expert_out(D, dsh, c);
-            if (split::out_kind(dsh) >= 2) walk |= 1u << CH;
+            const int kind = split::out_kind(dsh);
+            vsh = kind == 0 ? osh : kind == 1 ? parked_sum(D, dsh, c) : f32x4{0.f, 0.f, 0.f, 0.f};
+            if (kind >= 2) walk |= 1u << CH;
         }
         while (walk) {
             const int q = __builtin_ctz(walk);

@@ -98,7 +98,8 @@ constexpr long finished_item(long x0, long x1, long ns)
 
 // Where the combine kernel reads one row of a down item (an 8-byte output
 // descriptor, written by the range that holds the item's last unit):
-//   kind 0, whole item: bits 0-31 the row's grouped position p (its row of O);
+//   kind 0, whole item: bits 0-31 its row of O (the row's routed slot, or
+//     T * k + t for the shared expert's row of token t);
 //   kind 1, cut over two or three ranges: their slots (10 bits each, bits 0-29,
 //     in workgroup order), their count (bits 30-31) and the row r of the group
 //     (bits 32-37), the row's place in each slot;
