@@ -105,6 +105,27 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
     return ((uint64_t)hi << 32) | lo;
 }
 
+// Inclusive sum over lanes 0..lane of a wavefront: the same DPP steps as the
+// maximum above (an inclusive scan within each row of 16 lanes, then the row
+// totals carried into the later rows), a few cycles each, where a ds_bpermute
+// shuffle waits on the LDS crossbar at every step.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_add_step(int v)
+{
+    return v + __builtin_amdgcn_update_dpp(0, v, CTRL, ROW_MASK, 0xf, false);
+}
+
+__device__ __forceinline__ int wave_inclusive_sum(int v)
+{
+    v = dpp_add_step<0x111, 0xf>(v);  // row_shr:1
+    v = dpp_add_step<0x112, 0xf>(v);  // row_shr:2
+    v = dpp_add_step<0x114, 0xf>(v);  // row_shr:4
+    v = dpp_add_step<0x118, 0xf>(v);  // row_shr:8: each row scanned
+    v = dpp_add_step<0x142, 0xa>(v);  // row_bcast:15: row 0's total into row 1, row 2's into row 3
+    v = dpp_add_step<0x143, 0xc>(v);  // row_bcast:31: lanes 0..31's total into rows 2 and 3
+    return v;
+}
+
 // fp32 -> bf16 bits, round to nearest even (NaN stays NaN).
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f)
 {
@@ -125,21 +146,11 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b)
 __device__ __forceinline__ int block_exclusive_scan(int v, int *wave_tot, int *total)
 {
     const int lane = lane_id(), wave = threadIdx.x / kWave, nwaves = blockDim.x / kWave;
-    int incl = v;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const int n = __shfl_up(incl, o, kWave);
-        if (lane >= o) incl += n;
-    }
+    const int incl = wave_inclusive_sum(v);
     if (lane == kWave - 1) wave_tot[wave] = incl;
     __syncthreads();
     if (wave == 0) {
-        int w = lane < nwaves ? wave_tot[lane] : 0;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-            const int n = __shfl_up(w, o, kWave);
-            if (lane >= o) w += n;
-        }
+        const int w = wave_inclusive_sum(lane < nwaves ? wave_tot[lane] : 0);
         if (lane < nwaves) wave_tot[lane] = w;  // inclusive wave prefix
     }
     __syncthreads();
@@ -155,30 +166,15 @@ __device__ __forceinline__ void block_exclusive_scan2(int v0, int v1, int *wave_
                                                       int &tot1)
 {
     const int lane = lane_id(), wave = threadIdx.x / kWave, nwaves = blockDim.x / kWave;
-    int a = v0, b = v1;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const int na = __shfl_up(a, o, kWave), nb = __shfl_up(b, o, kWave);
-        if (lane >= o) {
-            a += na;
-            b += nb;
-        }
-    }
+    const int a = wave_inclusive_sum(v0), b = wave_inclusive_sum(v1);
     if (lane == kWave - 1) {
         wave_tot[wave] = a;
         wave_tot[nwaves + wave] = b;
     }
     __syncthreads();
     if (wave == 0) {
-        int wa = lane < nwaves ? wave_tot[lane] : 0, wb = lane < nwaves ? wave_tot[nwaves + lane] : 0;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-            const int na = __shfl_up(wa, o, kWave), nb = __shfl_up(wb, o, kWave);
-            if (lane >= o) {
-                wa += na;
-                wb += nb;
-            }
-        }
+        const int wa = wave_inclusive_sum(lane < nwaves ? wave_tot[lane] : 0);
+        const int wb = wave_inclusive_sum(lane < nwaves ? wave_tot[nwaves + lane] : 0);
         if (lane < nwaves) {
             wave_tot[lane] = wa;  // inclusive wave prefixes
             wave_tot[nwaves + lane] = wb;
