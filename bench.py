@@ -45,7 +45,9 @@ KSTATS_FILES = {"ds": "profiles/verify_ds_fp8_T64_U32.kernel_stats.txt",
                 "gpt": "profiles/verify_gpt_mxfp4_T64_U32.kernel_stats.txt"}
 PMC_SUMMARY = {"ds": os.path.join(PROFILES, "expert_ffn_ds_fp8_T64_U32.pmc.txt"),
                "gpt": os.path.join(PROFILES, "expert_ffn_gpt_mxfp4_T64_U32.pmc.txt")}
-FFN_SOURCE = os.path.join(ROOT, "paper_2607_12696_amd", "csrc", "expert_ffn.hip")
+# The expert kernels' sources: the kernel file and the headers it includes.
+FFN_SOURCES = [os.path.join(ROOT, "paper_2607_12696_amd", "csrc", f)
+               for f in ("expert_ffn.hip", "device.hpp", "launch.hpp", "split.hpp")]
 GATEUP_FP8 = "expert_ffn_kernel<1, false"   # demangled-name prefix of the FP8 gate/up kernel
 SWEEP_WARMUP = 20                           # untimed steps before each sweep point (the GPU stays busy between points)
 COPY_BYTES = 1 << 30                         # calibration copy: reads and writes 1 GiB
@@ -67,7 +69,10 @@ def log(*a):
 
 
 def source_sha() -> str:
-    return hashlib.sha256(open(FFN_SOURCE, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in FFN_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def pct(v, q):
