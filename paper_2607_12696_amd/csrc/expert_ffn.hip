@@ -244,6 +244,8 @@ struct FfnParams {
     long long *ranges;    // [workers][2]: unit range [x0, x1) of each workgroup, written by the expert kernel
     long long *fix;       // gate/up only: [workers][4] fix-up record of each workgroup (see write_fix_record)
     const int32_t *plan;  // token groups when T > 64 (else null: one group per expert)
+    void *dn_sched;       // T <= 64: the down launch's schedule (DownSched), written by the gate/up launch
+    int dn_K;             // gate/up: the down launch's units per token group (bands x steps)
 };
 
 // Distinct experts of the call (+ the shared one) and the number of token groups.
@@ -538,6 +540,82 @@ __device__ __forceinline__ void build_bounds(Split &sp, int n_groups, long K, in
 __device__ __forceinline__ int owner_of(const Split &sp, int n_groups, long K, int W, long x)
 {
     return split::owner_of(sp.cw, n_groups, K, W, x);
+}
+
+// The down launch's schedule when every expert's tokens form one group (T <= 64): its token
+// groups are the gate/up launch's (the union members in order, then the shared expert) with the
+// same costs, so only the unit ranges differ (K is the down launch's).  Workgroup 0 of the gate/up
+// launch, which also writes the union, writes it before its first weight load; the down launch
+// then reads it in one round trip instead of rebuilding it from the union.
+constexpr int kSchedGroups = 1025;  // n_groups <= E + 1, E <= 1024
+struct DownSched {
+    long long bound[kMaxWorkers + 1];
+    int cw[kSchedGroups + 1], ge[kSchedGroups], gp0[kSchedGroups], gM[kSchedGroups];
+};
+
+__device__ __forceinline__ void write_down_sched(const FfnParams &P, const Plan &pl, const Split &sp)
+{
+    DownSched *ds = static_cast<DownSched *>(P.dn_sched);
+    const long K = P.dn_K;
+    const long long C = (long long)sp.cw[pl.n_groups] * K;
+    for (int v = threadIdx.x; v <= P.workers; v += kEThreads)
+        ds->bound[v] = first_unit(sp, pl.n_groups, K, P.workers, C * v);
+    for (int g = threadIdx.x; g <= pl.n_groups; g += kEThreads) {
+        ds->cw[g] = sp.cw[g];
+        if (g < pl.n_groups) {
+            ds->ge[g] = sp.ge[g];
+            ds->gp0[g] = sp.gp0[g];
+            ds->gM[g] = sp.gM[g];
+        }
+    }
+}
+
+// The down launch's side (whole workgroup): the schedule, the union size and the slots of the
+// grouped positions, every load issued before the first LDS store (one round trip; entries past
+// the launch's groups are read but not used).
+__device__ __forceinline__ Plan load_down_sched(const FfnParams &P, Split &sp)
+{
+    constexpr int kG = (kSchedGroups + 1 + kEThreads - 1) / kEThreads;
+    constexpr int kB = (kMaxWorkers + 1 + kEThreads - 1) / kEThreads;
+    const DownSched *ds = static_cast<const DownSched *>(P.dn_sched);
+    const VerifyArgs &a = P.a;
+    const int tid = threadIdx.x, S = a.T * a.k;
+    long long b[kB];
+    int cw[kG], ge[kG], gp0[kG], gM[kG];
+#pragma unroll
+    for (int j = 0; j < kB; ++j) {
+        const int v = j * kEThreads + tid;
+        b[j] = v <= P.workers ? ds->bound[v] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kG; ++j) {
+        const int g = j * kEThreads + tid;
+        const bool ok = g <= kSchedGroups;
+        cw[j] = ok ? ds->cw[g] : 0;
+        ge[j] = ok && g < kSchedGroups ? ds->ge[g] : 0;
+        gp0[j] = ok && g < kSchedGroups ? ds->gp0[g] : 0;
+        gM[j] = ok && g < kSchedGroups ? ds->gM[g] : 0;
+    }
+    const Plan pl = load_plan(P);
+    if (S <= kMaxTokLds)
+        for (int p = tid; p < S; p += kEThreads) sp.tok[p] = a.perm[p];
+#pragma unroll
+    for (int j = 0; j < kB; ++j) {
+        const int v = j * kEThreads + tid;
+        if (v <= P.workers) sp.bound[v] = b[j];
+    }
+#pragma unroll
+    for (int j = 0; j < kG; ++j) {
+        const int g = j * kEThreads + tid;
+        if (g <= pl.n_groups) sp.cw[g] = cw[j];
+        if (g < pl.n_groups) {
+            sp.ge[g] = ge[j];
+            sp.gp0[g] = gp0[j];
+            sp.gM[g] = gM[j];
+        }
+    }
+    __syncthreads();
+    return pl;
 }
 
 // What a workgroup needs to know about one item.
@@ -1038,9 +1116,12 @@ void expert_ffn_kernel(FfnParams P)
     const int nsteps = P.nsteps, K = P.K;
     __shared__ Split sp;
     static_assert(NT * BBUF >= kPW * 1024 * 4, "the union's scratch fits the activation tiles");
+    const bool sched_in = DOWN && P.dn_sched != nullptr && P.plan == nullptr;
     const Plan pl = !DOWN && P.plan == nullptr ? union_and_costs<FMT, MXA>(P, sp, reinterpret_cast<int *>(lds))
+                  : sched_in                   ? load_down_sched(P, sp)
                                                : build_costs<FMT, MXA, DOWN>(P, sp);
-    build_bounds(sp, pl.n_groups, (long)P.nbands * nsteps, P.workers);
+    if (!sched_in) build_bounds(sp, pl.n_groups, (long)P.nbands * nsteps, P.workers);
+    if (!DOWN && P.dn_sched != nullptr && P.plan == nullptr && blockIdx.x == 0) write_down_sched(P, pl, sp);
     // Unit indices fit in 32 bits (fewer than 2^30 units: every matrix is below 2^31 bytes and a
     // launch has at most 4096 token groups), so the unit arithmetic below is 32-bit.
     const int x0 = (int)sp.bound[w], x1 = (int)sp.bound[w + 1];
@@ -1666,6 +1747,14 @@ static hipError_t launch_fmt(const VerifyArgs &args, uint8_t *ws_base, const Ver
     g.ranges = reinterpret_cast<long long *>(partials + (size_t)G * 2 * ws.slot_floats);
     g.fix = g.ranges + (size_t)G * 2;
     g.plan = grouped ? plan : nullptr;
+    // Without a plan the (unused) plan region holds the down launch's schedule.
+    static_assert(sizeof(DownSched) <= (8 + 2 * (size_t)kMaxGroups + 1026) * 4, "the down schedule fits the plan region");
+    g.dn_sched = grouped ? nullptr : static_cast<void *>(plan);
+    {
+        const int dn_nsteps = ((a.d_ff + kMacroK - 1) / kMacroK + SB - 1) / SB;
+        const int dn_nbands = (a.d + 32 * kWG - 1) / (32 * kWG);
+        g.dn_K = dn_nbands * dn_nsteps;
+    }
     hipLaunchKernelGGL((expert_ffn_kernel<FMT, false, PD, MXA>), dim3(G), dim3(kEThreads), 0, stream, g);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = mark(events, 1, stream)) != hipSuccess) return err;
