@@ -628,7 +628,7 @@ class Stack:
 
 # --------------------------------------------------------------------------- profiler summaries
 
-def summarize_kstats(kt_dir, out_path, shape="ds", last=50):
+def summarize_kstats(kt_dir, out_path, shape="ds", last=50, T=64, U=32):
     """The library's kernels of a `rocprofv3 --kernel-trace --stats` run of `bench.py --profile`: duration
     statistics over the last `last` dispatches of each kernel (the timed steps, after the warm-up)."""
     paths = glob.glob(os.path.join(kt_dir, "**", "*kernel_trace.csv"), recursive=True)
@@ -645,14 +645,17 @@ def summarize_kstats(kt_dir, out_path, shape="ds", last=50):
         d = [(e - b) / 1e3 for b, e in v[-last:]]
         rows.append((n, len(v), len(d), sum(d) / len(d), min(d), max(d)))
     rows.sort(key=lambda r: -r[3] * r[2])
-    name = {"ds": "DeepSeek-V3.1-shaped FP8 layer, T=64 draft tokens routed to U=32 of 256 experts + 1 shared",
-            "gpt": "GPT-OSS-120B-shaped MXFP4 layer, T=64 draft tokens routed to U=32 of 128 experts"}[shape]
+    name = {"ds": f"DeepSeek-V3.1-shaped FP8 layer, T={T} draft tokens routed to U={U} of 256 experts + 1 shared",
+            "gpt": f"GPT-OSS-120B-shaped MXFP4 layer, T={T} draft tokens routed to U={U} of 128 experts"}[shape]
+    tu = "" if (T, U) == (64, 32) else f" --T {T} --U {U}"
+    out_name = KSTATS_FILES[shape] if (T, U) == (64, 32) else out_path
     with open(out_path, "w") as f:
         f.write(f"# rocprofv3 kernel-trace statistics of the verification pass: {name}\n")
         f.write(f"# (bench.py --profile: 100 warm-up steps, then 50; statistics over the last {last} dispatches of\n")
         f.write("# each kernel, i.e. the 50 steps after the warm-up).\n# commands (repository root, TMPDIR=/tmp):\n")
-        f.write(f"#   rocprofv3 --kernel-trace --stats -d KT_DIR --output-format csv -- python3 bench.py --profile --shape {shape}\n")
-        f.write(f"#   python3 bench.py --summarize-kstats KT_DIR {KSTATS_FILES[shape]} --shape {shape}\n")
+        f.write("#   rocprofv3 --kernel-trace --stats -d KT_DIR --output-format csv -- python3 bench.py --profile "
+                f"--shape {shape}{tu}\n")
+        f.write(f"#   python3 bench.py --summarize-kstats KT_DIR {out_name} --shape {shape}{tu}\n")
         f.write("# rows: this library's kernels of the steps (weight packing and input generation omitted)\n")
         f.write(f"kernel_source_sha: {source_sha()}\n")
         f.write("# kernel | dispatches (summarised) | average us | min us | max us\n")
@@ -813,7 +816,7 @@ def main():
     args = ap.parse_args()
 
     if args.summarize_kstats:
-        summarize_kstats(*args.summarize_kstats, args.shape)
+        summarize_kstats(*args.summarize_kstats, args.shape, T=args.T, U=args.U)
         return 0
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.shape)
